@@ -1,0 +1,216 @@
+/*
+ * grpo.h -- C ABI of libgrpo, the MI355X (gfx950) GRPO scoring + loss library.
+ *
+ * The library computes, for every sampled rollout token, the policy
+ * log-probability under an LM head and the GRPO objective of AutoTriton
+ * (Sec. 3.3, Eq. 1 with the group advantage of Eq. 2), together with the
+ * gradients of the loss with respect to the final hidden states and the
+ * LM-head weight, without ever storing the N x V logits.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every array argument is caller-owned, contiguous DEVICE memory unless
+ *    stated otherwise. The library never allocates or frees device memory:
+ *    temporary storage is the caller's workspace, sized by
+ *    grpo_workspace_bytes().
+ *  - Work is enqueued on `stream` (NULL = the legacy default stream) and is
+ *    asynchronous; no call synchronises except grpo_check_error().
+ *  - Arguments are validated on the host before anything is launched. On
+ *    error nothing is enqueued and a nonzero grpo_status is returned.
+ *    No C++ exception crosses this interface.
+ *  - Errors that depend on device data (a token id outside [0, V), a
+ *    malformed cu_seqlens) cannot be seen on the host. Kernels then record
+ *    a flag in the workspace and skip the offending item instead of
+ *    trapping; grpo_check_error() reads the flag back.
+ *  - Layouts are row-major: hidden [N, H], weight [V, H] (the nn.Linear
+ *    layout, one row per vocabulary entry), grad_hidden [N, H],
+ *    grad_weight [V, H].
+ *  - A "row" is one token position. Rollout b owns rows
+ *    cu_seqlens[b] .. cu_seqlens[b+1]-1; a padded batch of B rollouts of
+ *    length T uses cu_seqlens[b] = b*T. A row takes part iff its mask byte
+ *    is nonzero (mask == NULL: every row). Outputs of masked rows are 0.
+ *  - Calls on distinct streams are thread-safe. Calls that share a
+ *    workspace must be ordered by the caller.
+ */
+#ifndef GRPO_H_
+#define GRPO_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* hipStream_t;
+
+typedef enum grpo_status {
+  GRPO_OK = 0,
+  GRPO_ERR_NULL = 1,        /* a required pointer is NULL */
+  GRPO_ERR_SHAPE = 2,       /* a size is out of range or inconsistent */
+  GRPO_ERR_DTYPE = 3,       /* unknown or unsupported dtype */
+  GRPO_ERR_PARAM = 4,       /* a hyper-parameter is out of range */
+  GRPO_ERR_ALIGN = 5,       /* a pointer lacks the required alignment */
+  GRPO_ERR_WORKSPACE = 6,   /* workspace NULL, misaligned or too small */
+  GRPO_ERR_DEVICE = 7,      /* no usable gfx950 device */
+  GRPO_ERR_HIP = 8,         /* a HIP runtime call failed */
+  GRPO_ERR_TOKEN_RANGE = 9, /* (device) a token id was outside [0, V) */
+  GRPO_ERR_SEQLENS = 10     /* (device) cu_seqlens not monotone from 0 to N */
+} grpo_status;
+
+typedef enum grpo_dtype {
+  GRPO_F32 = 0, /* IEEE binary32 */
+  GRPO_BF16 = 1 /* bfloat16; fp32 accumulation, round-to-nearest-even stores */
+} grpo_dtype;
+
+/* How the per-token terms of Eq. 1 are averaged into the loss. */
+typedef enum grpo_agg {
+  /* Eq. 1 as written: mean over the tokens of each rollout (1/|o_i|), then
+   * mean over all B = P*G rollouts. Weight of a token of rollout b is
+   * 1 / (B * |o_b|); an empty rollout adds 0 but still counts in B. */
+  GRPO_AGG_SEQ_MEAN = 0,
+  /* One global mean over all valid tokens: weight 1 / sum_b |o_b|. */
+  GRPO_AGG_TOKEN_MEAN = 1
+} grpo_agg;
+
+/* Operation selector for grpo_workspace_bytes(). */
+typedef enum grpo_op {
+  GRPO_OP_LOGPROB_FWD = 0,
+  GRPO_OP_LOSS_FWD_BWD = 1
+} grpo_op;
+
+/*
+ * group_advantages -- Eq. 2 of AutoTriton Sec. 3.3: the advantage of
+ * rollout i of a prompt is (r_i - mean) / (std + std_eps), where mean and
+ * std are taken over the G = group_size rollouts of the same prompt (the
+ * paper's set {o_i}, i = 1..G, that the rollouts are sampled as). The paper
+ * fixes neither the std convention nor an epsilon: unbiased_std != 0 selects
+ * the (G-1) estimate, 0 the population one. If all G rewards of a group are
+ * equal the advantages are exactly 0.
+ *
+ *   rewards  [num_prompts * group_size] fp32, prompt-major (the G rollouts
+ *            of one prompt contiguous). Device.
+ *   adv      [num_prompts * group_size] fp32 output, same order. Device.
+ * Requires num_prompts >= 1, group_size >= 2, std_eps >= 0 (and finite).
+ * Computed in fp32 with a fixed reduction order (bitwise reproducible).
+ */
+grpo_status group_advantages(const float* rewards, int64_t num_prompts, int32_t group_size,
+                             float std_eps, int32_t unbiased_std, float* adv,
+                             hipStream_t stream);
+
+/*
+ * grpo_pack_valid -- the token counts |o_b| of Eq. 1 and the compacted list
+ * of rows that take part (mask set), in increasing row order.
+ *
+ *   mask        [N] uint8, or NULL (every row valid). Device.
+ *   cu_seqlens  [num_seqs + 1] int64 row offsets, cu[0] = 0, cu[B] = N,
+ *               non-decreasing. Device.
+ *   rows        [N] int32 output: the first *num_valid entries are the valid
+ *               rows; the rest are left unspecified. Device.
+ *   counts      [num_seqs] int32 output: |o_b|. Device.
+ *   num_valid   [1] int32 output. Device.
+ *   workspace   at least grpo_workspace_bytes(GRPO_OP_LOGPROB_FWD, ...) for
+ *               the same N (only its small header is used). Device.
+ * Integer results are exact. Requires 1 <= N < 2^31.
+ */
+grpo_status grpo_pack_valid(const uint8_t* mask, const int64_t* cu_seqlens, int64_t num_seqs,
+                            int64_t N, int32_t* rows, int32_t* counts, int32_t* num_valid,
+                            void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * grpo_logprob_fwd -- the policy probability inside the ratio of Eq. 1,
+ * pi_theta(o_t | q, o_<t): for each valid row t,
+ *   z_{t,v} = <hidden_t, weight_v>              (all v in [0, V))
+ *   lse_t   = log sum_v exp z_{t,v}
+ *   logp_t  = z_{t, tokens_t} - lse_t
+ * The logits are reduced tile by tile (online max / sum-exp) and never
+ * stored.
+ *
+ *   dt        GRPO_BF16 (hidden, weight bf16; MFMA, fp32 accumulation) or
+ *             GRPO_F32 (fp32 throughout).
+ *   hidden    [N, H] dt. Device.       weight [V, H] dt. Device.
+ *   tokens    [N] int64 sampled ids.   mask   [N] uint8 or NULL.
+ *   logp, lse [N] fp32 outputs (0 on masked rows). Either may be NULL.
+ *   workspace >= grpo_workspace_bytes(GRPO_OP_LOGPROB_FWD, dt, N, H, V, 1),
+ *             256-byte aligned.
+ * Requires N, H, V >= 1, N < 2^31, V < 2^31; bf16 also needs H % 8 == 0 and
+ * 16-byte aligned hidden/weight.
+ */
+grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weight,
+                             const int64_t* tokens, const uint8_t* mask, int64_t N, int64_t H,
+                             int64_t V, float* logp, float* lse, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * grpo_loss_fwd_bwd -- loss = -J of Eq. 1 (AutoTriton Sec. 3.3) and its
+ * gradients. For each valid row t of rollout b, with logp_t as in
+ * grpo_logprob_fwd:
+ *   rho   = exp(logp_t - old_logp_t)                       (pi_theta / pi_theta_old)
+ *   pg    = -min(rho * A_b, clip(rho, 1-clip_eps, 1+clip_eps) * A_b)
+ *   kl    = exp(ref_logp_t - logp_t) - (ref_logp_t - logp_t) - 1      (k3 estimator)
+ *   ell_t = pg + beta * kl
+ *   loss  = sum_b c_b * sum_{valid t in b} ell_t     (c_b from `agg`, see grpo_agg)
+ * and the exact gradients dL/dhidden, dL/dweight through the log-softmax.
+ * A tie rho*A == clip(rho)*A takes the unclipped branch; the clipped branch
+ * has zero slope.
+ *
+ *   dt, hidden, weight, tokens, mask, N, H, V   as grpo_logprob_fwd.
+ *   cu_seqlens [num_seqs + 1] int64. Device.
+ *   old_logp   [N] fp32: log pi_theta_old of each row. Device.
+ *   ref_logp   [N] fp32: log pi_ref of each row; may be NULL iff beta == 0.
+ *   adv        [num_seqs] fp32: A_b (e.g. from group_advantages). Device.
+ *   clip_eps   in (0, 1); beta >= 0.
+ *   lse_in     [N] fp32 or NULL: the row's log-sum-exp from an earlier
+ *              grpo_logprob_fwd on the same hidden/weight; when given, the
+ *              forward vocabulary pass is skipped.
+ * Outputs (device, any may be NULL except loss):
+ *   loss        [1] fp32, reduced in a fixed order (bitwise reproducible).
+ *   logp_out, lse_out, token_loss (ell_t), dlogp (dL/dlogp_t)  [N] fp32.
+ *   clip_flag   [N] uint8: 1 where the clipped branch was taken.
+ *   grad_hidden [N, H] of grad_hidden_dt (GRPO_F32 or GRPO_BF16; bf16 needs
+ *               dt == GRPO_BF16). Zero rows where masked.
+ *   grad_weight [V, H] fp32: overwritten, or added to when
+ *               accumulate_grad_weight != 0.
+ * workspace >= grpo_workspace_bytes(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, num_seqs).
+ */
+grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight,
+                              const int64_t* tokens, const uint8_t* mask,
+                              const int64_t* cu_seqlens, int64_t num_seqs, int64_t N, int64_t H,
+                              int64_t V, const float* old_logp, const float* ref_logp,
+                              const float* adv, float clip_eps, float beta, grpo_agg agg,
+                              const float* lse_in, float* loss, float* logp_out, float* lse_out,
+                              float* token_loss, float* dlogp, uint8_t* clip_flag,
+                              void* grad_hidden, grpo_dtype grad_hidden_dt, float* grad_weight,
+                              int32_t accumulate_grad_weight, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of workspace an operation needs for these sizes (0 if the sizes are
+ * invalid). For GRPO_OP_LOGPROB_FWD pass num_seqs = 1. Host only. */
+size_t grpo_workspace_bytes(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V,
+                            int64_t num_seqs);
+
+/* Synchronises `stream`, then reads and clears the device error flag kept in
+ * the workspace. Returns GRPO_OK, GRPO_ERR_TOKEN_RANGE or GRPO_ERR_SEQLENS
+ * (or GRPO_ERR_HIP if a copy fails). */
+grpo_status grpo_check_error(void* workspace, hipStream_t stream);
+
+/* Static description of a status code. Never NULL. */
+const char* grpo_status_string(grpo_status status);
+
+/*
+ * Kernel timing (for benchmarks). When enabled, every kernel launch is
+ * bracketed by a pair of HIP events recorded on the launch stream, and
+ * grpo_profile_query() reports, per kernel kind, the launch count and the
+ * summed event time. Querying synchronises the recorded events. Disabled by
+ * default; enabling costs two event records per launch.
+ */
+void grpo_profile_enable(int32_t on);
+void grpo_profile_reset(void);
+int32_t grpo_profile_num_kinds(void);
+const char* grpo_profile_kind_name(int32_t kind);
+grpo_status grpo_profile_query(int32_t kind, int64_t* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GRPO_H_ */

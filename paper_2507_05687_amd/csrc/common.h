@@ -1,0 +1,39 @@
+// Shared device/host definitions of libgrpo (internal; not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace grpo {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Workspace header (first 256 bytes of every workspace). Each error kind has
+// its own word so that kernels can raise it with a plain store.
+struct WsHeader {
+  int32_t err_token;    // nonzero: some valid row had a token id outside [0, V)
+  int32_t err_seqlens;  // nonzero: cu_seqlens was not monotone from 0 to N
+  int32_t num_valid;    // number of valid rows after packing
+  int32_t pad_[61];
+};
+
+constexpr int kTile = 256;  // GEMM tile edge (rows and columns)
+constexpr int kBK = 64;     // GEMM K step
+
+__host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+__host__ __device__ inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
+
+// fp32 -> bf16 bits, round to nearest even (finite and infinite inputs; NaN stays NaN).
+__device__ inline uint16_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (uint16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+__device__ inline float bf16_bits_to_f32(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+
+}  // namespace grpo

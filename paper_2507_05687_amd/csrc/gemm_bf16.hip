@@ -1,0 +1,341 @@
+// bf16 MFMA contraction C[m, n] = sum_k A[m, k] * B[n, k] for gfx950, with
+// fused epilogues for the three uses on the GRPO path:
+//
+//   EpiLse   forward scoring: A = LM-head rows (vocabulary), B = hidden rows
+//            (tokens). Reduces each token column of the 256x256 tile to an
+//            online (max, sum-exp) partial and picks out z at the sampled id.
+//   EpiDz    backward: the same tile recomputed, turned into
+//            dz = g * (1[v = y] - exp(z - lse)) and stored in bf16 both
+//            token-major and vocabulary-major.
+//   EpiStore dL/dh = dz . W and dL/dW = dz^T . h: fp32 stores, optionally
+//            accumulating, gathering output rows, or converting to bf16.
+//
+// Tiling: one 256-thread workgroup (4 waves of 64) per 256x256 output tile;
+// each wave owns a 128x128 quarter as a 4x4 grid of 32x32x16 bf16 MFMA
+// blocks (256 fp32 accumulators per lane). K advances 64 at a time through a
+// double-buffered LDS stage of 2 x (256x64 A + 256x64 B) bf16 = 128 KiB.
+// LDS rows are 128 bytes; the eight 16-byte chunks of a row are XOR-swizzled
+// by a few row bits so that the MFMA fragment reads hit distinct banks.
+//
+// Tile order: workgroup ids are dealt round-robin to the 8 XCDs, so id
+// b runs on XCD b % 8. Tiles are assigned so that each XCD owns a band of
+// kGM tile-rows and walks the tile-columns in blocks of kGN, and all 8 XCDs
+// walk the same columns at the same time: the B operand is then shared
+// through the last-level cache and each XCD's L2 sees only kGM + kGN
+// distinct operand slices per K step.
+#include "kernels.h"
+
+namespace grpo {
+
+constexpr int kGM = 4;  // tile-rows per XCD band
+constexpr int kGN = 8;  // tile-columns per step of the walk
+constexpr int kLdsStage = 2 * kTile * kBK * 2;  // bytes of one A+B stage (64 KiB)
+
+#ifndef GRPO_SWZ_SHIFT
+#define GRPO_SWZ_SHIFT 1
+#endif
+
+__device__ inline int swz(int row) { return (row >> GRPO_SWZ_SHIFT) & 7; }
+
+// Maps a workgroup id to its (tile_m, tile_n); returns false for the
+// padding workgroups of the last band.
+__device__ inline bool tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+  int xcd = bid & 7, loc = bid >> 3;
+  int per_band = kGM * tiles_n;
+  int band = loc / per_band;
+  int r = loc - band * per_band;
+  int nb = r / (kGM * kGN);
+  int r2 = r - nb * (kGM * kGN);
+  tm = band * (8 * kGM) + xcd * kGM + r2 % kGM;
+  tn = nb * kGN + r2 / kGM;
+  return tm < tiles_m;
+}
+
+int gemm_grid(int tiles_m, int tiles_n) {
+  int bands = (int)ceil_div(tiles_m, 8 * kGM);
+  return bands * 8 * kGM * tiles_n;
+}
+
+// ------------------------------------------------------------ epilogues
+struct Frag {
+  int tm, tn, wm, wn, lane;
+  // row (within the 256x256 tile) of accumulator register r of block mi
+  __device__ int row(int mi, int r) const {
+    return wm * 128 + mi * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+  }
+  __device__ int col(int ni) const { return wn * 128 + ni * 32 + (lane & 31); }
+};
+
+struct EpiLse {
+  const int32_t* y_p;  // sampled id of each packed token
+  float* zy;           // z at the sampled id, per packed token
+  float2* ms;          // [tiles_m][ldms] partial (max, sum-exp)
+  int64_t ldms;
+  int64_t V;
+
+  __device__ void operator()(f32x16 (&acc)[4][4], const Frag& f, int m_valid, int n_valid,
+                             char* smem) const {
+    float pm[4], ps[4];
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni) {
+      int64_t t = (int64_t)f.tn * kTile + f.col(ni);
+      int y = t < n_valid ? y_p[t] : -1;
+      float m = -INFINITY;
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          int64_t v = (int64_t)f.tm * kTile + f.row(mi, r);
+          if (v < V) m = fmaxf(m, acc[mi][ni][r]);
+        }
+      float s = 0.f;
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          int64_t v = (int64_t)f.tm * kTile + f.row(mi, r);
+          if (v < V) s += __expf(acc[mi][ni][r] - m);
+          if (v == y) zy[t] = acc[mi][ni][r];
+        }
+      // merge with the lane holding the other 64 rows of this column
+      float m2 = __shfl_xor(m, 32, 64), s2 = __shfl_xor(s, 32, 64);
+      float mm = fmaxf(m, m2);
+      float sm = (s == 0.f ? 0.f : s * __expf(m - mm)) + (s2 == 0.f ? 0.f : s2 * __expf(m2 - mm));
+      pm[ni] = mm;
+      ps[ni] = sm;
+    }
+    // merge the two waves that share these columns (wm = 0 and 1)
+    float2* xch = (float2*)smem;  // [2 (wn)][128]
+    if (f.wm == 1 && f.lane < 32) {
+#pragma unroll
+      for (int ni = 0; ni < 4; ++ni) xch[f.wn * 128 + ni * 32 + f.lane] = make_float2(pm[ni], ps[ni]);
+    }
+    __syncthreads();
+    if (f.wm == 0 && f.lane < 32) {
+#pragma unroll
+      for (int ni = 0; ni < 4; ++ni) {
+        float2 o = xch[f.wn * 128 + ni * 32 + f.lane];
+        float mm = fmaxf(pm[ni], o.x);
+        float sm = (ps[ni] == 0.f ? 0.f : ps[ni] * __expf(pm[ni] - mm)) +
+                   (o.y == 0.f ? 0.f : o.y * __expf(o.x - mm));
+        int64_t t = (int64_t)f.tn * kTile + f.col(ni);
+        if (t < n_valid) ms[(int64_t)f.tm * ldms + t] = make_float2(mm, sm);
+      }
+    }
+  }
+};
+
+struct EpiDz {
+  const int32_t* y_p;
+  const float* lse_p;
+  const float* g_p;
+  uint16_t* dz;   // [tokens][lddz], columns = chunk-local vocabulary rows
+  int64_t lddz;
+  uint16_t* dzT;  // [chunk rows][lddzT], columns = tokens (may be NULL)
+  int64_t lddzT;
+  int64_t V;      // vocabulary size
+  int64_t v0;     // first vocabulary row of this chunk
+
+  __device__ void operator()(f32x16 (&acc)[4][4], const Frag& f, int m_valid, int n_valid,
+                             char*) const {
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni) {
+      int64_t t = (int64_t)f.tn * kTile + f.col(ni);
+      bool tv = t < n_valid;
+      int y = tv ? y_p[t] : -1;
+      float l = tv ? lse_p[t] : 0.f;
+      float g = tv ? g_p[t] : 0.f;
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          uint16_t b[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            int r = q * 4 + e;
+            int vl = f.tm * kTile + f.row(mi, r);
+            int64_t v = v0 + vl;
+            float d = 0.f;
+            if (tv && v < V) d = g * ((v == y ? 1.f : 0.f) - __expf(acc[mi][ni][r] - l));
+            b[e] = f32_to_bf16_bits(d);
+            if (dzT) dzT[(int64_t)vl * lddzT + t] = b[e];
+          }
+          int vl0 = f.tm * kTile + f.row(mi, q * 4);
+          uint2 pk = make_uint2((uint32_t)b[0] | ((uint32_t)b[1] << 16),
+                                (uint32_t)b[2] | ((uint32_t)b[3] << 16));
+          *(uint2*)(dz + t * lddz + vl0) = pk;
+        }
+    }
+  }
+};
+
+struct EpiStore {
+  float* acc_buf;        // fp32 accumulation buffer [M][ld_acc] (tile-local rows)
+  int64_t ld_acc;
+  int read_acc;          // add the buffer's current value
+  void* out;             // final output (NULL: write acc_buf instead)
+  int64_t ld_out;
+  int out_bf16;
+  int add_out;           // add the output's current value (fp32 output only)
+  const int32_t* out_rows;  // output row = out_rows[m] (NULL: m)
+  int64_t m_limit;       // rows >= m_limit are not stored (static bound)
+  int64_t n_limit;       // columns >= n_limit are not stored
+
+  __device__ void operator()(f32x16 (&acc)[4][4], const Frag& f, int m_valid, int n_valid,
+                             char*) const {
+    int64_t mlim = m_limit < m_valid ? m_limit : m_valid;
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        int64_t m = (int64_t)f.tm * kTile + f.row(mi, r);
+        if (m >= mlim) continue;
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni) {
+          int64_t n = (int64_t)f.tn * kTile + f.col(ni);
+          if (n >= n_limit) continue;
+          float x = acc[mi][ni][r];
+          if (read_acc) x += acc_buf[m * ld_acc + n];
+          if (out == nullptr) {
+            acc_buf[m * ld_acc + n] = x;
+          } else {
+            int64_t orow = out_rows ? (int64_t)out_rows[m] : m;
+            if (out_bf16) {
+              ((uint16_t*)out)[orow * ld_out + n] = f32_to_bf16_bits(x);
+            } else {
+              float* o = (float*)out + orow * ld_out + n;
+              *o = add_out ? *o + x : x;
+            }
+          }
+        }
+      }
+  }
+};
+
+// ------------------------------------------------------------ main loop
+template <class Epi, bool KTAIL>
+__global__ void __launch_bounds__(256, 1) k_gemm_bf16(GemmArgs g, Epi epi) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * kLdsStage];
+  int tm, tn;
+  if (!tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn)) return;
+  int m_valid = g.m_dev ? min(*g.m_dev, g.M) : g.M;
+  int n_valid = g.n_dev ? min(*g.n_dev, g.N) : g.N;
+  if (tm * kTile >= m_valid || tn * kTile >= n_valid) return;
+  int K = g.k_dev ? (int)round_up(*g.k_dev, kBK) : g.K;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const int wm = w & 1, wn = w >> 1;
+
+  // ---- global -> LDS loader: thread owns rows (tid/8 + 32j), chunk tid%8
+  const int lrow = tid >> 3, lch = tid & 7;
+  const uint16_t* pa[8];
+  const uint16_t* pb[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    int ra = min(tm * kTile + lrow + 32 * j, m_valid - 1);
+    pa[j] = g.A + (int64_t)ra * g.lda + lch * 8;
+    int rb = min(tn * kTile + lrow + 32 * j, n_valid - 1);
+    if (g.b_rows) rb = g.b_rows[rb];
+    pb[j] = g.B + (int64_t)rb * g.ldb + lch * 8;
+  }
+  const int st_off = lrow * 128 + ((lch ^ swz(lrow)) << 4);  // + 32j*128
+
+  // ---- fragment reads: lane reads row (l%32) of each 32-row block, chunk 2s + l/32
+  const int fr = lane & 31;
+  const int rd_base_a = (wm * 128 + fr) * 128;
+  const int rd_base_b = kTile * kBK * 2 + (wn * 128 + fr) * 128;
+  int rd_ch[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) rd_ch[s] = ((2 * s + (lane >> 5)) ^ swz(fr)) << 4;
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  u32x4 ra_[8], rb_[8];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (KTAIL && k0 + lch * 8 >= K) {
+        ra_[j] = u32x4{0, 0, 0, 0};
+        rb_[j] = u32x4{0, 0, 0, 0};
+      } else {
+        ra_[j] = *(const u32x4*)(pa[j] + k0);
+        rb_[j] = *(const u32x4*)(pb[j] + k0);
+      }
+    }
+  };
+  auto lstore = [&](int buf) {
+    char* base = smem + buf * kLdsStage;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      *(u32x4*)(base + st_off + j * 32 * 128) = ra_[j];
+      *(u32x4*)(base + kTile * kBK * 2 + st_off + j * 32 * 128) = rb_[j];
+    }
+  };
+
+  const int nk = K / kBK + ((KTAIL && K % kBK) ? 1 : 0);
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) gload((kt + 1) * kBK);
+    const char* base = smem + buf * kLdsStage;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      bf16x8 a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[i] = *(const bf16x8*)(base + rd_base_a + i * 32 * 128 + rd_ch[s]);
+        b[i] = *(const bf16x8*)(base + rd_base_b + i * 32 * 128 + rd_ch[s]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) lstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  Frag f{tm, tn, wm, wn, lane};
+  epi(acc, f, m_valid, n_valid, smem);
+}
+
+template <class Epi>
+static void launch_gemm(const GemmArgs& g, const Epi& e, hipStream_t s) {
+  int grid = gemm_grid(g.tiles_m, g.tiles_n);
+  bool ktail = (g.k_dev == nullptr) && (g.K % kBK != 0);
+  if (ktail)
+    hipLaunchKernelGGL((k_gemm_bf16<Epi, true>), dim3(grid), dim3(256), 0, s, g, e);
+  else
+    hipLaunchKernelGGL((k_gemm_bf16<Epi, false>), dim3(grid), dim3(256), 0, s, g, e);
+}
+
+void launch_gemm_lse(const GemmArgs& g, const int32_t* y_p, float* zy, float2* ms, int64_t ldms,
+                     int64_t V, hipStream_t s) {
+  EpiLse e{y_p, zy, ms, ldms, V};
+  launch_gemm(g, e, s);
+}
+
+void launch_gemm_dz(const GemmArgs& g, const int32_t* y_p, const float* lse_p, const float* g_p,
+                    uint16_t* dz, int64_t lddz, uint16_t* dzT, int64_t lddzT, int64_t V,
+                    int64_t v0, hipStream_t s) {
+  EpiDz e{y_p, lse_p, g_p, dz, lddz, dzT, lddzT, V, v0};
+  launch_gemm(g, e, s);
+}
+
+void launch_gemm_store(const GemmArgs& g, const StoreArgs& a, hipStream_t s) {
+  EpiStore e{a.acc_buf, a.ld_acc, a.read_acc, a.out, a.ld_out, a.out_bf16, a.add_out,
+             a.out_rows, a.m_limit, a.n_limit};
+  launch_gemm(g, e, s);
+}
+
+}  // namespace grpo

@@ -1,0 +1,559 @@
+// Host side of libgrpo: argument validation, workspace layout, the launch
+// sequence of each entry point, and optional per-kernel event timing.
+// Declarations and argument contracts are in include/grpo.h.
+#include "grpo.h"
+
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+#include <vector>
+
+#include "kernels.h"
+
+using namespace grpo;
+
+namespace {
+
+// --------------------------------------------------------- kernel timing
+enum Kind {
+  K_PACK, K_ADV, K_GEMM_LSE, K_LSE_FIN, K_TOKEN, K_TRANSPOSE, K_GEMM_DZ, K_GEMM_DH, K_GEMM_DW,
+  K_F32_SCORE, K_F32_DH, K_F32_DW, K_ZERO_ROWS, K_GATHER_DOT, K_NUM_KINDS
+};
+const char* kKindNames[K_NUM_KINDS] = {
+    "pack_valid",  "group_advantages", "gemm_logits_lse", "lse_finalize",   "token_objective",
+    "transpose",   "gemm_recompute_dz", "gemm_grad_hidden", "gemm_grad_weight", "f32_score",
+    "f32_grad_hidden", "f32_grad_weight", "zero_masked_rows", "gather_dot"};
+
+struct Prof {
+  std::mutex mu;
+  bool on = false;
+  struct Rec { int kind; hipEvent_t a, b; };
+  std::vector<Rec> recs;
+  int64_t launches[K_NUM_KINDS] = {};
+  double ms[K_NUM_KINDS] = {};
+};
+Prof& prof() {
+  static Prof p;
+  return p;
+}
+
+// Runs `launch` bracketed by events when timing is on.
+template <class F>
+grpo_status timed(int kind, hipStream_t s, F&& launch) {
+  Prof& p = prof();
+  bool on;
+  {
+    std::lock_guard<std::mutex> g(p.mu);
+    on = p.on;
+  }
+  hipEvent_t a = nullptr, b = nullptr;
+  if (on) {
+    if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return GRPO_ERR_HIP;
+    if (hipEventRecord(a, s) != hipSuccess) return GRPO_ERR_HIP;
+  }
+  launch();
+  if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+  if (on) {
+    if (hipEventRecord(b, s) != hipSuccess) return GRPO_ERR_HIP;
+    std::lock_guard<std::mutex> g(p.mu);
+    p.recs.push_back({kind, a, b});
+  }
+  return GRPO_OK;
+}
+
+#define TRY(x)                          \
+  do {                                  \
+    grpo_status st_ = (x);              \
+    if (st_ != GRPO_OK) return st_;     \
+  } while (0)
+
+// --------------------------------------------------------- device check
+grpo_status check_device() {
+  static std::mutex mu;
+  static int checked[64] = {};  // 0 unknown, 1 ok, 2 bad
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return GRPO_ERR_DEVICE;
+  std::lock_guard<std::mutex> g(mu);
+  if (checked[dev] == 0) {
+    hipDeviceProp_t p;
+    if (hipGetDeviceProperties(&p, dev) != hipSuccess) return GRPO_ERR_DEVICE;
+    checked[dev] = strncmp(p.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
+  }
+  return checked[dev] == 1 ? GRPO_OK : GRPO_ERR_DEVICE;
+}
+
+// --------------------------------------------------------- workspace
+constexpr size_t kAlign = 256;
+constexpr int64_t kDzBudget = 8ll << 30;  // bytes for the two bf16 dz chunk buffers
+constexpr int64_t kVcMax = 16384;
+
+struct Layout {
+  int64_t Npad = 0, Vpad = 0, tiles_v = 0, Vc = 0, nchunks = 0;
+  size_t hdr = 0, rows = 0, seq = 0, y = 0, pidx = 0, counts = 0, base = 0;
+  size_t lse = 0, zy = 0, logp = 0, g = 0, ms = 0, lpart = 0;
+  size_t hT = 0, WT = 0, dz = 0, dzT = 0, dhacc = 0;
+  size_t total = 0;
+};
+
+size_t take(size_t& cur, size_t bytes) {
+  size_t at = cur;
+  cur += (bytes + kAlign - 1) / kAlign * kAlign;
+  return at;
+}
+
+// Vocabulary chunk for the backward pass: the two bf16 dz buffers
+// (token-major and vocabulary-major) together stay within kDzBudget, chunks
+// are at most kVcMax rows, and all chunks but the last have equal size.
+void chunking(int64_t Npad, int64_t Vpad, int64_t& Vc, int64_t& nchunks) {
+  int64_t cap = kDzBudget / (4 * Npad) / kTile * kTile;
+  if (cap < kTile) cap = kTile;
+  if (cap > kVcMax) cap = kVcMax;
+  nchunks = ceil_div(Vpad, cap);
+  Vc = round_up(ceil_div(Vpad, nchunks), kTile);
+  nchunks = ceil_div(Vpad, Vc);
+}
+
+Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_t B) {
+  Layout L;
+  L.Npad = round_up(N, kTile);
+  L.Vpad = round_up(V, kTile);
+  L.tiles_v = L.Vpad / kTile;
+  size_t c = 0;
+  L.hdr = take(c, sizeof(WsHeader));
+  L.rows = take(c, 4 * L.Npad);
+  L.seq = take(c, 4 * L.Npad);
+  L.y = take(c, 4 * L.Npad);
+  L.pidx = take(c, 4 * N);
+  L.counts = take(c, 4 * B);
+  L.base = take(c, 4 * (B + 1));
+  L.lse = take(c, 4 * L.Npad);
+  L.zy = take(c, 4 * L.Npad);
+  L.logp = take(c, 4 * L.Npad);
+  L.g = take(c, 4 * L.Npad);
+  L.lpart = take(c, 4 * token_objective_blocks(N));
+  if (dt == GRPO_BF16) {
+    L.ms = take(c, 8 * L.tiles_v * L.Npad);
+    if (op == GRPO_OP_LOSS_FWD_BWD) {
+      chunking(L.Npad, L.Vpad, L.Vc, L.nchunks);
+      L.hT = take(c, 2 * H * L.Npad);
+      L.WT = take(c, 2 * H * L.Vpad);
+      L.dz = take(c, 2 * L.Npad * L.Vc);
+      L.dzT = take(c, 2 * L.Vc * L.Npad);
+      if (L.nchunks > 1) L.dhacc = take(c, 4 * L.Npad * H);
+    }
+  }
+  L.total = c;
+  return L;
+}
+
+template <class T>
+T* at(void* ws, size_t off) {
+  return (T*)((char*)ws + off);
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+grpo_status check_sizes(grpo_dtype dt, int64_t N, int64_t H, int64_t V) {
+  if (dt != GRPO_F32 && dt != GRPO_BF16) return GRPO_ERR_DTYPE;
+  if (N < 1 || H < 1 || V < 1) return GRPO_ERR_SHAPE;
+  if (N >= (1ll << 31) - kTile || V >= (1ll << 31) - kTile || H >= (1ll << 20)) return GRPO_ERR_SHAPE;
+  if (dt == GRPO_BF16 && H % 8 != 0) return GRPO_ERR_SHAPE;
+  if (dt == GRPO_F32 && H > 8192) return GRPO_ERR_SHAPE;  // two LDS rows of H floats
+  return GRPO_OK;
+}
+
+grpo_status check_ws(void* ws, size_t bytes, const Layout& L) {
+  if (ws == nullptr) return GRPO_ERR_WORKSPACE;
+  if (!aligned(ws, kAlign)) return GRPO_ERR_WORKSPACE;
+  if (bytes < L.total) return GRPO_ERR_WORKSPACE;
+  return GRPO_OK;
+}
+
+GemmArgs gemm_args(const void* A, int64_t lda, int64_t M, const void* B, int64_t ldb, int64_t N,
+                   const int32_t* b_rows, const int32_t* m_dev, const int32_t* n_dev, int64_t K,
+                   const int32_t* k_dev) {
+  GemmArgs g;
+  g.A = (const uint16_t*)A;
+  g.lda = lda;
+  g.M = (int)M;
+  g.B = (const uint16_t*)B;
+  g.ldb = ldb;
+  g.N = (int)N;
+  g.b_rows = b_rows;
+  g.m_dev = m_dev;
+  g.n_dev = n_dev;
+  g.K = (int)K;
+  g.k_dev = k_dev;
+  g.tiles_m = (int)ceil_div(M, kTile);
+  g.tiles_n = (int)ceil_div(N, kTile);
+  return g;
+}
+
+// Packing shared by every entry point that takes a mask.
+grpo_status run_pack(const Layout& L, void* ws, const uint8_t* mask, const int64_t* tokens,
+                     int64_t V, const int64_t* cu, int64_t B, int64_t N, int32_t* rows_out,
+                     int32_t* counts_out, int32_t* nvalid_out, hipStream_t s) {
+  PackArgs a;
+  a.mask = mask;
+  a.tokens = tokens;
+  a.V = V;
+  a.cu = cu;
+  a.B = B;
+  a.N = N;
+  a.counts = counts_out ? counts_out : at<int32_t>(ws, L.counts);
+  a.base = at<int32_t>(ws, L.base);
+  a.rows_p = rows_out ? rows_out : at<int32_t>(ws, L.rows);
+  a.seq_p = at<int32_t>(ws, L.seq);
+  a.y_p = tokens ? at<int32_t>(ws, L.y) : nullptr;
+  a.pidx = at<int32_t>(ws, L.pidx);
+  a.num_valid_out = nvalid_out;
+  a.hdr = at<WsHeader>(ws, L.hdr);
+  return timed(K_PACK, s, [&] { launch_pack(a, s); });
+}
+
+// Forward vocabulary pass: lse and logp (packed order) for every valid row.
+grpo_status run_scoring(const Layout& L, void* ws, grpo_dtype dt, const void* hidden,
+                        const void* weight, int64_t N, int64_t H, int64_t V, hipStream_t s) {
+  WsHeader* hdr = at<WsHeader>(ws, L.hdr);
+  int32_t* rows_p = at<int32_t>(ws, L.rows);
+  int32_t* y_p = at<int32_t>(ws, L.y);
+  float* lse_p = at<float>(ws, L.lse);
+  float* logp_p = at<float>(ws, L.logp);
+  float* zy = at<float>(ws, L.zy);
+  if (dt == GRPO_F32) {
+    return timed(K_F32_SCORE, s, [&] {
+      launch_f32_score((const float*)hidden, (const float*)weight, H, V, rows_p, y_p, hdr, lse_p,
+                       logp_p, zy, N, s);
+    });
+  }
+  float2* ms = at<float2>(ws, L.ms);
+  GemmArgs g = gemm_args(weight, H, V, hidden, H, N, rows_p, nullptr, &hdr->num_valid, H,
+                         nullptr);
+  TRY(timed(K_GEMM_LSE, s, [&] { launch_gemm_lse(g, y_p, zy, ms, L.Npad, V, s); }));
+  return timed(K_LSE_FIN, s, [&] {
+    launch_lse_finalize(ms, L.Npad, (int)L.tiles_v, zy, hdr, lse_p, logp_p, N, s);
+  });
+}
+
+}  // namespace
+
+// ======================================================================
+extern "C" {
+
+const char* grpo_status_string(grpo_status st) {
+  switch (st) {
+    case GRPO_OK: return "ok";
+    case GRPO_ERR_NULL: return "a required pointer is NULL";
+    case GRPO_ERR_SHAPE: return "a size is out of range or inconsistent";
+    case GRPO_ERR_DTYPE: return "unknown or unsupported dtype";
+    case GRPO_ERR_PARAM: return "a hyper-parameter is out of range";
+    case GRPO_ERR_ALIGN: return "a pointer lacks the required alignment";
+    case GRPO_ERR_WORKSPACE: return "workspace is NULL, misaligned or too small";
+    case GRPO_ERR_DEVICE: return "no usable gfx950 device";
+    case GRPO_ERR_HIP: return "a HIP runtime call failed";
+    case GRPO_ERR_TOKEN_RANGE: return "a token id was outside [0, V)";
+    case GRPO_ERR_SEQLENS: return "cu_seqlens was not monotone from 0 to N";
+  }
+  return "unknown status";
+}
+
+size_t grpo_workspace_bytes(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V,
+                            int64_t num_seqs) {
+  if (op != GRPO_OP_LOGPROB_FWD && op != GRPO_OP_LOSS_FWD_BWD) return 0;
+  if (check_sizes(dt, N, H, V) != GRPO_OK || num_seqs < 1) return 0;
+  return layout(op, dt, N, H, V, num_seqs).total;
+}
+
+grpo_status group_advantages(const float* rewards, int64_t num_prompts, int32_t group_size,
+                             float std_eps, int32_t unbiased_std, float* adv,
+                             hipStream_t stream) {
+  if (!rewards || !adv) return GRPO_ERR_NULL;
+  if (num_prompts < 1 || group_size < 2 || num_prompts > (1ll << 40) / group_size)
+    return GRPO_ERR_SHAPE;
+  if (!(std_eps >= 0.f) || isinf(std_eps)) return GRPO_ERR_PARAM;
+  TRY(check_device());
+  return timed(K_ADV, stream, [&] {
+    launch_group_advantages(rewards, num_prompts, group_size, std_eps, unbiased_std, adv, stream);
+  });
+}
+
+grpo_status grpo_pack_valid(const uint8_t* mask, const int64_t* cu_seqlens, int64_t num_seqs,
+                            int64_t N, int32_t* rows, int32_t* counts, int32_t* num_valid,
+                            void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!cu_seqlens || !rows || !counts || !num_valid) return GRPO_ERR_NULL;
+  if (N < 1 || N >= (1ll << 31) - kTile || num_seqs < 1 || num_seqs > N) return GRPO_ERR_SHAPE;
+  Layout L = layout(GRPO_OP_LOGPROB_FWD, GRPO_F32, N, 1, 1, num_seqs);
+  TRY(check_ws(workspace, workspace_bytes, L));
+  TRY(check_device());
+  return run_pack(L, workspace, mask, nullptr, 1, cu_seqlens, num_seqs, N, rows, counts,
+                  num_valid, stream);
+}
+
+grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weight,
+                             const int64_t* tokens, const uint8_t* mask, int64_t N, int64_t H,
+                             int64_t V, float* logp, float* lse, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  TRY(check_sizes(dt, N, H, V));
+  if (!hidden || !weight || !tokens) return GRPO_ERR_NULL;
+  size_t al = dt == GRPO_BF16 ? 16 : 4;
+  if (!aligned(hidden, al) || !aligned(weight, al) || !aligned(tokens, 8)) return GRPO_ERR_ALIGN;
+  if ((logp && !aligned(logp, 4)) || (lse && !aligned(lse, 4))) return GRPO_ERR_ALIGN;
+  Layout L = layout(GRPO_OP_LOGPROB_FWD, dt, N, H, V, 1);
+  TRY(check_ws(workspace, workspace_bytes, L));
+  TRY(check_device());
+  // one "rollout" covering every row (cu_seqlens = NULL means {0, N})
+  TRY(run_pack(L, workspace, mask, tokens, V, nullptr, 1, N, nullptr, nullptr, nullptr, stream));
+  TRY(run_scoring(L, workspace, dt, hidden, weight, N, H, V, stream));
+  if (logp || lse) {
+    return timed(K_LSE_FIN, stream, [&] {
+      launch_rows_out(at<int32_t>(workspace, L.pidx), N, at<float>(workspace, L.logp),
+                      at<float>(workspace, L.lse), logp, lse, stream);
+    });
+  }
+  return GRPO_OK;
+}
+
+grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight,
+                              const int64_t* tokens, const uint8_t* mask,
+                              const int64_t* cu_seqlens, int64_t num_seqs, int64_t N, int64_t H,
+                              int64_t V, const float* old_logp, const float* ref_logp,
+                              const float* adv, float clip_eps, float beta, grpo_agg agg,
+                              const float* lse_in, float* loss, float* logp_out, float* lse_out,
+                              float* token_loss, float* dlogp, uint8_t* clip_flag,
+                              void* grad_hidden, grpo_dtype grad_hidden_dt, float* grad_weight,
+                              int32_t accumulate_grad_weight, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
+  TRY(check_sizes(dt, N, H, V));
+  if (!hidden || !weight || !tokens || !cu_seqlens || !old_logp || !adv || !loss)
+    return GRPO_ERR_NULL;
+  if (num_seqs < 1 || num_seqs > N) return GRPO_ERR_SHAPE;
+  if (!(clip_eps > 0.f && clip_eps < 1.f)) return GRPO_ERR_PARAM;
+  if (!(beta >= 0.f) || isinf(beta)) return GRPO_ERR_PARAM;
+  if (beta != 0.f && !ref_logp) return GRPO_ERR_NULL;
+  if (agg != GRPO_AGG_SEQ_MEAN && agg != GRPO_AGG_TOKEN_MEAN) return GRPO_ERR_PARAM;
+  if (grad_hidden && grad_hidden_dt != GRPO_F32 && grad_hidden_dt != GRPO_BF16)
+    return GRPO_ERR_DTYPE;
+  if (grad_hidden && dt == GRPO_F32 && grad_hidden_dt != GRPO_F32) return GRPO_ERR_DTYPE;
+  size_t al = dt == GRPO_BF16 ? 16 : 4;
+  if (!aligned(hidden, al) || !aligned(weight, al) || !aligned(tokens, 8) ||
+      !aligned(cu_seqlens, 8) || !aligned(old_logp, 4) || !aligned(adv, 4) || !aligned(loss, 4))
+    return GRPO_ERR_ALIGN;
+  if ((grad_hidden && !aligned(grad_hidden, 4)) || (grad_weight && !aligned(grad_weight, 4)))
+    return GRPO_ERR_ALIGN;
+  Layout L = layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, num_seqs);
+  TRY(check_ws(workspace, workspace_bytes, L));
+  TRY(check_device());
+
+  void* ws = workspace;
+  hipStream_t s = stream;
+  WsHeader* hdr = at<WsHeader>(ws, L.hdr);
+  int32_t* rows_p = at<int32_t>(ws, L.rows);
+  int32_t* y_p = at<int32_t>(ws, L.y);
+  int32_t* pidx = at<int32_t>(ws, L.pidx);
+  float* lse_p = at<float>(ws, L.lse);
+  float* logp_p = at<float>(ws, L.logp);
+  float* zy = at<float>(ws, L.zy);
+  float* g_p = at<float>(ws, L.g);
+
+  // S9: pack the valid rows; per-rollout counts |o_b|.
+  TRY(run_pack(L, ws, mask, tokens, V, cu_seqlens, num_seqs, N, nullptr, nullptr, nullptr, s));
+
+  // S2-S4: scoring (or logp from a given lse).
+  if (lse_in == nullptr || dt == GRPO_F32) {
+    TRY(run_scoring(L, ws, dt, hidden, weight, N, H, V, s));
+  }
+  if (lse_in != nullptr) {
+    if (dt == GRPO_BF16) {
+      TRY(timed(K_GATHER_DOT, s, [&] {
+        launch_gather_dot_bf16((const uint16_t*)hidden, (const uint16_t*)weight, H, rows_p, y_p,
+                               hdr, zy, N, s);
+      }));
+    }
+    TRY(timed(K_LSE_FIN, s, [&] { launch_logp_from_lse(zy, lse_in, rows_p, hdr, lse_p, logp_p, N, s); }));
+  }
+
+  // S1 consumer, S5, S6: per-token objective, g = dL/dlogp, the loss.
+  TokenArgs ta;
+  ta.N = N;
+  ta.B = num_seqs;
+  ta.pidx = pidx;
+  ta.seq_p = at<int32_t>(ws, L.seq);
+  ta.counts = at<int32_t>(ws, L.counts);
+  ta.hdr = hdr;
+  ta.adv = adv;
+  ta.logp_p = logp_p;
+  ta.lse_p = lse_p;
+  ta.old_logp = old_logp;
+  ta.ref_logp = beta != 0.f ? ref_logp : nullptr;
+  ta.eps = clip_eps;
+  ta.beta = beta;
+  ta.agg = (int)agg;
+  ta.g_p = g_p;
+  ta.logp_out = logp_out;
+  ta.lse_out = lse_out;
+  ta.token_loss = token_loss;
+  ta.dlogp = dlogp;
+  ta.clip_flag = clip_flag;
+  ta.loss_part = at<float>(ws, L.lpart);
+  ta.loss = loss;
+  TRY(timed(K_TOKEN, s, [&] { launch_token_objective(ta, s); }));
+
+  if (!grad_hidden && !grad_weight) return GRPO_OK;
+
+  // S7: gradients.
+  if (dt == GRPO_F32) {
+    if (grad_hidden) {
+      TRY(timed(K_ZERO_ROWS, s, [&] { launch_zero_masked_rows(pidx, N, H, grad_hidden, 0, s); }));
+      TRY(timed(K_F32_DH, s, [&] {
+        launch_f32_grad_hidden((const float*)hidden, (const float*)weight, H, V, rows_p, y_p,
+                               lse_p, g_p, hdr, (float*)grad_hidden, N, s);
+      }));
+    }
+    if (grad_weight) {
+      TRY(timed(K_F32_DW, s, [&] {
+        launch_f32_grad_weight((const float*)hidden, (const float*)weight, H, V, rows_p, y_p,
+                               lse_p, g_p, hdr, grad_weight, accumulate_grad_weight != 0, s);
+      }));
+    }
+    return GRPO_OK;
+  }
+
+  uint16_t* hT = at<uint16_t>(ws, L.hT);
+  uint16_t* WT = at<uint16_t>(ws, L.WT);
+  uint16_t* dz = at<uint16_t>(ws, L.dz);
+  uint16_t* dzT = at<uint16_t>(ws, L.dzT);
+  float* dhacc = L.nchunks > 1 ? at<float>(ws, L.dhacc) : nullptr;
+  if (grad_weight) {
+    TRY(timed(K_TRANSPOSE, s, [&] {
+      launch_transpose_bf16((const uint16_t*)hidden, H, rows_p, 0, hdr, L.Npad, H, hT, L.Npad, s);
+    }));
+  }
+  if (grad_hidden) {
+    TRY(timed(K_TRANSPOSE, s, [&] {
+      launch_transpose_bf16((const uint16_t*)weight, H, nullptr, V, nullptr, L.Vpad, H, WT, L.Vpad,
+                            s);
+    }));
+  }
+  for (int64_t c = 0; c < L.nchunks; ++c) {
+    int64_t v0 = c * L.Vc;
+    int64_t Mc = V - v0 < L.Vc ? V - v0 : L.Vc;
+    if (Mc <= 0) break;
+    bool last = (c == L.nchunks - 1) || (v0 + L.Vc >= V);
+    // recompute the logits of this chunk and form dz (both layouts)
+    GemmArgs gz = gemm_args((const uint16_t*)weight + v0 * H, H, Mc, hidden, H, N, rows_p, nullptr,
+                            &hdr->num_valid, H, nullptr);
+    TRY(timed(K_GEMM_DZ, s, [&] {
+      launch_gemm_dz(gz, y_p, lse_p, g_p, dz, L.Vc, grad_weight ? dzT : nullptr, L.Npad, V, v0, s);
+    }));
+    if (grad_hidden) {
+      // dh[t, :] (+)= sum_{v in chunk} dz[t, v] W[v, :]
+      GemmArgs gh = gemm_args(dz, L.Vc, L.Npad, WT + v0, L.Vpad, H, nullptr, &hdr->num_valid,
+                              nullptr, round_up(Mc, kBK), nullptr);
+      StoreArgs sa{};
+      sa.acc_buf = dhacc;
+      sa.ld_acc = H;
+      sa.read_acc = c > 0;
+      sa.out = last ? grad_hidden : nullptr;
+      sa.ld_out = H;
+      sa.out_bf16 = grad_hidden_dt == GRPO_BF16;
+      sa.add_out = 0;
+      sa.out_rows = rows_p;
+      sa.m_limit = L.Npad;
+      sa.n_limit = H;
+      TRY(timed(K_GEMM_DH, s, [&] { launch_gemm_store(gh, sa, s); }));
+    }
+    if (grad_weight) {
+      // dW[v, :] = sum_t dz[t, v] h[t, :] over the valid tokens
+      GemmArgs gw = gemm_args(dzT, L.Npad, Mc, hT, L.Npad, H, nullptr, nullptr, nullptr, 0,
+                              &hdr->num_valid);
+      StoreArgs sa{};
+      sa.acc_buf = nullptr;
+      sa.ld_acc = 0;
+      sa.read_acc = 0;
+      sa.out = grad_weight + v0 * H;
+      sa.ld_out = H;
+      sa.out_bf16 = 0;
+      sa.add_out = accumulate_grad_weight != 0;
+      sa.out_rows = nullptr;
+      sa.m_limit = Mc;
+      sa.n_limit = H;
+      TRY(timed(K_GEMM_DW, s, [&] { launch_gemm_store(gw, sa, s); }));
+    }
+    if (last) break;
+  }
+  if (grad_hidden && mask) {
+    TRY(timed(K_ZERO_ROWS, s, [&] {
+      launch_zero_masked_rows(pidx, N, H, grad_hidden, grad_hidden_dt == GRPO_BF16, s);
+    }));
+  }
+  return GRPO_OK;
+}
+
+grpo_status grpo_check_error(void* workspace, hipStream_t stream) {
+  if (!workspace) return GRPO_ERR_NULL;
+  if (hipStreamSynchronize(stream) != hipSuccess) return GRPO_ERR_HIP;
+  WsHeader h;
+  if (hipMemcpy(&h, workspace, sizeof(h), hipMemcpyDeviceToHost) != hipSuccess) return GRPO_ERR_HIP;
+  grpo_status st = GRPO_OK;
+  if (h.err_seqlens) st = GRPO_ERR_SEQLENS;
+  else if (h.err_token) st = GRPO_ERR_TOKEN_RANGE;
+  if (h.err_seqlens || h.err_token) {
+    int32_t zero[2] = {0, 0};
+    if (hipMemcpy(workspace, zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess)
+      return GRPO_ERR_HIP;
+  }
+  return st;
+}
+
+void grpo_profile_enable(int32_t on) {
+  Prof& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  p.on = on != 0;
+}
+
+void grpo_profile_reset(void) {
+  Prof& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  for (auto& r : p.recs) {
+    (void)hipEventSynchronize(r.b);
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  p.recs.clear();
+  for (int k = 0; k < K_NUM_KINDS; ++k) {
+    p.launches[k] = 0;
+    p.ms[k] = 0.0;
+  }
+}
+
+int32_t grpo_profile_num_kinds(void) { return K_NUM_KINDS; }
+
+const char* grpo_profile_kind_name(int32_t kind) {
+  if (kind < 0 || kind >= K_NUM_KINDS) return "";
+  return kKindNames[kind];
+}
+
+grpo_status grpo_profile_query(int32_t kind, int64_t* launches, double* total_ms) {
+  if (kind < 0 || kind >= K_NUM_KINDS) return GRPO_ERR_PARAM;
+  if (!launches || !total_ms) return GRPO_ERR_NULL;
+  Prof& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  // fold finished records into the totals
+  for (auto& r : p.recs) {
+    if (hipEventSynchronize(r.b) != hipSuccess) return GRPO_ERR_HIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return GRPO_ERR_HIP;
+    p.launches[r.kind] += 1;
+    p.ms[r.kind] += ms;
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  p.recs.clear();
+  *launches = p.launches[kind];
+  *total_ms = p.ms[kind];
+  return GRPO_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,122 @@
+// Internal kernel launch interface of libgrpo (not part of the ABI).
+#pragma once
+
+#include "common.h"
+
+namespace grpo {
+
+// ---------------------------------------------------------------- GEMM
+// C[m, n] = sum_k A[m, k] * B[n, k], A and B bf16 row-major with K contiguous.
+struct GemmArgs {
+  const uint16_t* A;
+  int64_t lda;
+  int M;                  // rows of A (loads clamp to M-1)
+  const uint16_t* B;
+  int64_t ldb;
+  int N;                  // rows of B
+  const int32_t* b_rows;  // optional gather: B row n is B[b_rows[n]]
+  const int32_t* m_dev;   // optional device bound on M (e.g. the valid-token count)
+  const int32_t* n_dev;   // optional device bound on N
+  int K;                  // contraction length (used when k_dev is NULL)
+  const int32_t* k_dev;   // optional device K, rounded up to 64 (operands zero-padded)
+  int tiles_m, tiles_n;   // 256x256 tiles covering the static M x N
+};
+
+struct StoreArgs {
+  float* acc_buf;
+  int64_t ld_acc;
+  int read_acc;
+  void* out;
+  int64_t ld_out;
+  int out_bf16;
+  int add_out;
+  const int32_t* out_rows;
+  int64_t m_limit;
+  int64_t n_limit;
+};
+
+int gemm_grid(int tiles_m, int tiles_n);
+void launch_gemm_lse(const GemmArgs& g, const int32_t* y_p, float* zy, float2* ms, int64_t ldms,
+                     int64_t V, hipStream_t s);
+void launch_gemm_dz(const GemmArgs& g, const int32_t* y_p, const float* lse_p, const float* g_p,
+                    uint16_t* dz, int64_t lddz, uint16_t* dzT, int64_t lddzT, int64_t V,
+                    int64_t v0, hipStream_t s);
+void launch_gemm_store(const GemmArgs& g, const StoreArgs& a, hipStream_t s);
+
+// ------------------------------------------------------------- packing
+struct PackArgs {
+  const uint8_t* mask;
+  const int64_t* tokens;  // optional: ids are range-checked against V
+  int64_t V;
+  const int64_t* cu;
+  int64_t B, N;
+  int32_t* counts;   // [B]
+  int32_t* base;     // [B+1]
+  int32_t* rows_p;   // [N] packed -> row
+  int32_t* seq_p;    // [N] packed -> rollout (optional)
+  int32_t* y_p;      // [N] packed -> token id (optional)
+  int32_t* pidx;     // [N] row -> packed or -1 (optional)
+  int32_t* num_valid_out;  // optional extra copy of the count
+  WsHeader* hdr;
+};
+void launch_pack(const PackArgs& a, hipStream_t s);
+
+// ------------------------------------------------ token objective (Eq. 1)
+struct TokenArgs {
+  int64_t N, B;
+  const int32_t* pidx;
+  const int32_t* seq_p;
+  const int32_t* counts;
+  const WsHeader* hdr;
+  const float* adv;
+  const float* logp_p;
+  const float* lse_p;
+  const float* old_logp;
+  const float* ref_logp;
+  float eps, beta;
+  int agg;
+  float* g_p;
+  float* logp_out;
+  float* lse_out;
+  float* token_loss;
+  float* dlogp;
+  uint8_t* clip_flag;
+  float* loss_part;
+  float* loss;
+};
+int64_t token_objective_blocks(int64_t N);
+void launch_token_objective(const TokenArgs& a, hipStream_t s);
+
+// ------------------------------------------------------------ others
+void launch_group_advantages(const float* rewards, int64_t num_prompts, int group, float eps,
+                             int unbiased, float* adv, hipStream_t s);
+void launch_lse_finalize(const float2* ms, int64_t ldms, int tiles, const float* zy,
+                         const WsHeader* hdr, float* lse_p, float* logp_p, int64_t Nmax,
+                         hipStream_t s);
+void launch_logp_from_lse(const float* zy, const float* lse_in, const int32_t* rows_p,
+                          const WsHeader* hdr, float* lse_p, float* logp_p, int64_t Nmax,
+                          hipStream_t s);
+void launch_rows_out(const int32_t* pidx, int64_t N, const float* logp_p, const float* lse_p,
+                     float* logp, float* lse, hipStream_t s);
+void launch_gather_dot_bf16(const uint16_t* hidden, const uint16_t* W, int64_t H,
+                            const int32_t* rows_p, const int32_t* y_p, const WsHeader* hdr,
+                            float* zy, int64_t Nmax, hipStream_t s);
+void launch_zero_tail(float* g_p, int64_t Npad, const WsHeader* hdr, hipStream_t s);
+void launch_transpose_bf16(const uint16_t* in, int64_t ld_in, const int32_t* rows,
+                           int64_t n_static, const WsHeader* hdr, int64_t n_pad, int64_t K,
+                           uint16_t* out, int64_t ld_out, hipStream_t s);
+void launch_zero_masked_rows(const int32_t* pidx, int64_t N, int64_t H, void* out, int out_bf16,
+                             hipStream_t s);
+void launch_f32_score(const float* hidden, const float* W, int64_t H, int64_t V,
+                      const int32_t* rows_p, const int32_t* y_p, const WsHeader* hdr,
+                      float* lse_p, float* logp_p, float* zy_p, int64_t Nmax, hipStream_t s);
+void launch_f32_grad_hidden(const float* hidden, const float* W, int64_t H, int64_t V,
+                            const int32_t* rows_p, const int32_t* y_p, const float* lse_p,
+                            const float* g_p, const WsHeader* hdr, float* grad_hidden,
+                            int64_t Nmax, hipStream_t s);
+void launch_f32_grad_weight(const float* hidden, const float* W, int64_t H, int64_t V,
+                            const int32_t* rows_p, const int32_t* y_p, const float* lse_p,
+                            const float* g_p, const WsHeader* hdr, float* grad_weight,
+                            int accumulate, hipStream_t s);
+
+}  // namespace grpo

@@ -1,0 +1,267 @@
+"""Python binding of libgrpo (include/grpo.h): argument marshalling only.
+
+Tensors supply device pointers and the current HIP stream; every step of
+the computation runs in the library's HIP kernels. There is no CPU or
+PyTorch fallback: if libgrpo.so is missing or the device is not gfx950 the
+calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libgrpo.so")
+
+F32, BF16 = 0, 1
+AGG_SEQ_MEAN, AGG_TOKEN_MEAN = 0, 1
+OP_LOGPROB_FWD, OP_LOSS_FWD_BWD = 0, 1
+
+STATUS = {0: "GRPO_OK", 1: "GRPO_ERR_NULL", 2: "GRPO_ERR_SHAPE", 3: "GRPO_ERR_DTYPE",
+          4: "GRPO_ERR_PARAM", 5: "GRPO_ERR_ALIGN", 6: "GRPO_ERR_WORKSPACE",
+          7: "GRPO_ERR_DEVICE", 8: "GRPO_ERR_HIP", 9: "GRPO_ERR_TOKEN_RANGE",
+          10: "GRPO_ERR_SEQLENS"}
+
+# Every symbol include/grpo.h declares, with its ctypes signature.
+_vp, _i64, _i32, _f32, _sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float,
+                              ctypes.c_size_t)
+SIGNATURES = {
+    "group_advantages": (_i32, [_vp, _i64, _i32, _f32, _i32, _vp, _vp]),
+    "grpo_pack_valid": (_i32, [_vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "grpo_logprob_fwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp, _sz,
+                                _vp]),
+    "grpo_loss_fwd_bwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _vp, _vp,
+                                 _vp, _f32, _f32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                 _i32, _vp, _i32, _vp, _sz, _vp]),
+    "grpo_workspace_bytes": (_sz, [_i32, _i32, _i64, _i64, _i64, _i64]),
+    "grpo_check_error": (_i32, [_vp, _vp]),
+    "grpo_status_string": (ctypes.c_char_p, [_i32]),
+    "grpo_profile_enable": (None, [_i32]),
+    "grpo_profile_reset": (None, []),
+    "grpo_profile_num_kinds": (_i32, []),
+    "grpo_profile_kind_name": (ctypes.c_char_p, [_i32]),
+    "grpo_profile_query": (_i32, [_i32, ctypes.POINTER(_i64), ctypes.POINTER(ctypes.c_double)]),
+}
+
+_lib = None
+
+
+class GrpoError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)} ({status_string(status)})")
+
+
+def load(path: str = LIB_PATH):
+    """Load libgrpo.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build() or "
+                               "python -m paper_2507_05687_amd.build")
+        lib = ctypes.CDLL(path)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def status_string(st: int) -> str:
+    return load().grpo_status_string(st).decode()
+
+
+def _check(st: int, where: str):
+    if st != 0:
+        raise GrpoError(st, where)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _need(t, name, dtype=None, device=None):
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    return t
+
+
+# ------------------------------------------------------------ workspace
+_ws_cache: dict = {}
+
+
+def workspace_bytes(op: int, dt: int, N: int, H: int, V: int, num_seqs: int = 1) -> int:
+    return int(load().grpo_workspace_bytes(op, dt, N, H, V, num_seqs))
+
+
+def workspace(nbytes: int, device=None) -> torch.Tensor:
+    """A 256-byte-aligned device byte buffer of at least nbytes (cached per device)."""
+    device = torch.device(device or torch.cuda.current_device())
+    key = device.index
+    buf = _ws_cache.get(key)
+    if buf is None or buf.numel() < nbytes + 256:
+        _ws_cache.pop(key, None)
+        buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+        _ws_cache[key] = buf
+    off = (-buf.data_ptr()) % 256
+    return buf[off:off + nbytes]
+
+
+def free_workspace():
+    _ws_cache.clear()
+
+
+# ------------------------------------------------------------ entry points
+def group_advantages(rewards: torch.Tensor, group_size: int, std_eps: float = 1e-6,
+                     unbiased: bool = True, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Eq. 2: per-prompt group-normalised advantages (rewards [P*G] fp32, prompt-major)."""
+    _need(rewards, "rewards", torch.float32)
+    n = rewards.numel()
+    if n % group_size:
+        raise ValueError("rewards length must be a multiple of group_size")
+    out = torch.empty_like(rewards) if out is None else _need(out, "out", torch.float32)
+    st = load().group_advantages(_ptr(rewards), n // group_size, group_size, std_eps,
+                                 int(unbiased), _ptr(out), _stream())
+    _check(st, "group_advantages")
+    return out
+
+
+def pack_valid(mask: torch.Tensor | None, cu_seqlens: torch.Tensor):
+    """(rows int32 [num_valid], counts int32 [B], num_valid int) of the valid rows."""
+    _need(cu_seqlens, "cu_seqlens", torch.int64)
+    B = cu_seqlens.numel() - 1
+    N = int(cu_seqlens[-1].item()) if mask is None else mask.numel()
+    dev = cu_seqlens.device
+    rows = torch.empty(N, dtype=torch.int32, device=dev)
+    counts = torch.empty(B, dtype=torch.int32, device=dev)
+    nv = torch.empty(1, dtype=torch.int32, device=dev)
+    ws = workspace(workspace_bytes(OP_LOGPROB_FWD, F32, N, 1, 1, B), dev)
+    m = None if mask is None else _need(mask, "mask").view(torch.uint8)
+    st = load().grpo_pack_valid(_ptr(m), _ptr(cu_seqlens), B, N, _ptr(rows), _ptr(counts),
+                                _ptr(nv), _ptr(ws), ws.numel(), _stream())
+    _check(st, "grpo_pack_valid")
+    n = int(nv.item())
+    return rows[:n], counts, n
+
+
+def logprob_fwd(hidden: torch.Tensor, weight: torch.Tensor, tokens: torch.Tensor,
+                mask: torch.Tensor | None = None, check: bool = False):
+    """Per-token log-prob and log-sum-exp over the vocabulary: (logp, lse), fp32 [N]."""
+    _need(hidden, "hidden")
+    _need(weight, "weight", hidden.dtype)
+    _need(tokens, "tokens", torch.int64)
+    N, H = hidden.shape
+    V = weight.shape[0]
+    dt = _dt(hidden)
+    logp = torch.empty(N, dtype=torch.float32, device=hidden.device)
+    lse = torch.empty(N, dtype=torch.float32, device=hidden.device)
+    ws = workspace(workspace_bytes(OP_LOGPROB_FWD, dt, N, H, V, 1), hidden.device)
+    m = None if mask is None else _need(mask, "mask").view(torch.uint8)
+    st = load().grpo_logprob_fwd(dt, _ptr(hidden), _ptr(weight), _ptr(tokens), _ptr(m), N, H, V,
+                                 _ptr(logp), _ptr(lse), _ptr(ws), ws.numel(), _stream())
+    _check(st, "grpo_logprob_fwd")
+    if check:
+        check_error(ws)
+    return logp, lse
+
+
+def loss_fwd_bwd(hidden, weight, tokens, mask, cu_seqlens, old_logp, ref_logp, adv,
+                 clip_eps: float = 0.2, beta: float = 0.0, agg: int = AGG_SEQ_MEAN,
+                 lse_in=None, grad_hidden: bool = True, grad_weight: bool = True,
+                 grad_hidden_dtype=None, grad_weight_out: torch.Tensor | None = None,
+                 accumulate_grad_weight: bool = False, token_outputs: bool = True,
+                 check: bool = False) -> dict:
+    """GRPO loss (Eq. 1, k3 KL) and its gradients. Returns a dict of tensors:
+    loss [1], logp/lse/token_loss/dlogp [N], clip_flag uint8 [N],
+    grad_hidden [N,H], grad_weight [V,H] fp32 (as requested)."""
+    _need(hidden, "hidden")
+    _need(weight, "weight", hidden.dtype)
+    _need(tokens, "tokens", torch.int64)
+    _need(cu_seqlens, "cu_seqlens", torch.int64)
+    _need(old_logp, "old_logp", torch.float32)
+    _need(adv, "adv", torch.float32)
+    if ref_logp is not None:
+        _need(ref_logp, "ref_logp", torch.float32)
+    if lse_in is not None:
+        _need(lse_in, "lse_in", torch.float32)
+    N, H = hidden.shape
+    V = weight.shape[0]
+    B = cu_seqlens.numel() - 1
+    dt = _dt(hidden)
+    dev = hidden.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    out = {"loss": torch.empty(1, **f32)}
+    if token_outputs:
+        out.update(logp=torch.empty(N, **f32), lse=torch.empty(N, **f32),
+                   token_loss=torch.empty(N, **f32), dlogp=torch.empty(N, **f32),
+                   clip_flag=torch.empty(N, dtype=torch.uint8, device=dev))
+    gh_dt = hidden.dtype if grad_hidden_dtype is None else grad_hidden_dtype
+    if grad_hidden:
+        out["grad_hidden"] = torch.empty(N, H, dtype=gh_dt, device=dev)
+    if grad_weight:
+        if grad_weight_out is not None:
+            out["grad_weight"] = _need(grad_weight_out, "grad_weight_out", torch.float32)
+        else:
+            out["grad_weight"] = torch.empty(V, H, **f32)
+    ws = workspace(workspace_bytes(OP_LOSS_FWD_BWD, dt, N, H, V, B), dev)
+    m = None if mask is None else _need(mask, "mask").view(torch.uint8)
+    g = out.get
+    st = load().grpo_loss_fwd_bwd(
+        dt, _ptr(hidden), _ptr(weight), _ptr(tokens), _ptr(m), _ptr(cu_seqlens), B, N, H, V,
+        _ptr(old_logp), _ptr(ref_logp), _ptr(adv), clip_eps, beta, agg, _ptr(lse_in),
+        _ptr(out["loss"]), _ptr(g("logp")), _ptr(g("lse")), _ptr(g("token_loss")),
+        _ptr(g("dlogp")), _ptr(g("clip_flag")), _ptr(g("grad_hidden")),
+        _dt(out["grad_hidden"]) if grad_hidden else F32, _ptr(g("grad_weight")),
+        int(accumulate_grad_weight), _ptr(ws), ws.numel(), _stream())
+    _check(st, "grpo_loss_fwd_bwd")
+    if check:
+        check_error(ws)
+    return out
+
+
+def check_error(ws: torch.Tensor):
+    st = load().grpo_check_error(_ptr(ws), _stream())
+    _check(st, "device")
+
+
+# ------------------------------------------------------------ timing
+def profile_enable(on: bool = True):
+    load().grpo_profile_enable(int(on))
+
+
+def profile_reset():
+    load().grpo_profile_reset()
+
+
+def profile_read() -> dict:
+    """{kernel kind: (launches, total_ms)} for every kind launched since the last reset."""
+    lib = load()
+    res = {}
+    for k in range(lib.grpo_profile_num_kinds()):
+        n = ctypes.c_int64(0)
+        ms = ctypes.c_double(0.0)
+        _check(lib.grpo_profile_query(k, ctypes.byref(n), ctypes.byref(ms)), "profile")
+        if n.value:
+            res[lib.grpo_profile_kind_name(k).decode()] = (n.value, ms.value)
+    return res

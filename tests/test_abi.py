@@ -1,0 +1,133 @@
+"""C-ABI checks that need no GPU: libgrpo.so loads, exports every function
+include/grpo.h declares, and rejects bad arguments on the host before any
+launch (these paths return before touching the device)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "grpo.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2507_05687_amd import grpo
+
+    if not os.path.exists(grpo.LIB_PATH):
+        pytest.skip("libgrpo.so not built")
+    return grpo.load()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][\w\s\*]*?\b([a-z_][a-z0-9_]*)\s*\(", text,
+                       flags=re.M)
+    return sorted(set(n for n in names if n not in ("defined",)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for required in ("group_advantages", "grpo_logprob_fwd", "grpo_loss_fwd_bwd",
+                     "grpo_pack_valid", "grpo_workspace_bytes", "grpo_check_error",
+                     "grpo_status_string"):
+        assert required in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    from paper_2507_05687_amd import grpo
+
+    names = _declared_functions()
+    assert set(names) == set(grpo.SIGNATURES), "binding and header disagree"
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for st in range(11):
+        s = lib.grpo_status_string(st)
+        assert s and s != b"unknown status"
+    assert lib.grpo_status_string(99) == b"unknown status"
+
+
+def test_workspace_bytes(lib):
+    ws = lib.grpo_workspace_bytes
+    assert ws(0, 1, 100, 64, 1000, 1) > 0
+    assert ws(1, 1, 100, 64, 1000, 4) > ws(0, 1, 100, 64, 1000, 4)
+    assert ws(1, 1, 1000, 64, 1000, 4) > ws(1, 1, 100, 64, 1000, 4)
+    assert ws(0, 1, 0, 64, 1000, 1) == 0       # N < 1
+    assert ws(0, 1, 10, 60, 1000, 1) == 0      # bf16 needs H % 8 == 0
+    assert ws(0, 0, 10, 60, 1000, 1) > 0       # fp32 does not
+    assert ws(0, 7, 10, 64, 1000, 1) == 0      # unknown dtype
+    assert ws(9, 1, 10, 64, 1000, 1) == 0      # unknown op
+    # full-size loss workspace stays well inside one MI355X's 288 GB
+    assert ws(1, 1, 131072, 4096, 155136, 64) < 32 << 30
+
+
+NULL = None
+P = ctypes.c_void_p(0x1000)  # a non-NULL, 256-byte-aligned dummy (never dereferenced)
+
+
+def _loss(lib, **kw):
+    a = dict(dt=1, hidden=P, weight=P, tokens=P, mask=NULL, cu=P, B=2, N=8, H=64, V=100,
+             old=P, ref=P, adv=P, eps=0.2, beta=0.01, agg=0, lse_in=NULL, loss=P, logp=NULL,
+             lse=NULL, tl=NULL, dlogp=NULL, clip=NULL, gh=NULL, gh_dt=1, gw=NULL, acc=0,
+             ws=NULL, ws_bytes=0, stream=NULL)
+    a.update(kw)
+    return lib.grpo_loss_fwd_bwd(*a.values())
+
+
+def test_loss_argument_errors(lib):
+    assert _loss(lib, hidden=NULL) == 1
+    assert _loss(lib, loss=NULL) == 1
+    assert _loss(lib, beta=0.1, ref=NULL) == 1
+    assert _loss(lib, N=0) == 2
+    assert _loss(lib, H=60) == 2
+    assert _loss(lib, B=0) == 2
+    assert _loss(lib, B=9) == 2
+    assert _loss(lib, dt=5) == 3
+    assert _loss(lib, gh=P, gh_dt=7) == 3
+    assert _loss(lib, dt=0, gh=P, gh_dt=1) == 3
+    assert _loss(lib, eps=0.0) == 4
+    assert _loss(lib, eps=1.0) == 4
+    assert _loss(lib, beta=-1.0) == 4
+    assert _loss(lib, beta=float("nan")) == 4
+    assert _loss(lib, agg=3) == 4
+    assert _loss(lib, hidden=ctypes.c_void_p(0x1008)) == 5
+    assert _loss(lib) == 6                          # no workspace
+    assert _loss(lib, ws=ctypes.c_void_p(0x1010), ws_bytes=1 << 40) == 6  # misaligned
+    assert _loss(lib, ws=P, ws_bytes=16) == 6       # too small
+
+
+def test_other_entry_point_errors(lib):
+    adv = lib.group_advantages
+    assert adv(NULL, 2, 4, 1e-6, 1, P, NULL) == 1
+    assert adv(P, 2, 1, 1e-6, 1, P, NULL) == 2
+    assert adv(P, 0, 4, 1e-6, 1, P, NULL) == 2
+    assert adv(P, 2, 4, -1.0, 1, P, NULL) == 4
+    fwd = lib.grpo_logprob_fwd
+    assert fwd(1, NULL, P, P, NULL, 8, 64, 100, P, P, P, 1 << 30, NULL) == 1
+    assert fwd(1, P, P, P, NULL, 8, 12, 100, P, P, P, 1 << 30, NULL) == 2
+    assert fwd(1, P, P, P, NULL, 8, 64, 0, P, P, P, 1 << 30, NULL) == 2
+    assert fwd(2, P, P, P, NULL, 8, 64, 100, P, P, P, 1 << 30, NULL) == 3
+    assert fwd(1, P, P, P, NULL, 8, 64, 100, P, P, P, 8, NULL) == 6
+    pk = lib.grpo_pack_valid
+    assert pk(NULL, NULL, 2, 8, P, P, P, P, 1 << 30, NULL) == 1
+    assert pk(NULL, P, 0, 8, P, P, P, P, 1 << 30, NULL) == 2
+    assert pk(NULL, P, 2, 8, P, P, P, NULL, 0, NULL) == 6
+    assert lib.grpo_check_error(NULL, NULL) == 1
+
+
+def test_profile_interface_without_launches(lib):
+    n = lib.grpo_profile_num_kinds()
+    assert n >= 8
+    names = [lib.grpo_profile_kind_name(k).decode() for k in range(n)]
+    assert "gemm_logits_lse" in names and "gemm_grad_weight" in names
+    lib.grpo_profile_reset()
+    c = ctypes.c_int64(-1)
+    t = ctypes.c_double(-1)
+    assert lib.grpo_profile_query(0, ctypes.byref(c), ctypes.byref(t)) == 0
+    assert c.value == 0 and t.value == 0.0
+    assert lib.grpo_profile_query(n, ctypes.byref(c), ctypes.byref(t)) == 4

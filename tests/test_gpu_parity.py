@@ -1,0 +1,275 @@
+"""Parity of the HIP path (through the C ABI) with the double-precision
+oracle, on seeded synthetic inputs. GPU only.
+
+Tolerances: fp32 inputs 1e-5 relative (log-probs, loss, gradients
+norm-wise); bf16 inputs 2e-3 relative on log-probs and loss, 5e-3 norm-wise
+on gradients (dz is rounded to bf16 before the gradient products); integer
+outputs (packing, counts, clip flags away from the clip boundary) bit-exact.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2507_05687_amd import grpo, workloads
+from tests.gpu_util import (dev, host64, loss_tolerance_ok, norm_rel, oracle_problem, rel_err,
+                            to_dev)
+
+pytestmark = pytest.mark.gpu
+
+BF16_TOL = 2e-3
+BF16_GRAD_TOL = 5e-3
+F32_TOL = 1e-5
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _setup():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    oracle.build(force=False)
+    grpo.load()
+    yield
+    grpo.free_workspace()
+    torch.cuda.empty_cache()
+
+
+def _problem(name="tiny_fp32", **kw):
+    w = workloads.scaled(workloads.WORKLOADS[name], **kw)
+    W = workloads.make_weight(w)
+    h = workloads.make_hidden(w)
+    b = workloads.make_batch(w)
+    adv = oracle.advantages(b["rewards"], w.group).astype(np.float32)
+    _, logp, _ = oracle.score_rows(oracle.decode(h, w.dtype), oracle.decode(W, w.dtype),
+                                   b["tokens"])
+    old = (logp + b["old_noise"]).astype(np.float32)
+    ref = (logp + b["ref_noise"]).astype(np.float32)
+    return w, W, h, b, adv, old, ref
+
+
+def _run_loss(w, W, h, b, adv, old, ref, agg=0, **kw):
+    return grpo.loss_fwd_bwd(to_dev(h, w.dtype), to_dev(W, w.dtype), dev(b["tokens"]),
+                             dev(b["mask"]), dev(b["cu_seqlens"]), dev(old), dev(ref), dev(adv),
+                             w.clip_eps, w.beta, agg, check=True, **kw)
+
+
+def _compare_loss(w, W, h, b, adv, old, ref, out, tol, grad_tol, agg=0):
+    o = oracle_problem(h, W, w.dtype, b, adv.astype(np.float64), old.astype(np.float64),
+                       ref.astype(np.float64), w.clip_eps, w.beta, agg)
+    m = b["mask"].astype(bool)
+    torch.cuda.synchronize()
+    assert rel_err(host64(out["logp"])[m], o["logp"][m]) <= tol
+    assert rel_err(host64(out["lse"])[m], o["lse"][m]) <= tol
+    assert np.all(host64(out["logp"])[~m] == 0) and np.all(host64(out["lse"])[~m] == 0)
+    # per-row weights of the Eq. 1 sum, for the condition-aware loss check
+    counts = np.array([m[b["cu_seqlens"][i]:b["cu_seqlens"][i + 1]].sum()
+                       for i in range(w.num_seqs)])
+    c = oracle.seq_weights(counts, agg)
+    seq = np.repeat(np.arange(w.num_seqs), np.diff(b["cu_seqlens"]))
+    abs_sum = float(np.sum(c[seq] * np.abs(o["ell"])))
+    assert loss_tolerance_ok(float(out["loss"].item()), o["loss"], abs_sum, tol), \
+        (float(out["loss"].item()), o["loss"], abs_sum)
+    # token loss and dL/dlogp, absolute scale-aware
+    tl = host64(out["token_loss"])
+    assert np.max(np.abs(tl - o["ell"])) <= tol * max(1.0, np.max(np.abs(o["ell"])))
+    g = host64(out["dlogp"])
+    assert np.max(np.abs(g - o["g"])) <= tol * np.max(np.abs(o["g"])) + 1e-12
+    # clip flags bit-exact away from the clip boundary
+    rho = np.exp(o["logp"] - old)
+    far = (np.abs(rho - (1 - w.clip_eps)) > 1e-3) & (np.abs(rho - (1 + w.clip_eps)) > 1e-3) & m
+    flag = out["clip_flag"].cpu().numpy()
+    assert np.array_equal(flag[far], o["clipped"][far])
+    assert np.all(flag[~m] == 0)
+    dh = host64(out["grad_hidden"])
+    dW = host64(out["grad_weight"])
+    e_dh, e_dW = norm_rel(dh, o["dh"]), norm_rel(dW, o["dW"])
+    assert e_dh <= grad_tol, e_dh
+    assert e_dW <= grad_tol, e_dW
+    assert np.all(dh[~m] == 0)
+    return o, dict(dh=e_dh, dW=e_dW)
+
+
+# ------------------------------------------------------------ advantages
+def test_group_advantages_parity():
+    g = np.random.default_rng(0)
+    G = 8
+    r = (g.integers(0, 2, 64 * G) * 0.9 + g.integers(0, 2, 64 * G) * 0.1).astype(np.float32)
+    r[:G] = 1.0
+    r[G:2 * G] = 0.1  # equal but not exactly representable: must still give 0
+    r[2 * G:2 * G + 4] = [0, 0, 1, 1]
+    r[2 * G + 4:3 * G] = [0.5, 0.5, 0.5, 0.25]
+    for unbiased in (True, False):
+        got = grpo.group_advantages(dev(r), G, 1e-6, unbiased).cpu().numpy()
+        want = oracle.advantages(r.astype(np.float64), G, 1e-6, unbiased)
+        assert np.all(got[want == 0] == 0)
+        assert np.max(np.abs(got - want)) <= 1e-6 * max(1.0, np.max(np.abs(want)))
+    # G = 4 worked example, one prompt
+    got = grpo.group_advantages(dev(np.array([0, 0, 1, 1], np.float32)), 4).cpu().numpy()
+    np.testing.assert_allclose(got, [-0.8660239, -0.8660239, 0.8660239, 0.8660239], rtol=1e-6)
+    # a large group (several lanes per element)
+    r = g.random(3 * 200).astype(np.float32)
+    got = grpo.group_advantages(dev(r), 200).cpu().numpy()
+    np.testing.assert_allclose(got, oracle.advantages(r.astype(np.float64), 200), rtol=2e-5,
+                               atol=2e-6)
+
+
+# ------------------------------------------------------------ packing
+def test_pack_valid_bit_exact():
+    g = np.random.default_rng(1)
+    T, B = 700, 9
+    lens = g.integers(0, T + 1, B)
+    lens[3] = 0
+    lens[4] = T
+    mask = (np.arange(T)[None, :] < lens[:, None]).astype(np.uint8).reshape(-1)
+    mask[5 * T + 10] = 0  # a hole inside a rollout
+    cu = (np.arange(B + 1) * T).astype(np.int64)
+    rows, counts, n = grpo.pack_valid(dev(mask), dev(cu))
+    w_rows, w_counts, _ = oracle.pack_valid(mask, cu)
+    assert n == len(w_rows)
+    assert np.array_equal(rows.cpu().numpy(), w_rows)
+    assert np.array_equal(counts.cpu().numpy(), w_counts)
+
+
+# ------------------------------------------------------------ fp32 config
+def test_tiny_fp32_config():
+    """2 prompts x G=4 x 16 tokens, H=64, V=1000, fp32 (1e-5)."""
+    w, W, h, b, adv, old, ref = _problem("tiny_fp32")
+    out = _run_loss(w, W, h, b, adv, old, ref)
+    _compare_loss(w, W, h, b, adv, old, ref, out, F32_TOL, F32_TOL)
+
+
+def test_tiny_fp32_pipeline_from_rewards():
+    """Rewards -> group_advantages -> loss, all on the device, vs the oracle chain."""
+    w, W, h, b, _, old, ref = _problem("tiny_fp32", seed=5)
+    adv_dev = grpo.group_advantages(dev(b["rewards"]), w.group)
+    out = grpo.loss_fwd_bwd(to_dev(h, "f32"), to_dev(W, "f32"), dev(b["tokens"]), dev(b["mask"]),
+                            dev(b["cu_seqlens"]), dev(old), dev(ref), adv_dev, w.clip_eps, w.beta)
+    adv_o = oracle.advantages(b["rewards"].astype(np.float64), w.group)
+    o = oracle_problem(h, W, "f32", b, adv_o, old.astype(np.float64), ref.astype(np.float64),
+                       w.clip_eps, w.beta)
+    assert abs(out["loss"].item() - o["loss"]) <= F32_TOL * max(abs(o["loss"]), 1e-3)
+    assert norm_rel(host64(out["grad_weight"]), o["dW"]) <= F32_TOL
+
+
+# ------------------------------------------------------------ bf16, small
+SMALL = {
+    # several tiles on every axis, ragged token and vocabulary tails
+    "ragged_tiles": dict(prompts=3, group=4, seq_len=50, hidden=320, vocab=3000, ragged=True,
+                         min_len=1, forced_equal_groups=1),
+    # H not a multiple of the 64-wide K step
+    "k_tail": dict(prompts=2, group=4, seq_len=40, hidden=200, vocab=1100),
+    # several vocabulary chunks in the backward pass
+    "multi_chunk": dict(prompts=2, group=4, seq_len=40, hidden=128, vocab=40000),
+    # smallest shapes
+    "tiny": dict(prompts=1, group=2, seq_len=3, hidden=8, vocab=5),
+}
+
+
+@pytest.mark.parametrize("case", list(SMALL))
+def test_bf16_loss_parity(case):
+    kw = dict(SMALL[case], dtype="bf16", rms_norm_hidden=True, beta=0.01, noise_sigma=0.1,
+              seed=11)
+    w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    out = _run_loss(w, W, h, b, adv, old, ref)
+    _compare_loss(w, W, h, b, adv, old, ref, out, BF16_TOL, BF16_GRAD_TOL)
+
+
+def test_bf16_token_mean_aggregation():
+    kw = dict(SMALL["ragged_tiles"], dtype="bf16", rms_norm_hidden=True, beta=0.01, seed=12)
+    w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    out = _run_loss(w, W, h, b, adv, old, ref, agg=1)
+    _compare_loss(w, W, h, b, adv, old, ref, out, BF16_TOL, BF16_GRAD_TOL, agg=1)
+
+
+def test_bf16_f32_grad_hidden_and_accumulate():
+    kw = dict(SMALL["k_tail"], dtype="bf16", rms_norm_hidden=True, seed=13)
+    w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    base = _run_loss(w, W, h, b, adv, old, ref)
+    f32 = _run_loss(w, W, h, b, adv, old, ref, grad_hidden_dtype=torch.float32)
+    assert f32["grad_hidden"].dtype == torch.float32
+    d = (f32["grad_hidden"].bfloat16() - base["grad_hidden"]).abs().max().item()
+    assert d <= 1e-2 * base["grad_hidden"].float().abs().max().item()
+    acc = base["grad_weight"].clone()
+    again = _run_loss(w, W, h, b, adv, old, ref, grad_weight_out=acc, accumulate_grad_weight=True)
+    torch.testing.assert_close(again["grad_weight"], 2 * base["grad_weight"], rtol=1e-6, atol=0)
+
+
+def test_bf16_logprob_fwd_parity():
+    kw = dict(SMALL["ragged_tiles"], dtype="bf16", rms_norm_hidden=True, seed=14)
+    w = workloads.scaled(workloads.WORKLOADS["fwd_bf16"], **kw)
+    W, h, b = workloads.make_weight(w), workloads.make_hidden(w), workloads.make_batch(w)
+    logp, lse = grpo.logprob_fwd(to_dev(h, "bf16"), to_dev(W, "bf16"), dev(b["tokens"]),
+                                 dev(b["mask"]), check=True)
+    m = b["mask"].astype(bool)
+    o_lse, o_logp, _ = oracle.score_rows(oracle.decode(h, "bf16")[m], oracle.decode(W, "bf16"),
+                                         b["tokens"][m])
+    assert rel_err(host64(logp)[m], o_logp) <= BF16_TOL
+    assert rel_err(host64(lse)[m], o_lse) <= BF16_TOL
+    assert np.all(host64(logp)[~m] == 0) and np.all(host64(lse)[~m] == 0)
+
+
+# ------------------------------------------------------------ closed forms on the device
+def test_zero_weight_gives_log_vocab():
+    N, H, V = 300, 64, 155136
+    h = torch.randn(N, H, device="cuda").bfloat16()
+    W = torch.zeros(V, H, device="cuda", dtype=torch.bfloat16)
+    y = torch.randint(0, V, (N,), device="cuda")
+    logp, lse = grpo.logprob_fwd(h, W, y)
+    lnV = math.log(V)
+    assert torch.all((lse - lnV).abs() <= 2e-6 * lnV)
+    assert torch.all((logp + lnV).abs() <= 2e-6 * lnV)
+
+
+def test_on_policy_and_equal_rewards_closed_forms():
+    kw = dict(SMALL["ragged_tiles"], dtype="bf16", rms_norm_hidden=True, seed=15)
+    w, W, h, b, adv, _, _ = _problem("fwdbwd_bf16", **kw)
+    hd, Wd = to_dev(h, "bf16"), to_dev(W, "bf16")
+    logp, _ = grpo.logprob_fwd(hd, Wd, dev(b["tokens"]), dev(b["mask"]))
+    # old = ref = own logp: rho = 1, no clipping, kl = 0 -> ell = -A, loss = -(1/B) sum_b A_b
+    out = grpo.loss_fwd_bwd(hd, Wd, dev(b["tokens"]), dev(b["mask"]), dev(b["cu_seqlens"]), logp,
+                            logp, dev(adv), 0.2, 0.5)
+    m = b["mask"].astype(bool)
+    seq = np.repeat(np.arange(w.num_seqs), np.diff(b["cu_seqlens"]))
+    assert np.all(out["clip_flag"].cpu().numpy() == 0)
+    tl = out["token_loss"].cpu().numpy()
+    np.testing.assert_allclose(tl[m], -adv[seq[m]], rtol=1e-6, atol=1e-7)
+    assert abs(out["loss"].item() + adv[np.diff(b["cu_seqlens"]) > 0].sum() / w.num_seqs) < 1e-5
+    # all-equal rewards and beta = 0: loss and gradients exactly zero
+    zero = np.zeros_like(adv)
+    out = grpo.loss_fwd_bwd(hd, Wd, dev(b["tokens"]), dev(b["mask"]), dev(b["cu_seqlens"]), logp,
+                            None, dev(zero), 0.2, 0.0)
+    assert out["loss"].item() == 0.0
+    assert torch.all(out["grad_hidden"] == 0) and torch.all(out["grad_weight"] == 0)
+
+
+def test_deterministic_bits():
+    kw = dict(SMALL["multi_chunk"], dtype="bf16", rms_norm_hidden=True, seed=16)
+    w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    a = _run_loss(w, W, h, b, adv, old, ref)
+    c = _run_loss(w, W, h, b, adv, old, ref)
+    for k in ("loss", "logp", "lse", "dlogp", "grad_hidden", "grad_weight"):
+        assert torch.equal(a[k], c[k]), k
+
+
+def test_lse_in_reuse():
+    kw = dict(SMALL["ragged_tiles"], dtype="bf16", rms_norm_hidden=True, seed=17)
+    w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    hd, Wd = to_dev(h, "bf16"), to_dev(W, "bf16")
+    _, lse = grpo.logprob_fwd(hd, Wd, dev(b["tokens"]), dev(b["mask"]))
+    a = _run_loss(w, W, h, b, adv, old, ref)
+    c = _run_loss(w, W, h, b, adv, old, ref, lse_in=lse)
+    torch.testing.assert_close(c["lse"], a["lse"], rtol=0, atol=0)
+    torch.testing.assert_close(c["logp"], a["logp"], rtol=1e-5, atol=1e-5)
+    torch.testing.assert_close(c["grad_weight"], a["grad_weight"], rtol=1e-2, atol=1e-6)
+
+
+def test_token_out_of_range_sets_flag():
+    w, W, h, b, adv, old, ref = _problem("tiny_fp32", seed=18)
+    b["tokens"][7] = w.vocab  # one bad id
+    with pytest.raises(grpo.GrpoError) as e:
+        _run_loss(w, W, h, b, adv, old, ref)
+    assert e.value.status == 9
+    # the next call on the same workspace starts clean
+    b["tokens"][7] = 0
+    _run_loss(w, W, h, b, adv, old, ref)
