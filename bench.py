@@ -1,0 +1,255 @@
+"""Benchmark of the GRPO scoring + loss hot path on one MI355X.
+
+One step = one pass of the whole path over one batch: group advantages
+(Eq. 2) from the rewards, then the fused scoring + GRPO loss forward and
+backward (Eq. 1 with k3 KL): valid-row packing, LM-head contraction with
+online log-sum-exp, the per-token ratio/clip/KL epilogue, the masked
+aggregation, and dL/dh, dL/dW through a recomputed, chunked logits
+gradient. Inputs are seeded synthetic tensors already resident in HBM.
+
+Prints one JSON line (see the contract in the repository documentation).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "rollout tokens/sec for fused log-prob + GRPO loss fwd+bwd; % bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def _to_dev_bf16(bits, torch):
+    return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def _gemm_flops(kind: str, w, n_valid: int, vc_sizes: list[int]) -> float:
+    """Contraction flops of all launches of one GEMM kind in one step."""
+    H, V = w.hidden, w.vocab
+    if kind == "gemm_logits_lse":
+        return 2.0 * n_valid * V * H * (2 if w.double_scoring else 1)
+    if kind in ("gemm_recompute_dz", "gemm_grad_hidden", "gemm_grad_weight"):
+        return 2.0 * n_valid * V * H
+    return 0.0
+
+
+def _traffic_from_profiles(kernel: str):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
+    was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+        import hashlib
+
+        src = open(os.path.join(ROOT, "paper_2507_05687_amd", "csrc", "gemm_bf16.hip"),
+                   "rb").read()
+        if rec.get("gemm_source_sha256") != hashlib.sha256(src).hexdigest():
+            return None
+        return rec.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")
+    except Exception:
+        return None
+
+
+def cpu_baseline(w, W_bits, h_bits, batch, adv, old, ref, sample_tokens: int):
+    """Time the double-precision oracle on the host cores on a bounded sample
+    of the same workload: `sample_tokens` valid rows, scored at full H and V,
+    with their loss terms, their dL/dh rows and their contribution to dL/dW
+    over the whole vocabulary."""
+    import oracle
+
+    oracle.build(force=False)
+    rows = np.flatnonzero(batch["mask"])[:sample_tokens]
+    hd = oracle.decode(h_bits[rows], "bf16")
+    Wd = oracle.decode(W_bits, "bf16")
+    y = batch["tokens"][rows]
+    B = w.num_seqs
+    seq = np.repeat(np.arange(B), np.diff(batch["cu_seqlens"]))[rows]
+    counts = np.array([batch["mask"][batch["cu_seqlens"][b]:batch["cu_seqlens"][b + 1]].sum()
+                       for b in range(B)])
+    t0 = time.perf_counter()
+    lse, logp, _ = oracle.score_rows(hd, Wd, y)
+    c = oracle.seq_weights(counts)
+    ell, g, _ = oracle.token_objective(logp, old[rows], ref[rows], adv[seq], c[seq], None,
+                                       w.clip_eps, w.beta)
+    oracle.grad_hidden_rows(hd, Wd, y, lse, g)
+    oracle.grad_weight_rows(hd, Wd, y, lse, g)
+    dt = time.perf_counter() - t0
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    return {"value": len(rows) / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(rows)} valid tokens of {w.name} at H={w.hidden}, V={w.vocab}: "
+                      f"scoring, loss terms, dL/dh rows and their dL/dW over all V rows "
+                      f"({dt:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="fwdbwd_bf16",
+                    choices=["fwdbwd_bf16", "fwd_bf16", "ragged_bf16", "double_bf16"])
+    ap.add_argument("--cpu-sample", type=int, default=16,
+                    help="valid tokens timed on the CPU oracle (0 skips the CPU baseline)")
+    ap.add_argument("--verbose", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build "
+              "implements the single-GPU hot path, sharding is described in DESIGN.md",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2507_05687_amd import grpo, workloads
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    grpo.load()
+    w = workloads.WORKLOADS[args.workload]
+    log = (lambda *a: print(*a, file=sys.stderr, flush=True)) if args.verbose else (lambda *a: None)
+
+    t0 = time.time()
+    W_bits = workloads.make_weight(w, "policy")
+    h_bits = workloads.make_hidden(w)
+    batch = workloads.make_batch(w)
+    log(f"inputs generated in {time.time() - t0:.1f}s")
+    W = _to_dev_bf16(W_bits, torch)
+    Wref = _to_dev_bf16(workloads.make_weight(w, "reference"), torch) if w.double_scoring else None
+    h = _to_dev_bf16(h_bits, torch)
+    tokens = torch.from_numpy(batch["tokens"]).cuda()
+    mask = torch.from_numpy(batch["mask"]).cuda()
+    cu = torch.from_numpy(batch["cu_seqlens"]).cuda()
+    rewards = torch.from_numpy(batch["rewards"]).cuda()
+    n_valid = int(batch["mask"].sum())
+    N, H, V, B = w.num_tokens, w.hidden, w.vocab, w.num_seqs
+    use_mask = mask if w.ragged else None
+
+    # old/ref log-probs: the policy's own log-prob plus seeded noise
+    base, _ = grpo.logprob_fwd(h, W, tokens, use_mask)
+    old = base + torch.from_numpy(batch["old_noise"]).cuda()
+    ref = base + torch.from_numpy(batch["ref_noise"]).cuda()
+    del base
+    f32 = dict(dtype=torch.float32, device="cuda")
+    loss = torch.empty(1, **f32)
+    gh = torch.empty(N, H, dtype=torch.bfloat16, device="cuda")
+    gw = torch.empty(V, H, **f32)
+    adv = torch.empty(B, **f32)
+    lse_buf = torch.empty(N, **f32)
+    old_buf = torch.empty(N, **f32)
+    ref_buf = torch.empty(N, **f32)
+    ws_bytes = max(grpo.workspace_bytes(grpo.OP_LOSS_FWD_BWD, grpo.BF16, N, H, V, B),
+                   grpo.workspace_bytes(grpo.OP_LOGPROB_FWD, grpo.BF16, N, H, V, 1))
+    ws = grpo.workspace(ws_bytes)
+    lib = grpo.load()
+    P = grpo._ptr
+    stream = grpo._stream()
+    mptr = P(use_mask)
+
+    def step():
+        st = lib.group_advantages(P(rewards), w.prompts, w.group, 1e-6, 1, P(adv), stream)
+        assert st == 0, st
+        if args.workload == "fwd_bf16":
+            st = lib.grpo_logprob_fwd(grpo.BF16, P(h), P(W), P(tokens), mptr, N, H, V,
+                                      P(old_buf), P(lse_buf), P(ws), ws.numel(), stream)
+            assert st == 0, st
+            return
+        lse_in, o, r = None, old, ref
+        if w.double_scoring:  # S8: score under the policy (old) and the reference
+            st = lib.grpo_logprob_fwd(grpo.BF16, P(h), P(W), P(tokens), mptr, N, H, V,
+                                      P(old_buf), P(lse_buf), P(ws), ws.numel(), stream)
+            assert st == 0, st
+            st = lib.grpo_logprob_fwd(grpo.BF16, P(h), P(Wref), P(tokens), mptr, N, H, V,
+                                      P(ref_buf), None, P(ws), ws.numel(), stream)
+            assert st == 0, st
+            lse_in, o, r = lse_buf, old_buf, ref_buf
+        st = lib.grpo_loss_fwd_bwd(grpo.BF16, P(h), P(W), P(tokens), mptr, P(cu), B, N, H, V,
+                                   P(o), P(r), P(adv), w.clip_eps, w.beta, 0, P(lse_in), P(loss),
+                                   None, None, None, None, None, P(gh), grpo.BF16, P(gw), 0,
+                                   P(ws), ws.numel(), stream)
+        assert st == 0, st
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    grpo.check_error(ws)
+    log(f"warmup done, loss={loss.item():.6g}")
+
+    grpo.profile_reset()
+    grpo.profile_enable(True)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    grpo.profile_enable(False)
+    total_ms = e0.elapsed_time(e1)
+    prof = grpo.profile_read()
+    ms_per_step = total_ms / args.steps
+    tokens_per_s = n_valid / (ms_per_step / 1e3)
+    log(json.dumps(prof))
+
+    # dominant kernel: the kind with the largest summed time
+    kind, (launches, kms) = max(prof.items(), key=lambda kv: kv[1][1])
+    flops = _gemm_flops(kind, w, n_valid, []) * args.steps
+    achieved = flops / (kms / 1e3) / 1e12 if flops else None
+    traffic = _traffic_from_profiles(kind)
+    roofline = {"kernel": kind, "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": (achieved / PEAK_BF16_TFLOPS) if achieved else None,
+                "traffic": traffic, "launches_per_step": launches / args.steps,
+                "avg_launch_ms": kms / launches}
+    per_tok = {"fwd_bf16": 2, "fwdbwd_bf16": 6, "ragged_bf16": 6, "double_bf16": 8}[args.workload]
+    executed = {"fwd_bf16": 2, "fwdbwd_bf16": 8, "ragged_bf16": 8, "double_bf16": 10}[args.workload]
+    step_s = ms_per_step / 1e3
+    alg_frac = per_tok * n_valid * V * H / step_s / (PEAK_BF16_TFLOPS * 1e12)
+    exe_frac = executed * n_valid * V * H / step_s / (PEAK_BF16_TFLOPS * 1e12)
+
+    res = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded numpy inputs: h RMS-normalised N(0,1), W N(0,0.02), "
+                "uniform token ids, Bernoulli rewards)",
+        "config": {"workload": w.name, "prompts": w.prompts, "group": w.group,
+                   "seq_len": w.seq_len, "valid_tokens": n_valid, "hidden": H, "vocab": V,
+                   "clip_eps": w.clip_eps, "beta": w.beta},
+        "mfma_frac_algorithmic": alg_frac,
+        "mfma_frac_executed": exe_frac,
+        "roofline": roofline,
+        "kernels_ms_per_step": {k: v[1] / args.steps for k, v in sorted(prof.items())},
+    }
+    if args.cpu_sample > 0:
+        adv_h = adv.cpu().numpy().astype(np.float64)
+        res["cpu_baseline"] = cpu_baseline(w, W_bits, h_bits, batch, adv_h,
+                                           old.cpu().numpy().astype(np.float64),
+                                           ref.cpu().numpy().astype(np.float64),
+                                           args.cpu_sample)
+    else:
+        res["cpu_baseline"] = None
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

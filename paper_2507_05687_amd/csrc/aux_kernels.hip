@@ -406,14 +406,17 @@ void launch_gather_dot_bf16(const uint16_t* hidden, const uint16_t* W, int64_t H
 }
 
 // ------------------------------------------------------- transposes
-// out[k][i] = in[src_row(i)][k] for i < n_valid, 0 for n_valid <= i < n_pad.
-// src_row(i) = rows ? rows[i] : i. 64x64 bf16 tiles through LDS.
-__global__ void __launch_bounds__(256) k_transpose_bf16(const uint16_t* __restrict__ in,
-                                                        int64_t ld_in, const int32_t* __restrict__ rows,
-                                                        int64_t n_static,
-                                                        const WsHeader* __restrict__ hdr,
-                                                        int64_t K, uint16_t* __restrict__ out,
-                                                        int64_t ld_out) {
+// out(k, i) = in[src_row(i)][k] for i < n_valid, 0 for n_valid <= i < n_pad,
+// with src_row(i) = rows ? rows[i] : i. `out` is in the tiled layout with k
+// as the row and i as the column: block (k/256, i/64) of n_pad/64 blocks per
+// tile-row, row k%256, column i%64. 64x64 bf16 tiles go through LDS.
+__global__ void __launch_bounds__(256) k_transpose_tiled(const uint16_t* __restrict__ in,
+                                                         int64_t ld_in,
+                                                         const int32_t* __restrict__ rows,
+                                                         int64_t n_static,
+                                                         const WsHeader* __restrict__ hdr,
+                                                         int64_t n_pad, int64_t K,
+                                                         uint16_t* __restrict__ out) {
   __shared__ uint16_t tile[64][66];
   int64_t i0 = (int64_t)blockIdx.x * 64, k0 = (int64_t)blockIdx.y * 64;
   int64_t nvalid = hdr ? (int64_t)hdr->num_valid : n_static;
@@ -447,12 +450,12 @@ __global__ void __launch_bounds__(256) k_transpose_bf16(const uint16_t* __restri
     for (int q = 0; q < 16; ++q) tile[ri][c0 + q] = vals[q];
   }
   __syncthreads();
-  // store: 64 output rows (k) x 64 columns (i)
+  // store: 64 output rows (k) x 64 columns (i), one 128-byte block row each
   {
     int kk = t >> 2, c0 = (t & 3) * 16;
     int64_t k = k0 + kk;
     if (k < K) {
-      uint16_t* p = out + k * ld_out + i0 + c0;
+      uint16_t* p = out + ((k >> 8) * (n_pad >> 6) + (i0 >> 6)) * kTileElems + (k & 255) * 64 + c0;
       u32x4 a, b;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -465,13 +468,13 @@ __global__ void __launch_bounds__(256) k_transpose_bf16(const uint16_t* __restri
   }
 }
 
-// n_pad must be a multiple of 64 and ld_out >= n_pad, with 16-byte aligned rows.
-void launch_transpose_bf16(const uint16_t* in, int64_t ld_in, const int32_t* rows,
-                           int64_t n_static, const WsHeader* hdr, int64_t n_pad, int64_t K,
-                           uint16_t* out, int64_t ld_out, hipStream_t s) {
+// n_pad must be a multiple of 64; `out` holds round_up(K, 256) x n_pad elements.
+void launch_transpose_tiled(const uint16_t* in, int64_t ld_in, const int32_t* rows,
+                            int64_t n_static, const WsHeader* hdr, int64_t n_pad, int64_t K,
+                            uint16_t* out, hipStream_t s) {
   dim3 grid((unsigned)(n_pad / 64), (unsigned)ceil_div(K, 64));
-  hipLaunchKernelGGL(k_transpose_bf16, grid, dim3(256), 0, s, in, ld_in, rows, n_static, hdr, K,
-                     out, ld_out);
+  hipLaunchKernelGGL(k_transpose_tiled, grid, dim3(256), 0, s, in, ld_in, rows, n_static, hdr,
+                     n_pad, K, out);
 }
 
 // ------------------------------------------ zero the masked output rows

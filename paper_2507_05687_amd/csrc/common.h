@@ -4,6 +4,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 namespace grpo {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -22,6 +25,7 @@ struct WsHeader {
 
 constexpr int kTile = 256;  // GEMM tile edge (rows and columns)
 constexpr int kBK = 64;     // GEMM K step
+constexpr int kTileElems = kTile * kBK;  // elements of one 256x64 block of the tiled layout
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 __host__ __device__ inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
@@ -35,5 +39,16 @@ __device__ inline uint16_t f32_to_bf16_bits(float f) {
 }
 __device__ inline float bf16_bits_to_f32(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
+
+// Calls f(std::integral_constant<int, i>) for i = 0..N-1, unrolled at compile
+// time, so that register arrays indexed by i are never demoted to memory.
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 }  // namespace grpo

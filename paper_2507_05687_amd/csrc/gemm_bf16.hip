@@ -17,6 +17,12 @@
 // LDS rows are 128 bytes; the eight 16-byte chunks of a row are XOR-swizzled
 // by a few row bits so that the MFMA fragment reads hit distinct banks.
 //
+// Operands come row-major (the caller's hidden states and LM head) or in the
+// tiled layout that the library writes for its own intermediates: 256-row x
+// 64-column blocks stored contiguously, block (rb, kb) at
+// (rb * blocks_per_row + kb) * 16384 elements. A K step of a tile then reads
+// one contiguous 32 KiB block per operand.
+//
 // Tile order: workgroup ids are dealt round-robin to the 8 XCDs, so id
 // b runs on XCD b % 8. Tiles are assigned so that each XCD owns a band of
 // kGM tile-rows and walks the tile-columns in blocks of kGN, and all 8 XCDs
@@ -73,54 +79,54 @@ struct EpiLse {
   int64_t ldms;
   int64_t V;
 
-  __device__ void operator()(f32x16 (&acc)[4][4], const Frag& f, int m_valid, int n_valid,
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], const Frag& f, int m_valid,
+                                             int n_valid,
                              char* smem) const {
     float pm[4], ps[4];
-#pragma unroll
-    for (int ni = 0; ni < 4; ++ni) {
-      int64_t t = (int64_t)f.tn * kTile + f.col(ni);
-      int y = t < n_valid ? y_p[t] : -1;
+    const int vbase = f.tm * kTile + f.wm * 128 + (f.lane >> 5) * 4;
+    const int vlim = (int)(V - vbase);  // rows r of this lane are valid iff row offset < vlim
+    static_for<4>([&](auto ni) {
+      const int64_t t = (int64_t)f.tn * kTile + f.col(ni);
+      const int y = t < n_valid ? y_p[t] - vbase : -1;  // y as a row offset of this lane
       float m = -INFINITY;
-#pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          int64_t v = (int64_t)f.tm * kTile + f.row(mi, r);
-          if (v < V) m = fmaxf(m, acc[mi][ni][r]);
-        }
+      static_for<4>([&](auto mi) {
+        static_for<16>([&](auto r) {
+          constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
+          if (o < vlim) m = fmaxf(m, acc[mi][ni][r.value]);
+        });
+      });
       float s = 0.f;
-#pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          int64_t v = (int64_t)f.tm * kTile + f.row(mi, r);
-          if (v < V) s += __expf(acc[mi][ni][r] - m);
-          if (v == y) zy[t] = acc[mi][ni][r];
-        }
+      static_for<4>([&](auto mi) {
+        static_for<16>([&](auto r) {
+          constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
+          if (o < vlim) s += __expf(acc[mi][ni][r.value] - m);
+          if (o == y) zy[t] = acc[mi][ni][r.value];
+        });
+      });
       // merge with the lane holding the other 64 rows of this column
       float m2 = __shfl_xor(m, 32, 64), s2 = __shfl_xor(s, 32, 64);
       float mm = fmaxf(m, m2);
       float sm = (s == 0.f ? 0.f : s * __expf(m - mm)) + (s2 == 0.f ? 0.f : s2 * __expf(m2 - mm));
       pm[ni] = mm;
       ps[ni] = sm;
-    }
+    });
     // merge the two waves that share these columns (wm = 0 and 1)
     float2* xch = (float2*)smem;  // [2 (wn)][128]
     if (f.wm == 1 && f.lane < 32) {
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni) xch[f.wn * 128 + ni * 32 + f.lane] = make_float2(pm[ni], ps[ni]);
+      static_for<4>([&](auto ni) {
+        xch[f.wn * 128 + ni * 32 + f.lane] = make_float2(pm[ni], ps[ni]);
+      });
     }
     __syncthreads();
     if (f.wm == 0 && f.lane < 32) {
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni) {
+      static_for<4>([&](auto ni) {
         float2 o = xch[f.wn * 128 + ni * 32 + f.lane];
         float mm = fmaxf(pm[ni], o.x);
         float sm = (ps[ni] == 0.f ? 0.f : ps[ni] * __expf(pm[ni] - mm)) +
                    (o.y == 0.f ? 0.f : o.y * __expf(o.x - mm));
         int64_t t = (int64_t)f.tn * kTile + f.col(ni);
         if (t < n_valid) ms[(int64_t)f.tm * ldms + t] = make_float2(mm, sm);
-      }
+      });
     }
   }
 };
@@ -129,43 +135,47 @@ struct EpiDz {
   const int32_t* y_p;
   const float* lse_p;
   const float* g_p;
-  uint16_t* dz;   // [tokens][lddz], columns = chunk-local vocabulary rows
-  int64_t lddz;
-  uint16_t* dzT;  // [chunk rows][lddzT], columns = tokens (may be NULL)
-  int64_t lddzT;
-  int64_t V;      // vocabulary size
-  int64_t v0;     // first vocabulary row of this chunk
+  uint16_t* dz;    // tiled [tokens][chunk vocabulary], dz_kt 64-wide blocks per tile-row
+  int64_t dz_kt;
+  uint16_t* dzT;   // tiled [chunk vocabulary][tokens] (may be NULL), dzT_kt blocks per tile-row
+  int64_t dzT_kt;
+  int64_t V;       // vocabulary size
+  int64_t v0;      // first vocabulary row of this chunk
 
-  __device__ void operator()(f32x16 (&acc)[4][4], const Frag& f, int m_valid, int n_valid,
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], const Frag& f, int m_valid,
+                                             int n_valid,
                              char*) const {
-#pragma unroll
-    for (int ni = 0; ni < 4; ++ni) {
-      int64_t t = (int64_t)f.tn * kTile + f.col(ni);
-      bool tv = t < n_valid;
-      int y = tv ? y_p[t] : -1;
-      float l = tv ? lse_p[t] : 0.f;
-      float g = tv ? g_p[t] : 0.f;
-#pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          uint16_t b[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            int r = q * 4 + e;
-            int vl = f.tm * kTile + f.row(mi, r);
-            int64_t v = v0 + vl;
+    const int hi = (f.lane >> 5) * 4;
+    const int64_t vbase = v0 + (int64_t)f.tm * kTile + f.wm * 128 + hi;
+    const int vlim = (int)((V - vbase) < (1 << 20) ? (V - vbase) : (1 << 20));
+    static_for<4>([&](auto ni) {
+      const int64_t t = (int64_t)f.tn * kTile + f.col(ni);
+      const bool tv = t < n_valid;
+      const int y = tv ? (int)(y_p[t] - vbase) : -1;  // y as a row offset of this lane
+      const float l = tv ? lse_p[t] : 0.f;
+      const float g = tv ? g_p[t] : 0.f;
+      // element (t, vl) of dz lives at tile (t/256, vl/64), row t%256, column vl%64
+      uint16_t* pz = dz + ((t >> 8) * dz_kt + f.tm * 4 + f.wm * 2) * kTileElems + (t & 255) * 64 + hi;
+      // element (vl, t) of dzT lives at tile (vl/256, t/64), row vl%256, column t%64
+      uint16_t* pzt = dzT ? dzT + ((int64_t)f.tm * dzT_kt + (t >> 6)) * kTileElems + (t & 63) +
+                                (f.wm * 128 + hi) * 64
+                          : nullptr;
+      static_for<4>([&](auto mi) {
+        static_for<4>([&](auto q) {
+          uint32_t b[4];
+          static_for<4>([&](auto e) {
+            constexpr int r = q * 4 + e;
+            constexpr int o = mi * 32 + q * 8 + e;
             float d = 0.f;
-            if (tv && v < V) d = g * ((v == y ? 1.f : 0.f) - __expf(acc[mi][ni][r] - l));
+            if (tv && o < vlim) d = g * ((o == y ? 1.f : 0.f) - __expf(acc[mi][ni][r] - l));
             b[e] = f32_to_bf16_bits(d);
-            if (dzT) dzT[(int64_t)vl * lddzT + t] = b[e];
-          }
-          int vl0 = f.tm * kTile + f.row(mi, q * 4);
-          uint2 pk = make_uint2((uint32_t)b[0] | ((uint32_t)b[1] << 16),
-                                (uint32_t)b[2] | ((uint32_t)b[3] << 16));
-          *(uint2*)(dz + t * lddz + vl0) = pk;
-        }
-    }
+            if (pzt) pzt[o * 64] = (uint16_t)b[e];
+          });
+          uint2 pk = make_uint2(b[0] | (b[1] << 16), b[2] | (b[3] << 16));
+          *(uint2*)(pz + (mi >> 1) * kTileElems + (mi & 1) * 32 + q * 8) = pk;
+        });
+      });
+    });
   }
 };
 
@@ -181,39 +191,43 @@ struct EpiStore {
   int64_t m_limit;       // rows >= m_limit are not stored (static bound)
   int64_t n_limit;       // columns >= n_limit are not stored
 
-  __device__ void operator()(f32x16 (&acc)[4][4], const Frag& f, int m_valid, int n_valid,
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], const Frag& f, int m_valid,
+                                             int n_valid,
                              char*) const {
-    int64_t mlim = m_limit < m_valid ? m_limit : m_valid;
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        int64_t m = (int64_t)f.tm * kTile + f.row(mi, r);
-        if (m >= mlim) continue;
-#pragma unroll
-        for (int ni = 0; ni < 4; ++ni) {
-          int64_t n = (int64_t)f.tn * kTile + f.col(ni);
-          if (n >= n_limit) continue;
-          float x = acc[mi][ni][r];
-          if (read_acc) x += acc_buf[m * ld_acc + n];
-          if (out == nullptr) {
-            acc_buf[m * ld_acc + n] = x;
-          } else {
-            int64_t orow = out_rows ? (int64_t)out_rows[m] : m;
-            if (out_bf16) {
-              ((uint16_t*)out)[orow * ld_out + n] = f32_to_bf16_bits(x);
-            } else {
-              float* o = (float*)out + orow * ld_out + n;
-              *o = add_out ? *o + x : x;
+    const int64_t mlim = m_limit < m_valid ? m_limit : m_valid;
+    const int64_t mbase = (int64_t)f.tm * kTile + f.wm * 128 + (f.lane >> 5) * 4;
+    static_for<4>([&](auto mi) {
+      static_for<16>([&](auto r) {
+        constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
+        const int64_t m = mbase + o;
+        if (m < mlim) {
+          const int64_t orow = out_rows ? (int64_t)out_rows[m] : m;
+          static_for<4>([&](auto ni) {
+            const int64_t n = (int64_t)f.tn * kTile + f.col(ni);
+            if (n < n_limit) {
+              float x = acc[mi][ni][r.value];
+              if (read_acc) x += acc_buf[m * ld_acc + n];
+              if (out == nullptr) {
+                acc_buf[m * ld_acc + n] = x;
+              } else if (out_bf16) {
+                ((uint16_t*)out)[orow * ld_out + n] = f32_to_bf16_bits(x);
+              } else {
+                float* o2 = (float*)out + orow * ld_out + n;
+                *o2 = add_out ? *o2 + x : x;
+              }
             }
-          }
+          });
         }
-      }
+      });
+    });
   }
 };
 
 // ------------------------------------------------------------ main loop
-template <class Epi, bool KTAIL>
+// TILED: both operands are in the tiled layout (256x64 blocks, one block
+// per K step, contiguous); otherwise both are row-major with a row stride,
+// and B rows may be gathered through b_rows.
+template <class Epi, bool KTAIL, bool TILED>
 __global__ void __launch_bounds__(256, 1) k_gemm_bf16(GemmArgs g, Epi epi) {
   __shared__ __attribute__((aligned(16))) char smem[2 * kLdsStage];
   int tm, tn;
@@ -231,14 +245,26 @@ __global__ void __launch_bounds__(256, 1) k_gemm_bf16(GemmArgs g, Epi epi) {
   const int lrow = tid >> 3, lch = tid & 7;
   const uint16_t* pa[8];
   const uint16_t* pb[8];
+  if (TILED) {
+    const uint16_t* a0 = g.A + ((int64_t)tm * g.a_kt + g.a_kb0) * kTileElems + tid * 8;
+    const uint16_t* b0 = g.B + ((int64_t)tn * g.b_kt + g.b_kb0) * kTileElems + tid * 8;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    int ra = min(tm * kTile + lrow + 32 * j, m_valid - 1);
-    pa[j] = g.A + (int64_t)ra * g.lda + lch * 8;
-    int rb = min(tn * kTile + lrow + 32 * j, n_valid - 1);
-    if (g.b_rows) rb = g.b_rows[rb];
-    pb[j] = g.B + (int64_t)rb * g.ldb + lch * 8;
+    for (int j = 0; j < 8; ++j) {
+      pa[j] = a0 + j * 2048;
+      pb[j] = b0 + j * 2048;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      int ra = min(tm * kTile + lrow + 32 * j, m_valid - 1);
+      pa[j] = g.A + (int64_t)ra * g.lda + lch * 8;
+      int rb = min(tn * kTile + lrow + 32 * j, n_valid - 1);
+      if (g.b_rows) rb = g.b_rows[rb];
+      pb[j] = g.B + (int64_t)rb * g.ldb + lch * 8;
+    }
   }
+  // K step kt reads at +kt*64 (row-major) or +kt*kTileElems (tiled)
+  constexpr int kStep = TILED ? kTileElems : kBK;
   const int st_off = lrow * 128 + ((lch ^ swz(lrow)) << 4);  // + 32j*128
 
   // ---- fragment reads: lane reads row (l%32) of each 32-row block, chunk 2s + l/32
@@ -258,15 +284,16 @@ __global__ void __launch_bounds__(256, 1) k_gemm_bf16(GemmArgs g, Epi epi) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   u32x4 ra_[8], rb_[8];
-  auto gload = [&](int k0) {
+  auto gload = [&](int kt) {
+    const int64_t off = (int64_t)kt * kStep;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      if (KTAIL && k0 + lch * 8 >= K) {
+      if (KTAIL && kt * kBK + lch * 8 >= K) {
         ra_[j] = u32x4{0, 0, 0, 0};
         rb_[j] = u32x4{0, 0, 0, 0};
       } else {
-        ra_[j] = *(const u32x4*)(pa[j] + k0);
-        rb_[j] = *(const u32x4*)(pb[j] + k0);
+        ra_[j] = *(const u32x4*)(pa[j] + off);
+        rb_[j] = *(const u32x4*)(pb[j] + off);
       }
     }
   };
@@ -285,7 +312,7 @@ __global__ void __launch_bounds__(256, 1) k_gemm_bf16(GemmArgs g, Epi epi) {
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * kBK);
+    if (kt + 1 < nk) gload(kt + 1);
     const char* base = smem + buf * kLdsStage;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
@@ -309,33 +336,33 @@ __global__ void __launch_bounds__(256, 1) k_gemm_bf16(GemmArgs g, Epi epi) {
   epi(acc, f, m_valid, n_valid, smem);
 }
 
-template <class Epi>
+template <class Epi, bool TILED>
 static void launch_gemm(const GemmArgs& g, const Epi& e, hipStream_t s) {
   int grid = gemm_grid(g.tiles_m, g.tiles_n);
-  bool ktail = (g.k_dev == nullptr) && (g.K % kBK != 0);
+  bool ktail = !TILED && (g.k_dev == nullptr) && (g.K % kBK != 0);
   if (ktail)
-    hipLaunchKernelGGL((k_gemm_bf16<Epi, true>), dim3(grid), dim3(256), 0, s, g, e);
+    hipLaunchKernelGGL((k_gemm_bf16<Epi, true, false>), dim3(grid), dim3(256), 0, s, g, e);
   else
-    hipLaunchKernelGGL((k_gemm_bf16<Epi, false>), dim3(grid), dim3(256), 0, s, g, e);
+    hipLaunchKernelGGL((k_gemm_bf16<Epi, false, TILED>), dim3(grid), dim3(256), 0, s, g, e);
 }
 
 void launch_gemm_lse(const GemmArgs& g, const int32_t* y_p, float* zy, float2* ms, int64_t ldms,
                      int64_t V, hipStream_t s) {
   EpiLse e{y_p, zy, ms, ldms, V};
-  launch_gemm(g, e, s);
+  launch_gemm<EpiLse, false>(g, e, s);
 }
 
 void launch_gemm_dz(const GemmArgs& g, const int32_t* y_p, const float* lse_p, const float* g_p,
-                    uint16_t* dz, int64_t lddz, uint16_t* dzT, int64_t lddzT, int64_t V,
+                    uint16_t* dz, int64_t dz_kt, uint16_t* dzT, int64_t dzT_kt, int64_t V,
                     int64_t v0, hipStream_t s) {
-  EpiDz e{y_p, lse_p, g_p, dz, lddz, dzT, lddzT, V, v0};
-  launch_gemm(g, e, s);
+  EpiDz e{y_p, lse_p, g_p, dz, dz_kt, dzT, dzT_kt, V, v0};
+  launch_gemm<EpiDz, false>(g, e, s);
 }
 
 void launch_gemm_store(const GemmArgs& g, const StoreArgs& a, hipStream_t s) {
   EpiStore e{a.acc_buf, a.ld_acc, a.read_acc, a.out, a.ld_out, a.out_bf16, a.add_out,
              a.out_rows, a.m_limit, a.n_limit};
-  launch_gemm(g, e, s);
+  launch_gemm<EpiStore, true>(g, e, s);
 }
 
 }  // namespace grpo

@@ -137,8 +137,9 @@ Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_
     L.ms = take(c, 8 * L.tiles_v * L.Npad);
     if (op == GRPO_OP_LOSS_FWD_BWD) {
       chunking(L.Npad, L.Vpad, L.Vc, L.nchunks);
-      L.hT = take(c, 2 * H * L.Npad);
-      L.WT = take(c, 2 * H * L.Vpad);
+      int64_t Hpad = round_up(H, kTile);
+      L.hT = take(c, 2 * Hpad * L.Npad);
+      L.WT = take(c, 2 * Hpad * L.Vpad);
       L.dz = take(c, 2 * L.Npad * L.Vc);
       L.dzT = take(c, 2 * L.Vc * L.Npad);
       if (L.nchunks > 1) L.dhacc = take(c, 4 * L.Npad * H);
@@ -186,6 +187,7 @@ GemmArgs gemm_args(const void* A, int64_t lda, int64_t M, const void* B, int64_t
   g.n_dev = n_dev;
   g.K = (int)K;
   g.k_dev = k_dev;
+  g.a_kt = g.a_kb0 = g.b_kt = g.b_kb0 = 0;
   g.tiles_m = (int)ceil_div(M, kTile);
   g.tiles_n = (int)ceil_div(N, kTile);
   return g;
@@ -425,15 +427,17 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
   uint16_t* dz = at<uint16_t>(ws, L.dz);
   uint16_t* dzT = at<uint16_t>(ws, L.dzT);
   float* dhacc = L.nchunks > 1 ? at<float>(ws, L.dhacc) : nullptr;
+  // Intermediates in the tiled layout (256x64 blocks): h^T [H x tokens],
+  // W^T [H x V], dz [tokens x chunk] and dz^T [chunk x tokens].
+  const int64_t kt_tok = L.Npad / kBK, kt_voc = L.Vpad / kBK, kt_chunk = L.Vc / kBK;
   if (grad_weight) {
     TRY(timed(K_TRANSPOSE, s, [&] {
-      launch_transpose_bf16((const uint16_t*)hidden, H, rows_p, 0, hdr, L.Npad, H, hT, L.Npad, s);
+      launch_transpose_tiled((const uint16_t*)hidden, H, rows_p, 0, hdr, L.Npad, H, hT, s);
     }));
   }
   if (grad_hidden) {
     TRY(timed(K_TRANSPOSE, s, [&] {
-      launch_transpose_bf16((const uint16_t*)weight, H, nullptr, V, nullptr, L.Vpad, H, WT, L.Vpad,
-                            s);
+      launch_transpose_tiled((const uint16_t*)weight, H, nullptr, V, nullptr, L.Vpad, H, WT, s);
     }));
   }
   for (int64_t c = 0; c < L.nchunks; ++c) {
@@ -445,12 +449,16 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
     GemmArgs gz = gemm_args((const uint16_t*)weight + v0 * H, H, Mc, hidden, H, N, rows_p, nullptr,
                             &hdr->num_valid, H, nullptr);
     TRY(timed(K_GEMM_DZ, s, [&] {
-      launch_gemm_dz(gz, y_p, lse_p, g_p, dz, L.Vc, grad_weight ? dzT : nullptr, L.Npad, V, v0, s);
+      launch_gemm_dz(gz, y_p, lse_p, g_p, dz, kt_chunk, grad_weight ? dzT : nullptr, kt_tok, V, v0,
+                     s);
     }));
     if (grad_hidden) {
       // dh[t, :] (+)= sum_{v in chunk} dz[t, v] W[v, :]
-      GemmArgs gh = gemm_args(dz, L.Vc, L.Npad, WT + v0, L.Vpad, H, nullptr, &hdr->num_valid,
-                              nullptr, round_up(Mc, kBK), nullptr);
+      GemmArgs gh = gemm_args(dz, 0, L.Npad, WT, 0, H, nullptr, &hdr->num_valid, nullptr,
+                              round_up(Mc, kBK), nullptr);
+      gh.a_kt = kt_chunk;
+      gh.b_kt = kt_voc;
+      gh.b_kb0 = v0 / kBK;
       StoreArgs sa{};
       sa.acc_buf = dhacc;
       sa.ld_acc = H;
@@ -466,8 +474,10 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
     }
     if (grad_weight) {
       // dW[v, :] = sum_t dz[t, v] h[t, :] over the valid tokens
-      GemmArgs gw = gemm_args(dzT, L.Npad, Mc, hT, L.Npad, H, nullptr, nullptr, nullptr, 0,
+      GemmArgs gw = gemm_args(dzT, 0, Mc, hT, 0, H, nullptr, nullptr, nullptr, 0,
                               &hdr->num_valid);
+      gw.a_kt = kt_tok;
+      gw.b_kt = kt_tok;
       StoreArgs sa{};
       sa.acc_buf = nullptr;
       sa.ld_acc = 0;

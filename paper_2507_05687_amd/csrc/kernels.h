@@ -17,6 +17,8 @@ struct GemmArgs {
   const int32_t* b_rows;  // optional gather: B row n is B[b_rows[n]]
   const int32_t* m_dev;   // optional device bound on M (e.g. the valid-token count)
   const int32_t* n_dev;   // optional device bound on N
+  int64_t a_kt, a_kb0;    // tiled A: 64-wide blocks per tile-row, first block
+  int64_t b_kt, b_kb0;    // tiled B: same
   int K;                  // contraction length (used when k_dev is NULL)
   const int32_t* k_dev;   // optional device K, rounded up to 64 (operands zero-padded)
   int tiles_m, tiles_n;   // 256x256 tiles covering the static M x N
@@ -39,7 +41,7 @@ int gemm_grid(int tiles_m, int tiles_n);
 void launch_gemm_lse(const GemmArgs& g, const int32_t* y_p, float* zy, float2* ms, int64_t ldms,
                      int64_t V, hipStream_t s);
 void launch_gemm_dz(const GemmArgs& g, const int32_t* y_p, const float* lse_p, const float* g_p,
-                    uint16_t* dz, int64_t lddz, uint16_t* dzT, int64_t lddzT, int64_t V,
+                    uint16_t* dz, int64_t dz_kt, uint16_t* dzT, int64_t dzT_kt, int64_t V,
                     int64_t v0, hipStream_t s);
 void launch_gemm_store(const GemmArgs& g, const StoreArgs& a, hipStream_t s);
 
@@ -102,9 +104,9 @@ void launch_gather_dot_bf16(const uint16_t* hidden, const uint16_t* W, int64_t H
                             const int32_t* rows_p, const int32_t* y_p, const WsHeader* hdr,
                             float* zy, int64_t Nmax, hipStream_t s);
 void launch_zero_tail(float* g_p, int64_t Npad, const WsHeader* hdr, hipStream_t s);
-void launch_transpose_bf16(const uint16_t* in, int64_t ld_in, const int32_t* rows,
-                           int64_t n_static, const WsHeader* hdr, int64_t n_pad, int64_t K,
-                           uint16_t* out, int64_t ld_out, hipStream_t s);
+void launch_transpose_tiled(const uint16_t* in, int64_t ld_in, const int32_t* rows,
+                            int64_t n_static, const WsHeader* hdr, int64_t n_pad, int64_t K,
+                            uint16_t* out, hipStream_t s);
 void launch_zero_masked_rows(const int32_t* pidx, int64_t N, int64_t H, void* out, int out_bf16,
                              hipStream_t s);
 void launch_f32_score(const float* hidden, const float* W, int64_t H, int64_t V,
