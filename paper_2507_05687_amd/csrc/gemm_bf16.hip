@@ -43,6 +43,9 @@ constexpr int kLdsStage = 2 * kTile * kBK * 2;  // bytes of one A+B stage (64 Ki
 
 __device__ inline int swz(int row) { return (row >> GRPO_SWZ_SHIFT) & 7; }
 
+typedef __attribute__((address_space(1))) void* glb_ptr_t;
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
 // Maps a workgroup id to its (tile_m, tile_n); returns false for the
 // padding workgroups of the last band.
 __device__ inline bool tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
@@ -241,32 +244,6 @@ __global__ void __launch_bounds__(256, 1) k_gemm_bf16(GemmArgs g, Epi epi) {
   const int lane = tid & 63, w = tid >> 6;
   const int wm = w & 1, wn = w >> 1;
 
-  // ---- global -> LDS loader: thread owns rows (tid/8 + 32j), chunk tid%8
-  const int lrow = tid >> 3, lch = tid & 7;
-  const uint16_t* pa[8];
-  const uint16_t* pb[8];
-  if (TILED) {
-    const uint16_t* a0 = g.A + ((int64_t)tm * g.a_kt + g.a_kb0) * kTileElems + tid * 8;
-    const uint16_t* b0 = g.B + ((int64_t)tn * g.b_kt + g.b_kb0) * kTileElems + tid * 8;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      pa[j] = a0 + j * 2048;
-      pb[j] = b0 + j * 2048;
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      int ra = min(tm * kTile + lrow + 32 * j, m_valid - 1);
-      pa[j] = g.A + (int64_t)ra * g.lda + lch * 8;
-      int rb = min(tn * kTile + lrow + 32 * j, n_valid - 1);
-      if (g.b_rows) rb = g.b_rows[rb];
-      pb[j] = g.B + (int64_t)rb * g.ldb + lch * 8;
-    }
-  }
-  // K step kt reads at +kt*64 (row-major) or +kt*kTileElems (tiled)
-  constexpr int kStep = TILED ? kTileElems : kBK;
-  const int st_off = lrow * 128 + ((lch ^ swz(lrow)) << 4);  // + 32j*128
-
   // ---- fragment reads: lane reads row (l%32) of each 32-row block, chunk 2s + l/32
   const int fr = lane & 31;
   const int rd_base_a = (wm * 128 + fr) * 128;
@@ -283,53 +260,153 @@ __global__ void __launch_bounds__(256, 1) k_gemm_bf16(GemmArgs g, Epi epi) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  u32x4 ra_[8], rb_[8];
-  auto gload = [&](int kt) {
-    const int64_t off = (int64_t)kt * kStep;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      if (KTAIL && kt * kBK + lch * 8 >= K) {
-        ra_[j] = u32x4{0, 0, 0, 0};
-        rb_[j] = u32x4{0, 0, 0, 0};
-      } else {
-        ra_[j] = *(const u32x4*)(pa[j] + off);
-        rb_[j] = *(const u32x4*)(pb[j] + off);
-      }
-    }
+  bf16x8 fa[2][4], fb[2][4];
+  auto fload = [&](int slot, const char* base, int s) {
+    static_for<4>([&](auto i) {
+      fa[slot][i] = *(const bf16x8*)(base + rd_base_a + i * 32 * 128 + rd_ch[s]);
+      fb[slot][i] = *(const bf16x8*)(base + rd_base_b + i * 32 * 128 + rd_ch[s]);
+    });
   };
-  auto lstore = [&](int buf) {
-    char* base = smem + buf * kLdsStage;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      *(u32x4*)(base + st_off + j * 32 * 128) = ra_[j];
-      *(u32x4*)(base + kTile * kBK * 2 + st_off + j * 32 * 128) = rb_[j];
-    }
+  auto mfma16 = [&](int slot) {
+    static_for<4>([&](auto i) {
+      static_for<4>([&](auto j) {
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][i], fb[slot][j], acc[i][j],
+                                                            0, 0, 0);
+      });
+    });
   };
+  constexpr int kMfma = 0x008, kVmemRead = 0x020, kDsRead = 0x100, kDsWrite = 0x200;
+  // K step kt reads at +kt*64 (row-major) or +kt*kTileElems (tiled)
+  constexpr int kStep = TILED ? kTileElems : kBK;
 
-  const int nk = K / kBK + ((KTAIL && K % kBK) ? 1 : 0);
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-    const char* base = smem + buf * kLdsStage;
+  if constexpr (!KTAIL) {
+    // ---- global -> LDS directly (no register staging). The j-th load of
+    // lane l of wave w fills LDS row r = 8*(w + 4j) + l/8 at physical chunk
+    // l%8, i.e. logical chunk (l%8) ^ swz(r); one load instruction of a wave
+    // writes 1 KiB of consecutive LDS.
+    const int drow = 8 * w + (lane >> 3);
+    const int dch = (lane & 7) ^ swz(drow);  // swz(drow + 32j) == swz(drow)
+    const uint16_t* sa[8];
+    const uint16_t* sb[8];
+    if (TILED) {
+      const uint16_t* a0 =
+          g.A + ((int64_t)tm * g.a_kt + g.a_kb0) * kTileElems + drow * 64 + dch * 8;
+      const uint16_t* b0 =
+          g.B + ((int64_t)tn * g.b_kt + g.b_kb0) * kTileElems + drow * 64 + dch * 8;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      bf16x8 a[4], b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        a[i] = *(const bf16x8*)(base + rd_base_a + i * 32 * 128 + rd_ch[s]);
-        b[i] = *(const bf16x8*)(base + rd_base_b + i * 32 * 128 + rd_ch[s]);
+      for (int j = 0; j < 8; ++j) {
+        sa[j] = a0 + j * 2048;
+        sb[j] = b0 + j * 2048;
       }
+    } else {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < 8; ++j) {
+        int ra = min(tm * kTile + drow + 32 * j, m_valid - 1);
+        sa[j] = g.A + (int64_t)ra * g.lda + dch * 8;
+        int rb = min(tn * kTile + drow + 32 * j, n_valid - 1);
+        if (g.b_rows) rb = g.b_rows[rb];
+        sb[j] = g.B + (int64_t)rb * g.ldb + dch * 8;
+      }
     }
-    if (kt + 1 < nk) lstore(buf ^ 1);
+    auto dma = [&](int kt, int buf) {
+      const int64_t off = (int64_t)kt * kStep;
+      char* la = smem + buf * kLdsStage + w * 1024;
+      static_for<8>([&](auto j) {
+        __builtin_amdgcn_global_load_lds((glb_ptr_t)(sa[j] + off), (lds_ptr_t)(la + j * 4096),
+                                         16, 0, 0);
+      });
+      static_for<8>([&](auto j) {
+        __builtin_amdgcn_global_load_lds((glb_ptr_t)(sb[j] + off),
+                                         (lds_ptr_t)(la + kTile * kBK * 2 + j * 4096), 16, 0, 0);
+      });
+    };
+
+    // Pipeline: while the MFMAs consume LDS buffer kt%2, step kt+1 is landing
+    // in the other buffer. The barrier in the middle of step kt (after every
+    // wave has read sub-step 3) both publishes step kt+1 and frees buffer
+    // kt%2, which immediately receives step kt+2. Sub-step 0 of step kt+1 is
+    // read right after that barrier, behind the last 16 MFMAs of step kt.
+    // __syncthreads() waits for this thread's outstanding LDS loads before
+    // the barrier, which is the completion the next step needs.
+    const int nk = K / kBK;
+    dma(0, 0);
     __syncthreads();
+    dma(min(1, nk - 1), 1);
+    fload(0, smem, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+      const char* base = smem + (kt & 1) * kLdsStage;
+      fload(1, base, 1);
+      mfma16(0);
+      fload(0, base, 2);
+      mfma16(1);
+      fload(1, base, 3);
+      mfma16(0);
+      __builtin_amdgcn_sched_group_barrier(kDsRead, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(kMfma, 16, 0);
+      __builtin_amdgcn_sched_group_barrier(kDsRead, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(kMfma, 16, 0);
+      __builtin_amdgcn_sched_group_barrier(kDsRead, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(kMfma, 16, 0);
+      __syncthreads();
+      dma(min(kt + 2, nk - 1), kt & 1);
+      fload(0, smem + ((kt + 1) & 1) * kLdsStage, 0);
+      mfma16(1);
+      __builtin_amdgcn_sched_group_barrier(kDsRead, 8, 1);
+      static_for<16>([&](auto) {
+        __builtin_amdgcn_sched_group_barrier(kMfma, 1, 1);
+        __builtin_amdgcn_sched_group_barrier(kVmemRead, 1, 1);
+      });
+    }
+    __syncthreads();  // the last (redundant) loads land before LDS is reused
+  } else {
+    // ---- K not a multiple of 64: register-staged loads that zero-fill the
+    // columns past K. Thread owns rows (tid/8 + 32j), chunk tid%8.
+    const int lrow = tid >> 3, lch = tid & 7;
+    const uint16_t* pa[8];
+    const uint16_t* pb[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      int ra = min(tm * kTile + lrow + 32 * j, m_valid - 1);
+      pa[j] = g.A + (int64_t)ra * g.lda + lch * 8;
+      int rb = min(tn * kTile + lrow + 32 * j, n_valid - 1);
+      if (g.b_rows) rb = g.b_rows[rb];
+      pb[j] = g.B + (int64_t)rb * g.ldb + lch * 8;
+    }
+    const int st_off = lrow * 128 + ((lch ^ swz(lrow)) << 4);  // + 32j*128
+    u32x4 ra_[8], rb_[8];
+    auto gload = [&](int kt) {
+      const int64_t off = (int64_t)kt * kBK;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (kt * kBK + lch * 8 >= K) {
+          ra_[j] = u32x4{0, 0, 0, 0};
+          rb_[j] = u32x4{0, 0, 0, 0};
+        } else {
+          ra_[j] = *(const u32x4*)(pa[j] + off);
+          rb_[j] = *(const u32x4*)(pb[j] + off);
+        }
+      }
+    };
+    auto lstore = [&](int buf) {
+      char* base = smem + buf * kLdsStage;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        *(u32x4*)(base + st_off + j * 32 * 128) = ra_[j];
+        *(u32x4*)(base + kTile * kBK * 2 + st_off + j * 32 * 128) = rb_[j];
+      }
+    };
+    const int nk = (int)ceil_div(K, kBK);
+    for (int kt = 0; kt < nk; ++kt) {
+      gload(kt);
+      lstore(0);
+      __syncthreads();
+      const char* base = smem;
+      static_for<4>([&](auto s) {
+        fload(0, base, s);
+        mfma16(0);
+      });
+      __syncthreads();
+    }
   }
 
   Frag f{tm, tn, wm, wn, lane};
