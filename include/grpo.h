@@ -21,7 +21,9 @@
  *  - Errors that depend on device data (a token id outside [0, V), a
  *    malformed cu_seqlens) cannot be seen on the host. Kernels then record
  *    a flag in the workspace and skip the offending item instead of
- *    trapping; grpo_check_error() reads the flag back.
+ *    trapping; grpo_check_error() reads the flag back. Each call clears the
+ *    flags of its workspace when it starts, so the check reports the most
+ *    recent call that used that workspace.
  *  - Layouts are row-major: hidden [N, H], weight [V, H] (the nn.Linear
  *    layout, one row per vocabulary entry), grad_hidden [N, H],
  *    grad_weight [V, H].
@@ -189,9 +191,9 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
 size_t grpo_workspace_bytes(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V,
                             int64_t num_seqs);
 
-/* Synchronises `stream`, then reads and clears the device error flag kept in
- * the workspace. Returns GRPO_OK, GRPO_ERR_TOKEN_RANGE or GRPO_ERR_SEQLENS
- * (or GRPO_ERR_HIP if a copy fails). */
+/* Synchronises `stream`, then reads and clears the device error flags kept in
+ * the workspace by the most recent call that used it. Returns GRPO_OK,
+ * GRPO_ERR_TOKEN_RANGE or GRPO_ERR_SEQLENS (or GRPO_ERR_HIP if a copy fails). */
 grpo_status grpo_check_error(void* workspace, hipStream_t stream);
 
 /* Static description of a status code. Never NULL. */

@@ -219,7 +219,15 @@ __global__ void __launch_bounds__(256) k_pack_scatter(
   }
 }
 
+// Every entry point starts by clearing the workspace's error words, so that
+// grpo_check_error() reports the most recent call on that workspace.
+__global__ void k_reset_flags(WsHeader* hdr) {
+  hdr->err_token = 0;
+  hdr->err_seqlens = 0;
+}
+
 void launch_pack(const PackArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_reset_flags, dim3(1), dim3(1), 0, s, a.hdr);
   if (a.pidx) {
     hipLaunchKernelGGL(k_fill_i32, dim3((unsigned)ceil_div(a.N, 256)), dim3(256), 0, s, a.pidx,
                        a.N, -1);

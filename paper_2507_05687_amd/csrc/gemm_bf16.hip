@@ -226,6 +226,11 @@ struct EpiStore {
   }
 };
 
+// Distinct types (hence distinct kernel symbols in profiles) for the two
+// gradient products that share the store epilogue.
+struct EpiGradHidden : EpiStore {};
+struct EpiGradWeight : EpiStore {};
+
 // ------------------------------------------------------------ main loop
 // TILED: both operands are in the tiled layout (256x64 blocks, one block
 // per K step, contiguous); otherwise both are row-major with a row stride,
@@ -275,7 +280,7 @@ __global__ void __launch_bounds__(256, 1) k_gemm_bf16(GemmArgs g, Epi epi) {
       });
     });
   };
-  constexpr int kMfma = 0x008, kVmemRead = 0x020, kDsRead = 0x100, kDsWrite = 0x200;
+  constexpr int kMfma = 0x008, kVmemRead = 0x020, kDsRead = 0x100;
   // K step kt reads at +kt*64 (row-major) or +kt*kTileElems (tiled)
   constexpr int kStep = TILED ? kTileElems : kBK;
 
@@ -436,10 +441,13 @@ void launch_gemm_dz(const GemmArgs& g, const int32_t* y_p, const float* lse_p, c
   launch_gemm<EpiDz, false>(g, e, s);
 }
 
-void launch_gemm_store(const GemmArgs& g, const StoreArgs& a, hipStream_t s) {
+void launch_gemm_store(const GemmArgs& g, const StoreArgs& a, bool grad_weight, hipStream_t s) {
   EpiStore e{a.acc_buf, a.ld_acc, a.read_acc, a.out, a.ld_out, a.out_bf16, a.add_out,
              a.out_rows, a.m_limit, a.n_limit};
-  launch_gemm<EpiStore, true>(g, e, s);
+  if (grad_weight)
+    launch_gemm<EpiGradWeight, true>(g, EpiGradWeight{e}, s);
+  else
+    launch_gemm<EpiGradHidden, true>(g, EpiGradHidden{e}, s);
 }
 
 }  // namespace grpo

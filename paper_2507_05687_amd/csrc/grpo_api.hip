@@ -470,7 +470,7 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
       sa.out_rows = rows_p;
       sa.m_limit = L.Npad;
       sa.n_limit = H;
-      TRY(timed(K_GEMM_DH, s, [&] { launch_gemm_store(gh, sa, s); }));
+      TRY(timed(K_GEMM_DH, s, [&] { launch_gemm_store(gh, sa, false, s); }));
     }
     if (grad_weight) {
       // dW[v, :] = sum_t dz[t, v] h[t, :] over the valid tokens
@@ -489,7 +489,7 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
       sa.out_rows = nullptr;
       sa.m_limit = Mc;
       sa.n_limit = H;
-      TRY(timed(K_GEMM_DW, s, [&] { launch_gemm_store(gw, sa, s); }));
+      TRY(timed(K_GEMM_DW, s, [&] { launch_gemm_store(gw, sa, true, s); }));
     }
     if (last) break;
   }

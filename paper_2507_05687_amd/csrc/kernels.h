@@ -43,7 +43,7 @@ void launch_gemm_lse(const GemmArgs& g, const int32_t* y_p, float* zy, float2* m
 void launch_gemm_dz(const GemmArgs& g, const int32_t* y_p, const float* lse_p, const float* g_p,
                     uint16_t* dz, int64_t dz_kt, uint16_t* dzT, int64_t dzT_kt, int64_t V,
                     int64_t v0, hipStream_t s);
-void launch_gemm_store(const GemmArgs& g, const StoreArgs& a, hipStream_t s);
+void launch_gemm_store(const GemmArgs& g, const StoreArgs& a, bool grad_weight, hipStream_t s);
 
 // ------------------------------------------------------------- packing
 struct PackArgs {

@@ -1,0 +1,198 @@
+"""Parity at the benchmark's full sizes (H=4096, V=155136), in the launch
+configuration bench.py times. GPU only.
+
+* fwd+bwd workload (8 prompts x G=8 x 2048 tokens, N=131072): per-token
+  outputs (logp, lse, ell, dL/dlogp, dL/dh rows) of a seeded sample of rows
+  against the oracle, which scores each sampled row over the whole
+  vocabulary; dL/dW through identities that hold at any size.
+* reduced N (256 tokens) at full H and V: dL/dW rows against the oracle.
+* ragged rollouts with all-equal reward groups, and the two-model
+  (policy + reference) scoring sequence, at reduced sizes.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2507_05687_amd import grpo, workloads
+from tests.gpu_util import dev, host64, norm_rel, rel_err, to_dev
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-3
+GRAD_TOL = 5e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _setup():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    oracle.build(force=False)
+    grpo.load()
+    yield
+    grpo.free_workspace()
+    torch.cuda.empty_cache()
+
+
+def _seq_weights(batch, B):
+    m = batch["mask"]
+    cu = batch["cu_seqlens"]
+    counts = np.array([m[cu[b]:cu[b + 1]].sum() for b in range(B)])
+    return oracle.seq_weights(counts), np.repeat(np.arange(B), np.diff(cu))
+
+
+def test_fwdbwd_full_size_sampled_rows_and_identities():
+    w = workloads.WORKLOADS["fwdbwd_bf16"]
+    W_bits = workloads.make_weight(w)
+    h_bits = workloads.make_hidden(w)
+    b = workloads.make_batch(w)
+    N, H, V, B = w.num_tokens, w.hidden, w.vocab, w.num_seqs
+    rows = workloads.sample_rows(b["mask"], 24, seed=1)
+    Wd = oracle.decode(W_bits, "bf16")
+    hs = oracle.decode(h_bits[rows], "bf16")
+    o_lse, o_logp, _ = oracle.score_rows(hs, Wd, b["tokens"][rows])
+    # old/ref: for sampled rows the oracle's log-prob plus noise; for the
+    # others a constant base plus noise (those rows are checked only through
+    # identities, so their exact ratio does not matter)
+    base = np.full(N, -math.log(V))
+    base[rows] = o_logp
+    old = (base + b["old_noise"]).astype(np.float32)
+    ref = (base + b["ref_noise"]).astype(np.float32)
+    adv = oracle.advantages(b["rewards"], w.group).astype(np.float32)
+
+    hd, Wdv = to_dev(h_bits, "bf16"), to_dev(W_bits, "bf16")
+    out = grpo.loss_fwd_bwd(hd, Wdv, dev(b["tokens"]), None, dev(b["cu_seqlens"]), dev(old),
+                            dev(ref), dev(adv), w.clip_eps, w.beta, check=True)
+    torch.cuda.synchronize()
+
+    # per-token outputs of the sampled rows
+    c, seq = _seq_weights(b, B)
+    o_ell, o_g, _ = oracle.token_objective(o_logp, old[rows], ref[rows], adv[seq[rows]],
+                                           c[seq[rows]], None, w.clip_eps, w.beta)
+    assert rel_err(host64(out["logp"])[rows], o_logp) <= TOL
+    assert rel_err(host64(out["lse"])[rows], o_lse) <= TOL
+    tl = host64(out["token_loss"])[rows]
+    assert np.max(np.abs(tl - o_ell)) <= TOL * max(1.0, np.max(np.abs(o_ell)))
+    g = host64(out["dlogp"])[rows]
+    assert np.max(np.abs(g - o_g)) <= TOL * np.max(np.abs(o_g))
+    o_dh = oracle.grad_hidden_rows(hs, Wd, b["tokens"][rows], o_lse, o_g)
+    dh = host64(out["grad_hidden"][torch.from_numpy(rows).cuda()])
+    for i in range(len(rows)):
+        assert norm_rel(dh[i], o_dh[i]) <= GRAD_TOL, (i, norm_rel(dh[i], o_dh[i]))
+    del Wd
+
+    # the loss is the weighted sum of the per-token terms it also returns
+    c_t = torch.from_numpy(c[seq]).cuda()
+    want = float((out["token_loss"].double() * c_t).sum())
+    scale = float((out["token_loss"].double().abs() * c_t).sum())
+    assert abs(out["loss"].item() - want) <= 1e-5 * scale
+
+    # identities of dL/dW that hold at any size:
+    #  sum_v dL/dW_v = sum_t h_t * g_t * (1 - sum_v p_tv) = 0, up to the bf16
+    #  rounding of dz: |.| <= 2^-7 * sum_t |h_t| |g_t| (each dz row sums to 0
+    #  and its absolute sum is at most 2|g_t|)
+    gw = out["grad_weight"]
+    gt = out["dlogp"].double()
+    hf = hd.double()
+    colsum = gw.double().sum(0)
+    bound = 2.0 ** -7 * (hf.abs() * gt.abs()[:, None]).sum(0) + 1e-6
+    assert torch.all(colsum.abs() <= bound), float((colsum.abs() / bound).max())
+    #  <dW, W> = <dh, h> = sum_{t,v} dz_tv z_tv
+    a = float((gw.double() * Wdv.double()).sum())
+    bb = float((out["grad_hidden"].double() * hf).sum())
+    assert abs(a - bb) <= 5e-3 * max(abs(a), abs(bb)), (a, bb)
+    assert torch.isfinite(gw).all() and torch.isfinite(out["grad_hidden"].float()).all()
+
+
+def test_reduced_tokens_full_vocab_grad_weight_rows():
+    w = workloads.scaled(workloads.WORKLOADS["fwdbwd_bf16"], prompts=1, group=4, seq_len=64,
+                         seed=21)
+    W_bits = workloads.make_weight(w)
+    h_bits = workloads.make_hidden(w)
+    b = workloads.make_batch(w)
+    Wd, hd64 = oracle.decode(W_bits, "bf16"), oracle.decode(h_bits, "bf16")
+    o_lse, o_logp, _ = oracle.score_rows(hd64, Wd, b["tokens"])
+    old = (o_logp + b["old_noise"]).astype(np.float32)
+    ref = (o_logp + b["ref_noise"]).astype(np.float32)
+    adv = oracle.advantages(b["rewards"], w.group).astype(np.float32)
+    out = grpo.loss_fwd_bwd(to_dev(h_bits, "bf16"), to_dev(W_bits, "bf16"), dev(b["tokens"]),
+                            dev(b["mask"]), dev(b["cu_seqlens"]), dev(old), dev(ref), dev(adv),
+                            w.clip_eps, w.beta, check=True)
+    c, seq = _seq_weights(b, w.num_seqs)
+    o_ell, o_g, _ = oracle.token_objective(o_logp, old, ref, adv[seq], c[seq], None, w.clip_eps,
+                                           w.beta)
+    assert rel_err(host64(out["logp"]), o_logp) <= TOL
+    abs_sum = float(np.sum(c[seq] * np.abs(o_ell)))
+    assert abs(out["loss"].item() - float(np.sum(c[seq] * o_ell))) <= TOL * abs_sum
+    g = np.random.default_rng(3)
+    vrows = np.unique(np.concatenate([b["tokens"][:16], g.integers(0, w.vocab, 32),
+                                      [0, w.vocab - 1]]))
+    o_dW = oracle.grad_weight_rows(hd64, Wd, b["tokens"], o_lse, o_g, vrows)
+    dW = host64(out["grad_weight"][torch.from_numpy(vrows).cuda()])
+    assert norm_rel(dW, o_dW) <= GRAD_TOL, norm_rel(dW, o_dW)
+    for i in range(len(vrows)):
+        assert norm_rel(dW[i], o_dW[i]) <= 4 * GRAD_TOL, (vrows[i], norm_rel(dW[i], o_dW[i]))
+
+
+def test_ragged_equal_groups_zero_gradient():
+    """Ragged rollouts; groups whose rewards are all equal get A = 0, so with
+    beta = 0 their tokens contribute nothing: dL/dlogp and dL/dh are exactly 0."""
+    w = workloads.scaled(workloads.WORKLOADS["ragged_bf16"], prompts=4, group=4, seq_len=300,
+                         hidden=256, vocab=5000, min_len=16, forced_equal_groups=2, beta=0.0,
+                         seed=31)
+    W_bits, h_bits, b = workloads.make_weight(w), workloads.make_hidden(w), workloads.make_batch(w)
+    adv_dev = grpo.group_advantages(dev(b["rewards"]), w.group)
+    adv = adv_dev.cpu().numpy()
+    assert np.all(adv[:2 * w.group] == 0)
+    hd64, Wd = oracle.decode(h_bits, "bf16"), oracle.decode(W_bits, "bf16")
+    _, o_logp, _ = oracle.score_rows(hd64, Wd, b["tokens"])
+    old = (o_logp + b["old_noise"]).astype(np.float32)
+    out = grpo.loss_fwd_bwd(to_dev(h_bits, "bf16"), to_dev(W_bits, "bf16"), dev(b["tokens"]),
+                            dev(b["mask"]), dev(b["cu_seqlens"]), dev(old), None, adv_dev,
+                            w.clip_eps, 0.0, check=True)
+    eq_rows = np.arange(b["cu_seqlens"][2 * w.group])
+    assert np.all(out["dlogp"].cpu().numpy()[eq_rows] == 0)
+    assert torch.all(out["grad_hidden"][:len(eq_rows)] == 0)
+    o = oracle.grpo_loss(hd64, Wd, b["tokens"], b["mask"], b["cu_seqlens"], old.astype(np.float64),
+                         old.astype(np.float64), adv.astype(np.float64), w.clip_eps, 0.0)
+    assert norm_rel(host64(out["grad_weight"]), o["dW"]) <= GRAD_TOL
+    assert norm_rel(host64(out["grad_hidden"]), o["dh"]) <= GRAD_TOL
+
+
+def test_double_scoring_sequence():
+    """Policy and reference scoring, then the loss on the policy reusing the
+    policy's log-sum-exp (the two-model GRPO step), at reduced size."""
+    w = workloads.scaled(workloads.WORKLOADS["double_bf16"], prompts=2, group=4, seq_len=64,
+                         hidden=512, vocab=6000, seed=41)
+    Wp, Wr = workloads.make_weight(w, "policy"), workloads.make_weight(w, "reference")
+    h_bits, b = workloads.make_hidden(w), workloads.make_batch(w)
+    hd = to_dev(h_bits, "bf16")
+    Wpd, Wrd = to_dev(Wp, "bf16"), to_dev(Wr, "bf16")
+    y = dev(b["tokens"])
+    lp_pol, lse_pol = grpo.logprob_fwd(hd, Wpd, y)
+    lp_ref, _ = grpo.logprob_fwd(hd, Wrd, y)
+    h64 = oracle.decode(h_bits, "bf16")
+    o_lse_p, o_lp_p, _ = oracle.score_rows(h64, oracle.decode(Wp, "bf16"), b["tokens"])
+    _, o_lp_r, _ = oracle.score_rows(h64, oracle.decode(Wr, "bf16"), b["tokens"])
+    assert rel_err(host64(lp_pol), o_lp_p) <= TOL
+    assert rel_err(host64(lp_ref), o_lp_r) <= TOL
+    # the loss step takes old = policy log-prob and ref = reference log-prob
+    old, ref = o_lp_p.astype(np.float32), o_lp_r.astype(np.float32)
+    adv = oracle.advantages(b["rewards"], w.group).astype(np.float32)
+    out = grpo.loss_fwd_bwd(hd, Wpd, y, None, dev(b["cu_seqlens"]), dev(old), dev(ref), dev(adv),
+                            w.clip_eps, w.beta, lse_in=lse_pol, check=True)
+    o = oracle.grpo_loss(h64, oracle.decode(Wp, "bf16"), b["tokens"], None, b["cu_seqlens"],
+                         old.astype(np.float64), ref.astype(np.float64), adv.astype(np.float64),
+                         w.clip_eps, w.beta)
+    assert rel_err(host64(out["logp"]), o["logp"]) <= TOL
+    c, seq = _seq_weights(b, w.num_seqs)
+    abs_sum = float(np.sum(c[seq] * np.abs(o["ell"])))
+    assert abs(out["loss"].item() - o["loss"]) <= TOL * max(abs(o["loss"]), abs_sum)
+    assert norm_rel(host64(out["grad_weight"]), o["dW"]) <= GRAD_TOL
+    assert norm_rel(host64(out["grad_hidden"]), o["dh"]) <= GRAD_TOL
+    # on policy: rho = exp(logp - old) is 1 up to the difference between the
+    # device's and the oracle's log-prob
+    rho = np.exp(host64(out["logp"]) - old)
+    assert np.max(np.abs(rho - 1)) <= 1e-3
