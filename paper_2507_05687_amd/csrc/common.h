@@ -30,14 +30,20 @@ constexpr int kTileElems = kTile * kBK;  // elements of one 256x64 block of the 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 __host__ __device__ inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
 
-// fp32 -> bf16 bits, round to nearest even (finite and infinite inputs; NaN stays NaN).
-__device__ inline uint16_t f32_to_bf16_bits(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (uint16_t)((u >> 16) | 0x40);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// fp32 -> bf16, round to nearest even, with gfx950's packed conversion
+// instruction: two values -> one 32-bit word (first value in the low half).
+__device__ __forceinline__ uint32_t bf16_pack2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{a, b}), bf16x2_t));
+}
+__device__ __forceinline__ uint16_t bf16_bits(float a) {
+  return __builtin_bit_cast(uint16_t, (__bf16)a);
 }
 __device__ inline float bf16_bits_to_f32(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+constexpr float kLog2e = 1.4426950408889634f;
 
 
 // Calls f(std::integral_constant<int, i>) for i = 0..N-1, unrolled at compile

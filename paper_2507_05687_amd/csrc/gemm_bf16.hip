@@ -43,6 +43,10 @@ constexpr int kLdsStage = 2 * kTile * kBK * 2;  // bytes of one A+B stage (64 Ki
 
 __device__ inline int swz(int row) { return (row >> GRPO_SWZ_SHIFT) & 7; }
 
+// s_waitcnt immediate that waits for LDS/scalar-memory counters only
+// (vmcnt and expcnt left at their maxima).
+constexpr int kWaitLgkmOnly = 0xC07F;
+
 typedef __attribute__((address_space(1))) void* glb_ptr_t;
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -99,10 +103,11 @@ struct EpiLse {
         });
       });
       float s = 0.f;
+      const float m2l = m * kLog2e;
       static_for<4>([&](auto mi) {
         static_for<16>([&](auto r) {
           constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
-          if (o < vlim) s += __expf(acc[mi][ni][r.value] - m);
+          if (o < vlim) s += __builtin_amdgcn_exp2f(fmaf(acc[mi][ni][r.value], kLog2e, -m2l));
           if (o == y) zy[t] = acc[mi][ni][r.value];
         });
       });
@@ -146,8 +151,7 @@ struct EpiDz {
   int64_t v0;      // first vocabulary row of this chunk
 
   __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], const Frag& f, int m_valid,
-                                             int n_valid,
-                             char*) const {
+                                             int n_valid, char*) const {
     const int hi = (f.lane >> 5) * 4;
     const int64_t vbase = v0 + (int64_t)f.tm * kTile + f.wm * 128 + hi;
     const int vlim = (int)((V - vbase) < (1 << 20) ? (V - vbase) : (1 << 20));
@@ -155,7 +159,8 @@ struct EpiDz {
       const int64_t t = (int64_t)f.tn * kTile + f.col(ni);
       const bool tv = t < n_valid;
       const int y = tv ? (int)(y_p[t] - vbase) : -1;  // y as a row offset of this lane
-      const float l = tv ? lse_p[t] : 0.f;
+      // p = exp(z - lse) = exp2(z*log2e - lse*log2e); invalid columns get g = 0
+      const float l2 = tv ? lse_p[t] * kLog2e : 0.f;
       const float g = tv ? g_p[t] : 0.f;
       // element (t, vl) of dz lives at tile (t/256, vl/64), row t%256, column vl%64
       uint16_t* pz = dz + ((t >> 8) * dz_kt + f.tm * 4 + f.wm * 2) * kTileElems + (t & 255) * 64 + hi;
@@ -165,17 +170,23 @@ struct EpiDz {
                           : nullptr;
       static_for<4>([&](auto mi) {
         static_for<4>([&](auto q) {
-          uint32_t b[4];
+          float d[4];
           static_for<4>([&](auto e) {
             constexpr int r = q * 4 + e;
             constexpr int o = mi * 32 + q * 8 + e;
-            float d = 0.f;
-            if (tv && o < vlim) d = g * ((o == y ? 1.f : 0.f) - __expf(acc[mi][ni][r] - l));
-            b[e] = f32_to_bf16_bits(d);
-            if (pzt) pzt[o * 64] = (uint16_t)b[e];
+            const float p = __builtin_amdgcn_exp2f(fmaf(acc[mi][ni][r], kLog2e, -l2));
+            const float dv = g * ((o == y ? 1.f : 0.f) - p);
+            d[e] = o < vlim ? dv : 0.f;
           });
-          uint2 pk = make_uint2(b[0] | (b[1] << 16), b[2] | (b[3] << 16));
-          *(uint2*)(pz + (mi >> 1) * kTileElems + (mi & 1) * 32 + q * 8) = pk;
+          const uint32_t w0 = bf16_pack2(d[0], d[1]), w1 = bf16_pack2(d[2], d[3]);
+          if (pzt) {
+            constexpr int o = mi * 32 + q * 8;
+            pzt[o * 64] = (uint16_t)w0;
+            pzt[(o + 1) * 64] = (uint16_t)(w0 >> 16);
+            pzt[(o + 2) * 64] = (uint16_t)w1;
+            pzt[(o + 3) * 64] = (uint16_t)(w1 >> 16);
+          }
+          *(uint2*)(pz + (mi >> 1) * kTileElems + (mi & 1) * 32 + q * 8) = make_uint2(w0, w1);
         });
       });
     });
@@ -183,7 +194,7 @@ struct EpiDz {
 };
 
 struct EpiStore {
-  float* acc_buf;        // fp32 accumulation buffer [M][ld_acc] (tile-local rows)
+  float* acc_buf;        // fp32 accumulation buffer; every row/column of every tile exists
   int64_t ld_acc;
   int read_acc;          // add the buffer's current value
   void* out;             // final output (NULL: write acc_buf instead)
@@ -195,33 +206,91 @@ struct EpiStore {
   int64_t n_limit;       // columns >= n_limit are not stored
 
   __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], const Frag& f, int m_valid,
-                                             int n_valid,
-                             char*) const {
+                                             int n_valid, char*) const {
     const int64_t mlim = m_limit < m_valid ? m_limit : m_valid;
-    const int64_t mbase = (int64_t)f.tm * kTile + f.wm * 128 + (f.lane >> 5) * 4;
-    static_for<4>([&](auto mi) {
-      static_for<16>([&](auto r) {
-        constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
-        const int64_t m = mbase + o;
-        if (m < mlim) {
-          const int64_t orow = out_rows ? (int64_t)out_rows[m] : m;
-          static_for<4>([&](auto ni) {
-            const int64_t n = (int64_t)f.tn * kTile + f.col(ni);
-            if (n < n_limit) {
-              float x = acc[mi][ni][r.value];
-              if (read_acc) x += acc_buf[m * ld_acc + n];
-              if (out == nullptr) {
-                acc_buf[m * ld_acc + n] = x;
-              } else if (out_bf16) {
-                ((uint16_t*)out)[orow * ld_out + n] = f32_to_bf16_bits(x);
-              } else {
-                float* o2 = (float*)out + orow * ld_out + n;
-                *o2 = add_out ? *o2 + x : x;
-              }
-            }
+    const int64_t m0 = (int64_t)f.tm * kTile + f.wm * 128 + (f.lane >> 5) * 4;
+    const int64_t n0 = (int64_t)f.tn * kTile + f.wn * 128 + (f.lane & 31);
+    const bool full = (int64_t)f.tm * kTile + kTile <= mlim &&
+                      (int64_t)f.tn * kTile + kTile <= n_limit;
+    float* pacc = acc_buf ? acc_buf + m0 * ld_acc + n0 : nullptr;
+    // Batches of 32 values (8 rows x 4 columns of this lane): each batch is
+    // loaded, combined and stored before the next starts, so the loads of a
+    // batch are in flight together and its registers die right after.
+    // (mi, r) -> row offset mi*32 + (r/4)*8 + r%4; ni -> column offset ni*32.
+    static_for<8>([&](auto bq) {
+      constexpr int mi = bq / 2, r0 = (bq % 2) * 8;
+      float v[8][4];
+      static_for<8>([&](auto rr) {
+        static_for<4>([&](auto ni) { v[rr][ni] = acc[mi][ni][r0 + rr]; });
+      });
+      if (read_acc) {  // the accumulation buffer holds every row/column of the tile
+        float prev[8][4];
+        static_for<8>([&](auto rr) {
+          constexpr int r = r0 + rr;
+          constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
+          const float* pr = pacc + o * ld_acc;
+          static_for<4>([&](auto ni) { prev[rr][ni] = pr[ni * 32]; });
+        });
+        static_for<8>([&](auto rr) {
+          static_for<4>([&](auto ni) { v[rr][ni] += prev[rr][ni]; });
+        });
+      }
+      if (out == nullptr) {
+        static_for<8>([&](auto rr) {
+          constexpr int r = r0 + rr;
+          constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
+          float* pr = pacc + o * ld_acc;
+          static_for<4>([&](auto ni) { pr[ni * 32] = v[rr][ni]; });
+        });
+      } else if (full) {
+        int64_t orow[8];
+        static_for<8>([&](auto rr) {
+          constexpr int r = r0 + rr;
+          constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
+          orow[rr] = (out_rows ? (int64_t)out_rows[m0 + o] : m0 + o) * ld_out + n0;
+        });
+        if (out_bf16) {
+          uint16_t* ob = (uint16_t*)out;
+          static_for<8>([&](auto rr) {
+            static_for<4>([&](auto ni) { ob[orow[rr] + ni * 32] = bf16_bits(v[rr][ni]); });
+          });
+        } else {
+          float* of = (float*)out;
+          if (add_out) {
+            float prev[8][4];
+            static_for<8>([&](auto rr) {
+              static_for<4>([&](auto ni) { prev[rr][ni] = of[orow[rr] + ni * 32]; });
+            });
+            static_for<8>([&](auto rr) {
+              static_for<4>([&](auto ni) { v[rr][ni] += prev[rr][ni]; });
+            });
+          }
+          static_for<8>([&](auto rr) {
+            static_for<4>([&](auto ni) { of[orow[rr] + ni * 32] = v[rr][ni]; });
           });
         }
-      });
+      } else {  // edge tile: per-element bounds
+        static_for<8>([&](auto rr) {
+          constexpr int r = r0 + rr;
+          constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
+          const int64_t m = m0 + o;
+          if (m < mlim) {
+            const int64_t orow = out_rows ? (int64_t)out_rows[m] : m;
+            static_for<4>([&](auto ni) {
+              const int64_t n = n0 + ni * 32;
+              if (n < n_limit) {
+                if (out_bf16) {
+                  ((uint16_t*)out)[orow * ld_out + n] = bf16_bits(v[rr][ni]);
+                } else {
+                  float* o2 = (float*)out + orow * ld_out + n;
+                  *o2 = add_out ? *o2 + v[rr][ni] : v[rr][ni];
+                }
+              }
+            });
+          }
+        });
+      }
+      __builtin_amdgcn_sched_barrier(0);
     });
   }
 };

@@ -142,7 +142,8 @@ Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_
       L.WT = take(c, 2 * Hpad * L.Vpad);
       L.dz = take(c, 2 * L.Npad * L.Vc);
       L.dzT = take(c, 2 * L.Vc * L.Npad);
-      if (L.nchunks > 1) L.dhacc = take(c, 4 * L.Npad * H);
+      // fp32 dh accumulator with every row and column of every tile present
+      if (L.nchunks > 1) L.dhacc = take(c, 4 * L.Npad * Hpad);
     }
   }
   L.total = c;
@@ -461,7 +462,7 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
       gh.b_kb0 = v0 / kBK;
       StoreArgs sa{};
       sa.acc_buf = dhacc;
-      sa.ld_acc = H;
+      sa.ld_acc = round_up(H, kTile);
       sa.read_acc = c > 0;
       sa.out = last ? grad_hidden : nullptr;
       sa.ld_out = H;
