@@ -273,3 +273,15 @@ def test_token_out_of_range_sets_flag():
     # the next call on the same workspace starts clean
     b["tokens"][7] = 0
     _run_loss(w, W, h, b, adv, old, ref)
+
+
+def test_all_rows_masked():
+    """No valid row at all: loss, per-token outputs and both gradients are 0
+    (the weight-gradient contraction then has K = 0)."""
+    kw = dict(SMALL["ragged_tiles"], dtype="bf16", rms_norm_hidden=True, seed=19)
+    w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    b["mask"][:] = 0
+    out = _run_loss(w, W, h, b, adv, old, ref)
+    assert out["loss"].item() == 0.0
+    assert torch.all(out["logp"] == 0) and torch.all(out["dlogp"] == 0)
+    assert torch.all(out["grad_hidden"] == 0) and torch.all(out["grad_weight"] == 0)
