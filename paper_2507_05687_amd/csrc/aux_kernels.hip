@@ -463,7 +463,8 @@ __global__ void __launch_bounds__(256) k_transpose_tiled(const uint16_t* __restr
     int kk = t >> 2, c0 = (t & 3) * 16;
     int64_t k = k0 + kk;
     if (k < K) {
-      uint16_t* p = out + ((k >> 8) * (n_pad >> 6) + (i0 >> 6)) * kTileElems + (k & 255) * 64 + c0;
+      const int64_t i = i0 + c0;  // 16 consecutive columns, within one 32-wide block
+      uint16_t* p = out + ((k >> 8) * (n_pad >> 5) + (i >> 5)) * kTileElems + (k & 255) * 32 + (i & 31);
       u32x4 a, b;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -474,6 +475,53 @@ __global__ void __launch_bounds__(256) k_transpose_tiled(const uint16_t* __restr
       *(u32x4*)(p + 8) = b;
     }
   }
+}
+
+// --------------------------------------- row-major rows -> tiled layout
+// One workgroup per 256 x 32 output block; thread t writes 16 bytes of rows
+// t/4 + 64i (i = 0..3), chunk t%4, so that the block is written contiguously
+// and each source row is read as one 64-byte piece.
+__global__ void __launch_bounds__(256) k_tile_rows(const uint16_t* __restrict__ in, int64_t ld_in,
+                                                   const int32_t* __restrict__ rows,
+                                                   int64_t n_static,
+                                                   const WsHeader* __restrict__ hdr, int64_t K,
+                                                   int64_t kb_per_row,
+                                                   uint16_t* __restrict__ out) {
+  const int64_t blk = blockIdx.x;
+  const int64_t rb = blk / kb_per_row, kb = blk - rb * kb_per_row;
+  const int64_t nvalid = hdr ? (int64_t)hdr->num_valid : n_static;
+  const int t = threadIdx.x;
+  const int64_t k0 = kb * 32 + (t & 3) * 8;
+  uint16_t* ob = out + blk * kTileElems + (t & 3) * 8;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = (t >> 2) + 64 * i;
+    const int64_t row = rb * 256 + r;
+    u32x4 v = {0, 0, 0, 0};
+    if (row < nvalid) {
+      const uint16_t* p = in + (rows ? (int64_t)rows[row] : row) * ld_in + k0;
+      if (k0 + 8 <= K) {
+        v = *(const u32x4*)p;
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          uint32_t lo = k0 + 2 * q < K ? p[2 * q] : 0;
+          uint32_t hi = k0 + 2 * q + 1 < K ? p[2 * q + 1] : 0;
+          v[q] = lo | (hi << 16);
+        }
+      }
+    }
+    *(u32x4*)(ob + r * 32) = v;
+  }
+}
+
+void launch_tile_rows(const uint16_t* in, int64_t ld_in, const int32_t* rows, int64_t n_static,
+                      const WsHeader* hdr, int64_t r_pad, int64_t K, uint16_t* out,
+                      hipStream_t s) {
+  const int64_t kb_per_row = ceil_div(K, 32);
+  const int64_t blocks = r_pad / 256 * kb_per_row;
+  hipLaunchKernelGGL(k_tile_rows, dim3((unsigned)blocks), dim3(256), 0, s, in, ld_in, rows,
+                     n_static, hdr, K, kb_per_row, out);
 }
 
 // n_pad must be a multiple of 64; `out` holds round_up(K, 256) x n_pad elements.

@@ -24,8 +24,11 @@ struct WsHeader {
 };
 
 constexpr int kTile = 256;  // GEMM tile edge (rows and columns)
-constexpr int kBK = 64;     // GEMM K step
-constexpr int kTileElems = kTile * kBK;  // elements of one 256x64 block of the tiled layout
+constexpr int kBK = 32;     // GEMM K step = column width of a tiled-layout block
+// Tiled layout of a GEMM operand with R rows and K columns: blocks of 256 rows
+// x 32 columns (16 KiB of bf16, rows of 64 bytes), block (rb, kb) at
+// (rb * ceil(K/32) + kb) * kTileElems elements; padding rows and columns are 0.
+constexpr int kTileElems = kTile * kBK;
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 __host__ __device__ inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }

@@ -10,18 +10,8 @@
 //   EpiStore dL/dh = dz . W and dL/dW = dz^T . h: fp32 stores, optionally
 //            accumulating, gathering output rows, or converting to bf16.
 //
-// Tiling: one 256-thread workgroup (4 waves of 64) per 256x256 output tile;
-// each wave owns a 128x128 quarter as a 4x4 grid of 32x32x16 bf16 MFMA
-// blocks (256 fp32 accumulators per lane). K advances 64 at a time through a
-// double-buffered LDS stage of 2 x (256x64 A + 256x64 B) bf16 = 128 KiB.
-// LDS rows are 128 bytes; the eight 16-byte chunks of a row are XOR-swizzled
-// by a few row bits so that the MFMA fragment reads hit distinct banks.
-//
-// Operands come row-major (the caller's hidden states and LM head) or in the
-// tiled layout that the library writes for its own intermediates: 256-row x
-// 64-column blocks stored contiguously, block (rb, kb) at
-// (rb * blocks_per_row + kb) * 16384 elements. A K step of a tile then reads
-// one contiguous 32 KiB block per operand.
+// Tiling: one 512-thread workgroup per 256x256 output tile, K in steps of
+// 32 from operands in the library's tiled layout (see the main loop).
 //
 // Tile order: workgroup ids are dealt round-robin to the 8 XCDs, so id
 // b runs on XCD b % 8. Tiles are assigned so that each XCD owns a band of
@@ -35,17 +25,9 @@ namespace grpo {
 
 constexpr int kGM = 4;  // tile-rows per XCD band
 constexpr int kGN = 8;  // tile-columns per step of the walk
-constexpr int kLdsStage = 2 * kTile * kBK * 2;  // bytes of one A+B stage (64 KiB)
-
-#ifndef GRPO_SWZ_SHIFT
-#define GRPO_SWZ_SHIFT 1
-#endif
-
-__device__ inline int swz(int row) { return (row >> GRPO_SWZ_SHIFT) & 7; }
-
-// s_waitcnt immediate that waits for LDS/scalar-memory counters only
-// (vmcnt and expcnt left at their maxima).
-constexpr int kWaitLgkmOnly = 0xC07F;
+// s_waitcnt immediate: vmcnt <= n (6 bits, split over [3:0] and [15:14]),
+// expcnt left at its maximum (7 in [6:4]), lgkmcnt 0 ([11:8]).
+constexpr int wait_vm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0070; }
 
 typedef __attribute__((address_space(1))) void* glb_ptr_t;
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
@@ -145,7 +127,7 @@ struct EpiDz {
   const int32_t* y_p;
   const float* lse_p;
   const float* g_p;
-  uint16_t* dz;    // tiled [tokens][chunk vocabulary], dz_kt 64-wide blocks per tile-row
+  uint16_t* dz;    // tiled [tokens][chunk vocabulary], dz_kt 32-wide blocks per tile-row
   int64_t dz_kt;
   uint16_t* dzT;   // tiled [chunk vocabulary][tokens] (may be NULL), dzT_kt blocks per tile-row
   int64_t dzT_kt;
@@ -165,11 +147,11 @@ struct EpiDz {
       // p = exp(z - lse) = exp2(z*log2e - lse*log2e); invalid columns get g = 0
       const float l2 = tv ? lse_p[t] * kLog2e : 0.f;
       const float g = tv ? g_p[t] : 0.f;
-      // element (t, vl) of dz lives at tile (t/256, vl/64), row t%256, column vl%64
-      uint16_t* pz = dz + ((t >> 8) * dz_kt + f.tm * 4 + f.wm * 2) * kTileElems + (t & 255) * 64 + hi;
-      // element (vl, t) of dzT lives at tile (vl/256, t/64), row vl%256, column t%64
-      uint16_t* pzt = dzT ? dzT + ((int64_t)f.tm * dzT_kt + (t >> 6)) * kTileElems + (t & 63) +
-                                (f.wm * 128 + hi) * 64
+      // element (t, vl) of dz lives in block (t/256, vl/32), row t%256, column vl%32
+      uint16_t* pz = dz + ((t >> 8) * dz_kt + f.tm * 8 + f.wm * 4) * kTileElems + (t & 255) * 32 + hi;
+      // element (vl, t) of dzT lives in block (vl/256, t/32), row vl%256, column t%32
+      uint16_t* pzt = dzT ? dzT + ((int64_t)f.tm * dzT_kt + (t >> 5)) * kTileElems + (t & 31) +
+                                (f.wm * 128 + hi) * 32
                           : nullptr;
       static_for<4>([&](auto mi) {
         static_for<4>([&](auto q) {
@@ -184,12 +166,12 @@ struct EpiDz {
           const uint32_t w0 = bf16_pack2(d[0], d[1]), w1 = bf16_pack2(d[2], d[3]);
           if (pzt) {
             constexpr int o = mi * 32 + q * 8;
-            pzt[o * 64] = (uint16_t)w0;
-            pzt[(o + 1) * 64] = (uint16_t)(w0 >> 16);
-            pzt[(o + 2) * 64] = (uint16_t)w1;
-            pzt[(o + 3) * 64] = (uint16_t)(w1 >> 16);
+            pzt[o * 32] = (uint16_t)w0;
+            pzt[(o + 1) * 32] = (uint16_t)(w0 >> 16);
+            pzt[(o + 2) * 32] = (uint16_t)w1;
+            pzt[(o + 3) * 32] = (uint16_t)(w1 >> 16);
           }
-          *(uint2*)(pz + (mi >> 1) * kTileElems + (mi & 1) * 32 + q * 8) = make_uint2(w0, w1);
+          *(uint2*)(pz + mi * kTileElems + q * 8) = make_uint2(w0, w1);
         });
       });
     });
@@ -305,42 +287,45 @@ struct EpiGradHidden : EpiStore {};
 struct EpiGradWeight : EpiStore {};
 
 // ------------------------------------------------------------ main loop
-// TILED: both operands are in the tiled layout (256x64 blocks, one block
-// per K step, contiguous); otherwise both are row-major with a row stride,
-// and B rows may be gathered through b_rows.
+// Both operands are in the tiled layout: tile-row r of an operand is a run
+// of 256 x 32 blocks (16 KiB each, rows of 64 bytes), block kb of it at
+// (r * kt + kb0 + kb) * 8192 elements. One K step (32) of a tile is then
+// one contiguous 16 KiB block per operand, and each 1 KiB load instruction
+// of a wave covers eight whole 128-byte lines.
 //
-// WN is the width of one wave's output block: 128 (4 waves, one per SIMD,
-// 4x4 MFMA blocks and 256 accumulators each) or 64 (8 waves, two per SIMD,
-// 4x2 blocks and 128 accumulators each, so that one wave's MFMAs can run
-// while the other waits on LDS or a barrier).
-template <class Epi, bool KTAIL, bool TILED, int WN>
-__global__ void __launch_bounds__(64 * 2 * (kTile / WN), 1) k_gemm_bf16(GemmArgs g, Epi epi) {
-  constexpr int NI = WN / 32;               // MFMA blocks per wave along N
-  constexpr int kWaves = 2 * (kTile / WN);  // 4 or 8
-  constexpr int kJ = 32 / kWaves;           // 1 KiB LDS loads per operand per wave per step
-  // 8 waves: ring of 5 stages of K = 32 (5 x 32 KiB); 4 waves: 2 stages of K = 64
-  constexpr int kSmem = kWaves == 8 && !KTAIL ? 5 * 2 * kTile * 64 : 2 * kLdsStage;
-  __shared__ __attribute__((aligned(16))) char smem[kSmem];
+// Eight waves of 64 (two per SIMD); wave w owns rows (w%2)*128 and columns
+// (w/2)*64 of the tile as 4 x 2 blocks of 32x32x16 MFMAs (128 fp32
+// accumulators per lane), so that one wave's MFMAs can run while the other
+// wave of its SIMD waits on LDS, a load or a barrier.
+//
+// LDS is a ring of 5 stages of 32 KiB (A block + B block of one K step).
+// After the barrier of step kt every wave has read step kt, so its stage
+// receives step kt+5; those four loads per wave are spread over the MFMAs
+// up to the next barrier (one per four MFMAs), which keeps the load
+// pipeline fed without stalling MFMA issue on a full load queue, and each
+// step is requested about four steps before it is read.
+constexpr int kWaves = 8;
+constexpr int kWN = 64;                    // columns per wave
+constexpr int kNI = kWN / 32;              // MFMA blocks per wave along N
+constexpr int kStage = 2 * kTileElems * 2; // bytes of one A + B stage
+constexpr int kStages = 5;
+constexpr int kJ = kTileElems * 2 / 1024 / kWaves;  // 1 KiB loads per operand per wave per step
+
+template <class Epi>
+__global__ void __launch_bounds__(64 * kWaves, 1) k_gemm_bf16(GemmArgs g, Epi epi) {
+  constexpr int NI = kNI;
+  __shared__ __attribute__((aligned(16))) char smem[kStages * kStage];
   int tm, tn;
   if (!tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn)) return;
-  int m_valid = g.m_dev ? min(*g.m_dev, g.M) : g.M;
-  int n_valid = g.n_dev ? min(*g.n_dev, g.N) : g.N;
+  const int m_valid = g.m_dev ? min(*g.m_dev, g.M) : g.M;
+  const int n_valid = g.n_dev ? min(*g.n_dev, g.N) : g.N;
   if (tm * kTile >= m_valid || tn * kTile >= n_valid) return;
-  int K = g.k_dev ? (int)round_up(*g.k_dev, kBK) : g.K;
+  const int K = g.k_dev ? (int)round_up(*g.k_dev, kBK) : g.K;
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, w = tid >> 6;
-  // wave -> output block: rows wm*128, columns wn*WN. With 8 waves, waves w
-  // and w+4 share a SIMD and belong to different groups (see below).
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = w & 1, wn = w >> 1;
-
-  // ---- fragment reads: lane reads row (l%32) of each 32-row block, chunk 2s + l/32
-  const int fr = lane & 31;
-  const int rd_base_a = (wm * 128 + fr) * 128;
-  const int rd_base_b = kTile * kBK * 2 + (wn * WN + fr) * 128;
-  int rd_ch[4];
-#pragma unroll
-  for (int s = 0; s < 4; ++s) rd_ch[s] = ((2 * s + (lane >> 5)) ^ swz(fr)) << 4;
 
   f32x16 acc[4][NI];
   static_for<4>([&](auto i) {
@@ -350,300 +335,138 @@ __global__ void __launch_bounds__(64 * 2 * (kTile / WN), 1) k_gemm_bf16(GemmArgs
     });
   });
 
+  // ---- loads: the j-th load of lane l of wave w fills stage row
+  // q = 16*(w + 8j) + l/4 at physical chunk l%4, i.e. logical chunk
+  // (l%4) ^ ((q/4)%4); one instruction writes 1 KiB of consecutive LDS.
+  const int qrow = 16 * w + (lane >> 2);
+  const int qch = (lane & 3) ^ ((qrow >> 2) & 3);  // the same for q + 128j
+  const uint16_t* pa = g.A + ((int64_t)tm * g.a_kt + g.a_kb0) * kTileElems + qrow * 32 + qch * 8;
+  const uint16_t* pb = g.B + ((int64_t)tn * g.b_kt + g.b_kb0) * kTileElems + qrow * 32 + qch * 8;
+  // load l of a step: l < kJ is A part l, else B part l - kJ
+  auto load = [&](const uint16_t* a_step, const uint16_t* b_step, char* la, auto l) {
+    if constexpr (l.value < kJ)
+      __builtin_amdgcn_global_load_lds((glb_ptr_t)(a_step + l.value * 16 * kWaves * 32),
+                                       (lds_ptr_t)(la + l.value * 1024 * kWaves), 16, 0, 0);
+    else
+      __builtin_amdgcn_global_load_lds(
+          (glb_ptr_t)(b_step + (l.value - kJ) * 16 * kWaves * 32),
+          (lds_ptr_t)(la + kTileElems * 2 + (l.value - kJ) * 1024 * kWaves), 16, 0, 0);
+  };
+  auto load_step = [&](int kt, int stage) {
+    char* la = smem + stage * kStage + w * 1024;
+    static_for<2 * kJ>([&](auto l) {
+      load(pa + (int64_t)kt * kTileElems, pb + (int64_t)kt * kTileElems, la, l);
+    });
+  };
+
+  // ---- fragment reads: lane reads row l%32 of each 32-row block, logical
+  // chunk 2t + l/32 for sub-step t (K 16t .. 16t+15)
+  const int fr = lane & 31;
+  const int rd_a = (wm * 128 + fr) * 64;
+  const int rd_b = kTileElems * 2 + (wn * kWN + fr) * 64;
+  int rd_ch[2];
+  static_for<2>([&](auto t) { rd_ch[t] = ((2 * t + (lane >> 5)) ^ ((fr >> 2) & 3)) << 4; });
   bf16x8 fa[2][4], fb[2][NI];
-  auto fload = [&](int slot, const char* base, int s) {
-    static_for<4>([&](auto i) {
-      fa[slot][i] = *(const bf16x8*)(base + rd_base_a + i * 32 * 128 + rd_ch[s]);
-    });
-    static_for<NI>([&](auto i) {
-      fb[slot][i] = *(const bf16x8*)(base + rd_base_b + i * 32 * 128 + rd_ch[s]);
+  // fragment r (A blocks first, then B blocks) of sub-step t of step kt
+  auto fread = [&](auto slot, int kt, int t, auto r) {
+    const char* base = smem + (kt % kStages) * kStage;
+    if constexpr (r.value < 4)
+      fa[slot.value][r.value] = *(const bf16x8*)(base + rd_a + r.value * 32 * 64 + rd_ch[t]);
+    else
+      fb[slot.value][r.value - 4] =
+          *(const bf16x8*)(base + rd_b + (r.value - 4) * 32 * 64 + rd_ch[t]);
+  };
+  constexpr int kReads = 4 + NI;  // fragment reads per sub-step
+  auto fread_half = [&](auto slot, int kt, int t, auto h) {
+    static_for<kReads>([&](auto r) {
+      if constexpr ((r.value < kReads / 2) == (h.value == 0)) fread(slot, kt, t, r);
     });
   };
-  auto mfma_sub = [&](int slot) {
-    static_for<4>([&](auto i) {
-      static_for<NI>([&](auto j) {
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][i], fb[slot][j], acc[i][j],
-                                                            0, 0, 0);
-      });
-    });
+  auto mfma = [&](auto slot, auto m) {
+    constexpr int i = m.value / NI, j = m.value % NI;
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot.value][i], fb[slot.value][j],
+                                                        acc[i][j], 0, 0, 0);
   };
-  constexpr int kMfma = 0x008, kVmem = 0x010, kDsRead = 0x100;
-  constexpr int kSubMfma = 4 * NI, kSubReads = 4 + NI;
-  // K step kt reads at +kt*64 (row-major) or +kt*kTileElems (tiled)
-  constexpr int kStep = TILED ? kTileElems : kBK;
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  constexpr int kMfmas = 4 * NI;                  // MFMAs per sub-step
+  constexpr int kSpread = kMfmas / kJ;            // MFMAs per load
+  constexpr int kPerStep = 2 * kJ;                // loads per wave per step
 
-  if constexpr (!KTAIL) {
-    // ---- global -> LDS directly (no register staging). The j-th load of
-    // lane l of wave w fills LDS row r = 8*(w + kWaves*j) + l/8 at physical
-    // chunk l%8, i.e. logical chunk (l%8) ^ swz(r); one load instruction of
-    // a wave writes 1 KiB of consecutive LDS.
-    const int drow = 8 * w + (lane >> 3);
-    const int dch = (lane & 7) ^ swz(drow);  // swz(drow + 8*kWaves*j) == swz(drow)
-    const uint16_t* sa[kJ];
-    const uint16_t* sb[kJ];
-    if (TILED) {
-      const uint16_t* a0 =
-          g.A + ((int64_t)tm * g.a_kt + g.a_kb0) * kTileElems + drow * 64 + dch * 8;
-      const uint16_t* b0 =
-          g.B + ((int64_t)tn * g.b_kt + g.b_kb0) * kTileElems + drow * 64 + dch * 8;
-#pragma unroll
-      for (int j = 0; j < kJ; ++j) {
-        sa[j] = a0 + j * (8 * kWaves * 64);
-        sb[j] = b0 + j * (8 * kWaves * 64);
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < kJ; ++j) {
-        int ra = min(tm * kTile + drow + 8 * kWaves * j, m_valid - 1);
-        sa[j] = g.A + (int64_t)ra * g.lda + dch * 8;
-        int rb = min(tn * kTile + drow + 8 * kWaves * j, n_valid - 1);
-        if (g.b_rows) rb = g.b_rows[rb];
-        sb[j] = g.B + (int64_t)rb * g.ldb + dch * 8;
-      }
-    }
-    auto dma = [&](int kt, int buf) {
-      const int64_t off = (int64_t)kt * kStep;
-      char* la = smem + buf * kLdsStage + w * 1024;
-      static_for<kJ>([&](auto j) {
-        __builtin_amdgcn_global_load_lds((glb_ptr_t)(sa[j] + off),
-                                         (lds_ptr_t)(la + j * 1024 * kWaves), 16, 0, 0);
-      });
-      static_for<kJ>([&](auto j) {
-        __builtin_amdgcn_global_load_lds((glb_ptr_t)(sb[j] + off),
-                                         (lds_ptr_t)(la + kTile * kBK * 2 + j * 1024 * kWaves),
-                                         16, 0, 0);
-      });
-    };
-      if constexpr (kWaves == 8) {
-        // ---- 8 waves: K moves 32 at a time through a ring of 5 LDS stages
-        // of 32 KiB (256 rows x 64 bytes for A and for B; the four 16-byte
-        // chunks of a row are swizzled by (row/4)%4). Loads run 3 steps
-        // ahead, so about three stages of data are in flight per CU, which
-        // is what the L2-miss latency needs. Step kt: read sub-step 1, MFMAs
-        // of sub-step 0; barrier (this thread's loads of step kt+1 have
-        // landed -- steps kt+2 and kt+3 may still be in flight -- and every
-        // read of stage kt is done); loads of step kt+4 into the stage step
-        // kt-1 used; read sub-step 0 of step kt+1; MFMAs of sub-step 1.
-        constexpr int kStage32 = 2 * kTile * 64;
-        constexpr int kJ32 = 2;  // 1 KiB loads per operand per wave per step
-        const int qrow = 16 * w + (lane >> 2);
-        const int qch = (lane & 3) ^ ((qrow >> 2) & 3);  // same for row + 128j
-        const uint16_t* qa[kJ32];
-        const uint16_t* qb[kJ32];
-        if (TILED) {
-          const uint16_t* a0 =
-              g.A + ((int64_t)tm * g.a_kt + g.a_kb0) * kTileElems + qrow * 64 + qch * 8;
-          const uint16_t* b0 =
-              g.B + ((int64_t)tn * g.b_kt + g.b_kb0) * kTileElems + qrow * 64 + qch * 8;
-          static_for<kJ32>([&](auto j) {
-            qa[j] = a0 + j * 128 * 64;
-            qb[j] = b0 + j * 128 * 64;
-          });
-        } else {
-          static_for<kJ32>([&](auto j) {
-            int ra = min(tm * kTile + qrow + 128 * j, m_valid - 1);
-            qa[j] = g.A + (int64_t)ra * g.lda + qch * 8;
-            int rb = min(tn * kTile + qrow + 128 * j, n_valid - 1);
-            if (g.b_rows) rb = g.b_rows[rb];
-            qb[j] = g.B + (int64_t)rb * g.ldb + qch * 8;
-          });
-        }
-        // loads K columns 32kt..32kt+31 (row-major: +32kt; tiled: block kt/2,
-        // column 32*(kt%2)) into ring stage `buf`
-        auto dma32 = [&](int kt, int buf) {
-          const int64_t off =
-              TILED ? (int64_t)(kt >> 1) * kTileElems + (kt & 1) * 32 : (int64_t)kt * 32;
-          char* la = smem + buf * kStage32 + w * 1024;
-          static_for<kJ32>([&](auto j) {
-            __builtin_amdgcn_global_load_lds((glb_ptr_t)(qa[j] + off),
-                                             (lds_ptr_t)(la + j * 8192), 16, 0, 0);
-          });
-          static_for<kJ32>([&](auto j) {
-            __builtin_amdgcn_global_load_lds((glb_ptr_t)(qb[j] + off),
-                                             (lds_ptr_t)(la + kTile * 64 + j * 8192), 16, 0,
-                                             0);
-          });
-        };
-        const int ra32 = (wm * 128 + fr) * 64;
-        const int rb32 = kTile * 64 + (wn * WN + fr) * 64;
-        int rc32[2];
-        static_for<2>([&](auto t) { rc32[t] = ((2 * t + (lane >> 5)) ^ ((fr >> 2) & 3)) << 4; });
-        auto fload32 = [&](int slot, int kt, int t) {
-          const char* base = smem + (kt % 5) * kStage32;
-          static_for<4>([&](auto i) {
-            fa[slot][i] = *(const bf16x8*)(base + ra32 + i * 32 * 64 + rc32[t]);
-          });
-          static_for<NI>([&](auto i) {
-            fb[slot][i] = *(const bf16x8*)(base + rb32 + i * 32 * 64 + rc32[t]);
-          });
-        };
-        // s_waitcnt immediates: vmcnt in bits [3:0], expcnt [6:4] = 7 (no
-        // wait), lgkmcnt [11:8] = 0
-        constexpr int kPerStep = 2 * kJ32;                        // loads per wave per step
-        constexpr int kWaitTwoSteps = 0x0070 | (2 * kPerStep);    // steps kt+2, kt+3 in flight
-        constexpr int kWaitThreeSteps = 0x0070 | (3 * kPerStep);
-        const int nk = K / 32;
-        const int last = nk > 0 ? nk - 1 : 0;  // K = 0 (no valid tokens) still loads stage 0
-        dma32(0, 0);
-        dma32(min(1, last), 1);
-        dma32(min(2, last), 2);
-        dma32(min(3, last), 3);
-        __builtin_amdgcn_s_waitcnt(kWaitThreeSteps);
-        __builtin_amdgcn_s_barrier();
-        fload32(0, 0, 0);
-        for (int kt = 0; kt < nk; ++kt) {
-          fload32(1, kt, 1);
-          mfma_sub(0);
-          __builtin_amdgcn_sched_group_barrier(kDsRead, kSubReads, 0);
-          __builtin_amdgcn_sched_group_barrier(kMfma, kSubMfma, 0);
-          __builtin_amdgcn_s_waitcnt(kWaitTwoSteps);
-          __builtin_amdgcn_s_barrier();
-          // step kt+4 goes to the stage of step kt-1; past the end the last
-          // step is loaded again there (never into a stage still in use)
-          dma32(min(kt + 4, last), (kt + 4) % 5);
-          fload32(0, kt + 1, 0);
-          mfma_sub(1);
-          __builtin_amdgcn_sched_group_barrier(kDsRead, kSubReads, 1);
-          static_for<2 * kJ32>([&](auto) {
-            __builtin_amdgcn_sched_group_barrier(kMfma, 1, 1);
-            __builtin_amdgcn_sched_group_barrier(kVmem, 1, 1);
-          });
-        }
-        __syncthreads();  // the last (redundant) loads land before LDS is reused
-      } else {
-      const int nk = K / kBK;
+  const int nk = K / kBK;
+  const int last = nk > 0 ? nk - 1 : 0;  // K = 0 (no valid tokens) still loads step 0
+  static_for<kStages>([&](auto st) { load_step(min((int)st.value, last), st.value); });
+  __builtin_amdgcn_s_waitcnt(wait_vm((kStages - 1) * kPerStep));  // step 0 has landed
+  __builtin_amdgcn_s_barrier();
+  fread_half(I0{}, 0, 0, I0{});
+  fread_half(I0{}, 0, 0, I1{});
 
-        // ---- Pipeline: while the MFMAs consume LDS buffer kt%2, step kt+1 is
-        // landing in the other buffer. The barrier in the middle of step kt
-        // (after every wave has read sub-step 3) both publishes step kt+1 and
-        // frees buffer kt%2, which immediately receives step kt+2. Sub-step 0
-        // of step kt+1 is read right after that barrier, behind the last MFMAs
-        // of step kt. __syncthreads() waits for this thread's outstanding LDS
-        // loads before the barrier, which is the completion the next step
-        // needs. With 8 waves, the two waves of a SIMD interleave their MFMAs
-        // with each other's LDS and barrier waits.
-        const int last = nk > 0 ? nk - 1 : 0;  // K = 0 (no valid tokens) still loads stage 0
-        dma(0, 0);
-        __syncthreads();
-        dma(min(1, last), 1);
-        fload(0, smem, 0);
-        for (int kt = 0; kt < nk; ++kt) {
-          const char* base = smem + (kt & 1) * kLdsStage;
-          fload(1, base, 1);
-          mfma_sub(0);
-          fload(0, base, 2);
-          mfma_sub(1);
-          fload(1, base, 3);
-          mfma_sub(0);
-          __builtin_amdgcn_sched_group_barrier(kDsRead, kSubReads, 0);
-          __builtin_amdgcn_sched_group_barrier(kMfma, kSubMfma, 0);
-          __builtin_amdgcn_sched_group_barrier(kDsRead, kSubReads, 0);
-          __builtin_amdgcn_sched_group_barrier(kMfma, kSubMfma, 0);
-          __builtin_amdgcn_sched_group_barrier(kDsRead, kSubReads, 0);
-          __builtin_amdgcn_sched_group_barrier(kMfma, kSubMfma, 0);
-          __syncthreads();
-          dma(min(kt + 2, last), kt & 1);
-          fload(0, smem + ((kt + 1) & 1) * kLdsStage, 0);
-          mfma_sub(1);
-          __builtin_amdgcn_sched_group_barrier(kDsRead, kSubReads, 1);
-          static_for<2 * kJ>([&](auto) {
-            __builtin_amdgcn_sched_group_barrier(kMfma, 1, 1);
-            __builtin_amdgcn_sched_group_barrier(kVmem, 1, 1);
-          });
-        }
-        __syncthreads();  // the last (redundant) loads land before LDS is reused
+  // The instruction order is fixed by scheduling fences. Each sub-step's
+  // MFMAs run on fragments read one sub-step earlier; the next sub-step's
+  // reads go out right after its first two MFMAs. Step kt: sub-step 0 (with
+  // the B half of step kt+4's loads), wait for step kt+1, barrier, sub-step
+  // 1 (with the A half of step kt+5's loads and the reads of step kt+1).
+  // Past the end the last step is loaded again, into free stages only.
+  const uint16_t* na = pa;
+  const uint16_t* nb = pb;
+  char* nl = smem;
+  for (int kt = 0; kt < nk; ++kt) {
+    static_for<kMfmas>([&](auto m) {
+      mfma(I0{}, m);
+      if constexpr (m.value < 2) fread_half(I1{}, kt, 1, std::integral_constant<int, m.value>{});
+      if constexpr (m.value % kSpread == kSpread - 1) {
+        if (kt > 0) load(na, nb, nl, std::integral_constant<int, kJ + m.value / kSpread>{});
       }
-  } else {
-    // ---- K not a multiple of 64: register-staged loads that zero-fill the
-    // columns past K. Thread owns rows (tid/8 + 8*kWaves*j), chunk tid%8.
-    const int lrow = tid >> 3, lch = tid & 7;
-    const uint16_t* pa[kJ];
-    const uint16_t* pb[kJ];
-#pragma unroll
-    for (int j = 0; j < kJ; ++j) {
-      int ra = min(tm * kTile + lrow + 8 * kWaves * j, m_valid - 1);
-      pa[j] = g.A + (int64_t)ra * g.lda + lch * 8;
-      int rb = min(tn * kTile + lrow + 8 * kWaves * j, n_valid - 1);
-      if (g.b_rows) rb = g.b_rows[rb];
-      pb[j] = g.B + (int64_t)rb * g.ldb + lch * 8;
-    }
-    const int st_off = lrow * 128 + ((lch ^ swz(lrow)) << 4);  // + 8*kWaves*j rows
-    u32x4 ra_[kJ], rb_[kJ];
-    auto gload = [&](int kt) {
-      const int64_t off = (int64_t)kt * kBK;
-#pragma unroll
-      for (int j = 0; j < kJ; ++j) {
-        if (kt * kBK + lch * 8 >= K) {
-          ra_[j] = u32x4{0, 0, 0, 0};
-          rb_[j] = u32x4{0, 0, 0, 0};
-        } else {
-          ra_[j] = *(const u32x4*)(pa[j] + off);
-          rb_[j] = *(const u32x4*)(pb[j] + off);
-        }
-      }
-    };
-    auto lstore = [&](int buf) {
-      char* base = smem + buf * kLdsStage;
-#pragma unroll
-      for (int j = 0; j < kJ; ++j) {
-        *(u32x4*)(base + st_off + j * 8 * kWaves * 128) = ra_[j];
-        *(u32x4*)(base + kTile * kBK * 2 + st_off + j * 8 * kWaves * 128) = rb_[j];
-      }
-    };
-    const int nk = (int)ceil_div(K, kBK);
-    for (int kt = 0; kt < nk; ++kt) {
-      gload(kt);
-      lstore(0);
-      __syncthreads();
-      static_for<4>([&](auto s) {
-        fload(0, smem, s);
-        mfma_sub(0);
-      });
-      __syncthreads();
-    }
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    __builtin_amdgcn_s_waitcnt(wait_vm(3 * kPerStep));  // step kt+1 has landed
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    const int64_t nxt = (int64_t)min(kt + kStages, last) * kTileElems;
+    na = pa + nxt;
+    nb = pb + nxt;
+    nl = smem + (kt % kStages) * kStage + w * 1024;
+    static_for<kMfmas>([&](auto m) {
+      if constexpr (m.value % kSpread == kSpread - 1)
+        load(na, nb, nl, std::integral_constant<int, m.value / kSpread>{});
+      mfma(I1{}, m);
+      if constexpr (m.value == 1 || m.value == 2)
+        fread_half(I0{}, kt + 1, 0, std::integral_constant<int, m.value - 1>{});
+      __builtin_amdgcn_sched_barrier(0);
+    });
   }
+  __syncthreads();  // every load has landed before LDS is reused
 
-  Frag f{tm, tn, wm, wn, lane, wn * WN};
+  Frag f{tm, tn, wm, wn, lane, wn * kWN};
   epi(acc, f, m_valid, n_valid, smem);
 }
 
-#ifndef GRPO_GEMM_WN
-#define GRPO_GEMM_WN 64
-#endif
-
-template <class Epi, bool TILED>
+template <class Epi>
 static void launch_gemm(const GemmArgs& g, const Epi& e, hipStream_t s) {
   int grid = gemm_grid(g.tiles_m, g.tiles_n);
-  bool ktail = !TILED && (g.k_dev == nullptr) && (g.K % kBK != 0);
-  if (ktail) {
-    hipLaunchKernelGGL((k_gemm_bf16<Epi, true, false, 128>), dim3(grid), dim3(256), 0, s, g, e);
-  } else {
-    constexpr int WN = GRPO_GEMM_WN;
-    hipLaunchKernelGGL((k_gemm_bf16<Epi, false, TILED, WN>), dim3(grid),
-                       dim3(64 * 2 * (kTile / WN)), 0, s, g, e);
-  }
+  hipLaunchKernelGGL((k_gemm_bf16<Epi>), dim3(grid), dim3(64 * kWaves), 0, s, g, e);
 }
 
 void launch_gemm_lse(const GemmArgs& g, const int32_t* y_p, float* zy, float2* ms, int64_t ldms,
                      int64_t V, hipStream_t s) {
   EpiLse e{y_p, zy, ms, ldms, V};
-  launch_gemm<EpiLse, false>(g, e, s);
+  launch_gemm<EpiLse>(g, e, s);
 }
 
 void launch_gemm_dz(const GemmArgs& g, const int32_t* y_p, const float* lse_p, const float* g_p,
                     uint16_t* dz, int64_t dz_kt, uint16_t* dzT, int64_t dzT_kt, int64_t V,
                     int64_t v0, hipStream_t s) {
   EpiDz e{y_p, lse_p, g_p, dz, dz_kt, dzT, dzT_kt, V, v0};
-  launch_gemm<EpiDz, false>(g, e, s);
+  launch_gemm<EpiDz>(g, e, s);
 }
 
 void launch_gemm_store(const GemmArgs& g, const StoreArgs& a, bool grad_weight, hipStream_t s) {
   EpiStore e{a.acc_buf, a.ld_acc, a.read_acc, a.out, a.ld_out, a.out_bf16, a.add_out,
              a.out_rows, a.m_limit, a.n_limit};
   if (grad_weight)
-    launch_gemm<EpiGradWeight, true>(g, EpiGradWeight{e}, s);
+    launch_gemm<EpiGradWeight>(g, EpiGradWeight{e}, s);
   else
-    launch_gemm<EpiGradHidden, true>(g, EpiGradHidden{e}, s);
+    launch_gemm<EpiGradHidden>(g, EpiGradHidden{e}, s);
 }
 
 }  // namespace grpo

@@ -19,12 +19,12 @@ namespace {
 // --------------------------------------------------------- kernel timing
 enum Kind {
   K_PACK, K_ADV, K_GEMM_LSE, K_LSE_FIN, K_TOKEN, K_TRANSPOSE, K_GEMM_DZ, K_GEMM_DH, K_GEMM_DW,
-  K_F32_SCORE, K_F32_DH, K_F32_DW, K_ZERO_ROWS, K_GATHER_DOT, K_NUM_KINDS
+  K_F32_SCORE, K_F32_DH, K_F32_DW, K_ZERO_ROWS, K_GATHER_DOT, K_TILE, K_NUM_KINDS
 };
 const char* kKindNames[K_NUM_KINDS] = {
     "pack_valid",  "group_advantages", "gemm_logits_lse", "lse_finalize",   "token_objective",
     "transpose",   "gemm_recompute_dz", "gemm_grad_hidden", "gemm_grad_weight", "f32_score",
-    "f32_grad_hidden", "f32_grad_weight", "zero_masked_rows", "gather_dot"};
+    "f32_grad_hidden", "f32_grad_weight", "zero_masked_rows", "gather_dot", "tile"};
 
 struct Prof {
   std::mutex mu;
@@ -93,7 +93,8 @@ struct Layout {
   int64_t Npad = 0, Vpad = 0, tiles_v = 0, Vc = 0, nchunks = 0;
   size_t hdr = 0, rows = 0, seq = 0, y = 0, pidx = 0, counts = 0, base = 0;
   size_t lse = 0, zy = 0, logp = 0, g = 0, ms = 0, lpart = 0;
-  size_t hT = 0, WT = 0, dz = 0, dzT = 0, dhacc = 0;
+  int64_t Hk = 0;  // H rounded up to the tiled block width
+  size_t WK = 0, hK = 0, hT = 0, WT = 0, dz = 0, dzT = 0, dhacc = 0;
   size_t total = 0;
 };
 
@@ -135,6 +136,10 @@ Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_
   L.lpart = take(c, 4 * token_objective_blocks(N));
   if (dt == GRPO_BF16) {
     L.ms = take(c, 8 * L.tiles_v * L.Npad);
+    // tiled copies of W and of the valid hidden rows (K = H contiguous blocks)
+    L.Hk = round_up(H, kBK);
+    L.WK = take(c, 2 * L.Vpad * L.Hk);
+    L.hK = take(c, 2 * L.Npad * L.Hk);
     if (op == GRPO_OP_LOSS_FWD_BWD) {
       chunking(L.Npad, L.Vpad, L.Vc, L.nchunks);
       int64_t Hpad = round_up(H, kTile);
@@ -173,22 +178,22 @@ grpo_status check_ws(void* ws, size_t bytes, const Layout& L) {
   return GRPO_OK;
 }
 
-GemmArgs gemm_args(const void* A, int64_t lda, int64_t M, const void* B, int64_t ldb, int64_t N,
-                   const int32_t* b_rows, const int32_t* m_dev, const int32_t* n_dev, int64_t K,
+// Operands in the tiled layout: A has a_kt blocks per tile-row, B b_kt.
+GemmArgs gemm_args(const void* A, int64_t a_kt, int64_t M, const void* B, int64_t b_kt,
+                   int64_t N, const int32_t* m_dev, const int32_t* n_dev, int64_t K,
                    const int32_t* k_dev) {
   GemmArgs g;
   g.A = (const uint16_t*)A;
-  g.lda = lda;
   g.M = (int)M;
   g.B = (const uint16_t*)B;
-  g.ldb = ldb;
   g.N = (int)N;
-  g.b_rows = b_rows;
   g.m_dev = m_dev;
   g.n_dev = n_dev;
+  g.a_kt = a_kt;
+  g.b_kt = b_kt;
+  g.a_kb0 = g.b_kb0 = 0;
   g.K = (int)K;
   g.k_dev = k_dev;
-  g.a_kt = g.a_kb0 = g.b_kt = g.b_kb0 = 0;
   g.tiles_m = (int)ceil_div(M, kTile);
   g.tiles_n = (int)ceil_div(N, kTile);
   return g;
@@ -216,6 +221,22 @@ grpo_status run_pack(const Layout& L, void* ws, const uint8_t* mask, const int64
   return timed(K_PACK, s, [&] { launch_pack(a, s); });
 }
 
+// Tiled copies of W (all V rows) and of the valid hidden rows in packed
+// order, the operands of the scoring and dz products.
+grpo_status run_tiles(const Layout& L, void* ws, const void* hidden, const void* weight,
+                      int64_t H, int64_t V, hipStream_t s) {
+  const int32_t* rows_p = at<int32_t>(ws, L.rows);
+  const WsHeader* hdr = at<WsHeader>(ws, L.hdr);
+  TRY(timed(K_TILE, s, [&] {
+    launch_tile_rows((const uint16_t*)weight, H, nullptr, V, nullptr, L.Vpad, H,
+                     at<uint16_t>(ws, L.WK), s);
+  }));
+  return timed(K_TILE, s, [&] {
+    launch_tile_rows((const uint16_t*)hidden, H, rows_p, 0, hdr, L.Npad, H,
+                     at<uint16_t>(ws, L.hK), s);
+  });
+}
+
 // Forward vocabulary pass: lse and logp (packed order) for every valid row.
 grpo_status run_scoring(const Layout& L, void* ws, grpo_dtype dt, const void* hidden,
                         const void* weight, int64_t N, int64_t H, int64_t V, hipStream_t s) {
@@ -232,8 +253,9 @@ grpo_status run_scoring(const Layout& L, void* ws, grpo_dtype dt, const void* hi
     });
   }
   float2* ms = at<float2>(ws, L.ms);
-  GemmArgs g = gemm_args(weight, H, V, hidden, H, N, rows_p, nullptr, &hdr->num_valid, H,
-                         nullptr);
+  const int64_t kb = L.Hk / kBK;
+  GemmArgs g = gemm_args(at<uint16_t>(ws, L.WK), kb, V, at<uint16_t>(ws, L.hK), kb, L.Npad,
+                         nullptr, &hdr->num_valid, L.Hk, nullptr);
   TRY(timed(K_GEMM_LSE, s, [&] { launch_gemm_lse(g, y_p, zy, ms, L.Npad, V, s); }));
   return timed(K_LSE_FIN, s, [&] {
     launch_lse_finalize(ms, L.Npad, (int)L.tiles_v, zy, hdr, lse_p, logp_p, N, s);
@@ -308,6 +330,7 @@ grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weig
   TRY(check_device());
   // one "rollout" covering every row (cu_seqlens = NULL means {0, N})
   TRY(run_pack(L, workspace, mask, tokens, V, nullptr, 1, N, nullptr, nullptr, nullptr, stream));
+  if (dt == GRPO_BF16) TRY(run_tiles(L, workspace, hidden, weight, H, V, stream));
   TRY(run_scoring(L, workspace, dt, hidden, weight, N, H, V, stream));
   if (logp || lse) {
     return timed(K_LSE_FIN, stream, [&] {
@@ -364,6 +387,8 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
   TRY(run_pack(L, ws, mask, tokens, V, cu_seqlens, num_seqs, N, nullptr, nullptr, nullptr, s));
 
   // S2-S4: scoring (or logp from a given lse).
+  if (dt == GRPO_BF16 && (lse_in == nullptr || grad_hidden || grad_weight))
+    TRY(run_tiles(L, ws, hidden, weight, H, V, s));
   if (lse_in == nullptr || dt == GRPO_F32) {
     TRY(run_scoring(L, ws, dt, hidden, weight, N, H, V, s));
   }
@@ -428,9 +453,10 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
   uint16_t* dz = at<uint16_t>(ws, L.dz);
   uint16_t* dzT = at<uint16_t>(ws, L.dzT);
   float* dhacc = L.nchunks > 1 ? at<float>(ws, L.dhacc) : nullptr;
-  // Intermediates in the tiled layout (256x64 blocks): h^T [H x tokens],
-  // W^T [H x V], dz [tokens x chunk] and dz^T [chunk x tokens].
+  // Intermediates in the tiled layout: h^T [H x tokens], W^T [H x V],
+  // dz [tokens x chunk] and dz^T [chunk x tokens].
   const int64_t kt_tok = L.Npad / kBK, kt_voc = L.Vpad / kBK, kt_chunk = L.Vc / kBK;
+  const int64_t kt_h = L.Hk / kBK;
   if (grad_weight) {
     TRY(timed(K_TRANSPOSE, s, [&] {
       launch_transpose_tiled((const uint16_t*)hidden, H, rows_p, 0, hdr, L.Npad, H, hT, s);
@@ -447,18 +473,17 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
     if (Mc <= 0) break;
     bool last = (c == L.nchunks - 1) || (v0 + L.Vc >= V);
     // recompute the logits of this chunk and form dz (both layouts)
-    GemmArgs gz = gemm_args((const uint16_t*)weight + v0 * H, H, Mc, hidden, H, N, rows_p, nullptr,
-                            &hdr->num_valid, H, nullptr);
+    GemmArgs gz = gemm_args(at<uint16_t>(ws, L.WK) + (v0 / kTile) * kt_h * kTileElems, kt_h, Mc,
+                            at<uint16_t>(ws, L.hK), kt_h, L.Npad, nullptr, &hdr->num_valid, L.Hk,
+                            nullptr);
     TRY(timed(K_GEMM_DZ, s, [&] {
       launch_gemm_dz(gz, y_p, lse_p, g_p, dz, kt_chunk, grad_weight ? dzT : nullptr, kt_tok, V, v0,
                      s);
     }));
     if (grad_hidden) {
       // dh[t, :] (+)= sum_{v in chunk} dz[t, v] W[v, :]
-      GemmArgs gh = gemm_args(dz, 0, L.Npad, WT, 0, H, nullptr, &hdr->num_valid, nullptr,
+      GemmArgs gh = gemm_args(dz, kt_chunk, L.Npad, WT, kt_voc, H, &hdr->num_valid, nullptr,
                               round_up(Mc, kBK), nullptr);
-      gh.a_kt = kt_chunk;
-      gh.b_kt = kt_voc;
       gh.b_kb0 = v0 / kBK;
       StoreArgs sa{};
       sa.acc_buf = dhacc;
@@ -475,10 +500,8 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
     }
     if (grad_weight) {
       // dW[v, :] = sum_t dz[t, v] h[t, :] over the valid tokens
-      GemmArgs gw = gemm_args(dzT, 0, Mc, hT, 0, H, nullptr, nullptr, nullptr, 0,
+      GemmArgs gw = gemm_args(dzT, kt_tok, Mc, hT, kt_tok, H, nullptr, nullptr, 0,
                               &hdr->num_valid);
-      gw.a_kt = kt_tok;
-      gw.b_kt = kt_tok;
       StoreArgs sa{};
       sa.acc_buf = nullptr;
       sa.ld_acc = 0;

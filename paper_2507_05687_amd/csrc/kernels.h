@@ -6,21 +6,18 @@
 namespace grpo {
 
 // ---------------------------------------------------------------- GEMM
-// C[m, n] = sum_k A[m, k] * B[n, k], A and B bf16 row-major with K contiguous.
+// C[m, n] = sum_k A[m, k] * B[n, k]; A and B bf16 in the tiled layout.
 struct GemmArgs {
   const uint16_t* A;
-  int64_t lda;
-  int M;                  // rows of A (loads clamp to M-1)
+  int M;                  // rows of A (static bound)
   const uint16_t* B;
-  int64_t ldb;
-  int N;                  // rows of B
-  const int32_t* b_rows;  // optional gather: B row n is B[b_rows[n]]
+  int N;                  // rows of B (static bound)
   const int32_t* m_dev;   // optional device bound on M (e.g. the valid-token count)
   const int32_t* n_dev;   // optional device bound on N
-  int64_t a_kt, a_kb0;    // tiled A: 64-wide blocks per tile-row, first block
-  int64_t b_kt, b_kb0;    // tiled B: same
-  int K;                  // contraction length (used when k_dev is NULL)
-  const int32_t* k_dev;   // optional device K, rounded up to 64 (operands zero-padded)
+  int64_t a_kt, a_kb0;    // A: blocks per tile-row, first block used
+  int64_t b_kt, b_kb0;    // B: same
+  int K;                  // contraction length, a multiple of 32 (when k_dev is NULL)
+  const int32_t* k_dev;   // optional device K, rounded up to 32 (operands zero-padded)
   int tiles_m, tiles_n;   // 256x256 tiles covering the static M x N
 };
 
@@ -104,6 +101,14 @@ void launch_gather_dot_bf16(const uint16_t* hidden, const uint16_t* W, int64_t H
                             const int32_t* rows_p, const int32_t* y_p, const WsHeader* hdr,
                             float* zy, int64_t Nmax, hipStream_t s);
 void launch_zero_tail(float* g_p, int64_t Npad, const WsHeader* hdr, hipStream_t s);
+// Tiled layout of rows of `in` (row i = in[rows ? rows[i] : i], K columns):
+// r_pad x round_up(K, 32), rows >= the valid count (hdr->num_valid, else
+// n_static) and columns >= K zero.
+void launch_tile_rows(const uint16_t* in, int64_t ld_in, const int32_t* rows, int64_t n_static,
+                      const WsHeader* hdr, int64_t r_pad, int64_t K, uint16_t* out,
+                      hipStream_t s);
+// Tiled layout of the transpose of those rows: round_up(K, 256) rows x
+// n_pad columns (n_pad a multiple of 64), invalid rows as zero columns.
 void launch_transpose_tiled(const uint16_t* in, int64_t ld_in, const int32_t* rows,
                             int64_t n_static, const WsHeader* hdr, int64_t n_pad, int64_t K,
                             uint16_t* out, hipStream_t s);
