@@ -424,6 +424,7 @@ __global__ void __launch_bounds__(256) k_transpose_tiled(const uint16_t* __restr
                                                          int64_t n_static,
                                                          const WsHeader* __restrict__ hdr,
                                                          int64_t n_pad, int64_t K,
+                                                         int64_t stride,
                                                          uint16_t* __restrict__ out) {
   __shared__ uint16_t tile[64][66];
   int64_t i0 = (int64_t)blockIdx.x * 64, k0 = (int64_t)blockIdx.y * 64;
@@ -464,7 +465,7 @@ __global__ void __launch_bounds__(256) k_transpose_tiled(const uint16_t* __restr
     int64_t k = k0 + kk;
     if (k < K) {
       const int64_t i = i0 + c0;  // 16 consecutive columns, within one 32-wide block
-      uint16_t* p = out + ((k >> 8) * (n_pad >> 5) + (i >> 5)) * kTileElems + (k & 255) * 32 + (i & 31);
+      uint16_t* p = out + ((k >> 8) * stride + (i >> 5)) * kTileElems + (k & 255) * 32 + (i & 31);
       u32x4 a, b;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -485,10 +486,10 @@ __global__ void __launch_bounds__(256) k_tile_rows(const uint16_t* __restrict__ 
                                                    const int32_t* __restrict__ rows,
                                                    int64_t n_static,
                                                    const WsHeader* __restrict__ hdr, int64_t K,
-                                                   int64_t kb_per_row,
+                                                   int64_t kb_per_row, int64_t stride,
                                                    uint16_t* __restrict__ out) {
-  const int64_t blk = blockIdx.x;
-  const int64_t rb = blk / kb_per_row, kb = blk - rb * kb_per_row;
+  const int64_t rb = blockIdx.x / kb_per_row, kb = blockIdx.x - rb * kb_per_row;
+  const int64_t blk = rb * stride + kb;
   const int64_t nvalid = hdr ? (int64_t)hdr->num_valid : n_static;
   const int t = threadIdx.x;
   const int64_t k0 = kb * 32 + (t & 3) * 8;
@@ -516,21 +517,21 @@ __global__ void __launch_bounds__(256) k_tile_rows(const uint16_t* __restrict__ 
 }
 
 void launch_tile_rows(const uint16_t* in, int64_t ld_in, const int32_t* rows, int64_t n_static,
-                      const WsHeader* hdr, int64_t r_pad, int64_t K, uint16_t* out,
-                      hipStream_t s) {
+                      const WsHeader* hdr, int64_t r_pad, int64_t K, int64_t stride,
+                      uint16_t* out, hipStream_t s) {
   const int64_t kb_per_row = ceil_div(K, 32);
   const int64_t blocks = r_pad / 256 * kb_per_row;
   hipLaunchKernelGGL(k_tile_rows, dim3((unsigned)blocks), dim3(256), 0, s, in, ld_in, rows,
-                     n_static, hdr, K, kb_per_row, out);
+                     n_static, hdr, K, kb_per_row, stride, out);
 }
 
 // n_pad must be a multiple of 64; `out` holds round_up(K, 256) x n_pad elements.
 void launch_transpose_tiled(const uint16_t* in, int64_t ld_in, const int32_t* rows,
                             int64_t n_static, const WsHeader* hdr, int64_t n_pad, int64_t K,
-                            uint16_t* out, hipStream_t s) {
+                            int64_t stride, uint16_t* out, hipStream_t s) {
   dim3 grid((unsigned)(n_pad / 64), (unsigned)ceil_div(K, 64));
   hipLaunchKernelGGL(k_transpose_tiled, grid, dim3(256), 0, s, in, ld_in, rows, n_static, hdr,
-                     n_pad, K, out);
+                     n_pad, K, stride, out);
 }
 
 // ------------------------------------------ zero the masked output rows

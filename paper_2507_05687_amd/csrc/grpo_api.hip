@@ -94,9 +94,19 @@ struct Layout {
   size_t hdr = 0, rows = 0, seq = 0, y = 0, pidx = 0, counts = 0, base = 0;
   size_t lse = 0, zy = 0, logp = 0, g = 0, ms = 0, lpart = 0;
   int64_t Hk = 0;  // H rounded up to the tiled block width
+  // tiled buffers and their tile-row strides in blocks
   size_t WK = 0, hK = 0, hT = 0, WT = 0, dz = 0, dzT = 0, dhacc = 0;
+  int64_t sK = 0, sTok = 0, sVoc = 0, sChunk = 0;
   size_t total = 0;
 };
+
+// Tile-rows of a tiled buffer are one block further apart than their length,
+// so that the blocks that concurrent tiles read at the same K step do not
+// all share the same low address bits (and L2 sets).
+#ifndef GRPO_TILE_SKEW
+#define GRPO_TILE_SKEW 1
+#endif
+int64_t tile_stride(int64_t K) { return ceil_div(K, kBK) + GRPO_TILE_SKEW; }
 
 size_t take(size_t& cur, size_t bytes) {
   size_t at = cur;
@@ -138,15 +148,19 @@ Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_
     L.ms = take(c, 8 * L.tiles_v * L.Npad);
     // tiled copies of W and of the valid hidden rows (K = H contiguous blocks)
     L.Hk = round_up(H, kBK);
-    L.WK = take(c, 2 * L.Vpad * L.Hk);
-    L.hK = take(c, 2 * L.Npad * L.Hk);
+    L.sK = tile_stride(H);
+    L.WK = take(c, 2 * L.Vpad * L.sK * kBK);
+    L.hK = take(c, 2 * L.Npad * L.sK * kBK);
     if (op == GRPO_OP_LOSS_FWD_BWD) {
       chunking(L.Npad, L.Vpad, L.Vc, L.nchunks);
       int64_t Hpad = round_up(H, kTile);
-      L.hT = take(c, 2 * Hpad * L.Npad);
-      L.WT = take(c, 2 * Hpad * L.Vpad);
-      L.dz = take(c, 2 * L.Npad * L.Vc);
-      L.dzT = take(c, 2 * L.Vc * L.Npad);
+      L.sTok = tile_stride(L.Npad);
+      L.sVoc = tile_stride(L.Vpad);
+      L.sChunk = tile_stride(L.Vc);
+      L.hT = take(c, 2 * Hpad * L.sTok * kBK);
+      L.WT = take(c, 2 * Hpad * L.sVoc * kBK);
+      L.dz = take(c, 2 * L.Npad * L.sChunk * kBK);
+      L.dzT = take(c, 2 * L.Vc * L.sTok * kBK);
       // fp32 dh accumulator with every row and column of every tile present
       if (L.nchunks > 1) L.dhacc = take(c, 4 * L.Npad * Hpad);
     }
@@ -228,11 +242,11 @@ grpo_status run_tiles(const Layout& L, void* ws, const void* hidden, const void*
   const int32_t* rows_p = at<int32_t>(ws, L.rows);
   const WsHeader* hdr = at<WsHeader>(ws, L.hdr);
   TRY(timed(K_TILE, s, [&] {
-    launch_tile_rows((const uint16_t*)weight, H, nullptr, V, nullptr, L.Vpad, H,
+    launch_tile_rows((const uint16_t*)weight, H, nullptr, V, nullptr, L.Vpad, H, L.sK,
                      at<uint16_t>(ws, L.WK), s);
   }));
   return timed(K_TILE, s, [&] {
-    launch_tile_rows((const uint16_t*)hidden, H, rows_p, 0, hdr, L.Npad, H,
+    launch_tile_rows((const uint16_t*)hidden, H, rows_p, 0, hdr, L.Npad, H, L.sK,
                      at<uint16_t>(ws, L.hK), s);
   });
 }
@@ -253,8 +267,7 @@ grpo_status run_scoring(const Layout& L, void* ws, grpo_dtype dt, const void* hi
     });
   }
   float2* ms = at<float2>(ws, L.ms);
-  const int64_t kb = L.Hk / kBK;
-  GemmArgs g = gemm_args(at<uint16_t>(ws, L.WK), kb, V, at<uint16_t>(ws, L.hK), kb, L.Npad,
+  GemmArgs g = gemm_args(at<uint16_t>(ws, L.WK), L.sK, V, at<uint16_t>(ws, L.hK), L.sK, L.Npad,
                          nullptr, &hdr->num_valid, L.Hk, nullptr);
   TRY(timed(K_GEMM_LSE, s, [&] { launch_gemm_lse(g, y_p, zy, ms, L.Npad, V, s); }));
   return timed(K_LSE_FIN, s, [&] {
@@ -455,16 +468,17 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
   float* dhacc = L.nchunks > 1 ? at<float>(ws, L.dhacc) : nullptr;
   // Intermediates in the tiled layout: h^T [H x tokens], W^T [H x V],
   // dz [tokens x chunk] and dz^T [chunk x tokens].
-  const int64_t kt_tok = L.Npad / kBK, kt_voc = L.Vpad / kBK, kt_chunk = L.Vc / kBK;
-  const int64_t kt_h = L.Hk / kBK;
+  const int64_t kt_tok = L.sTok, kt_voc = L.sVoc, kt_chunk = L.sChunk, kt_h = L.sK;
   if (grad_weight) {
     TRY(timed(K_TRANSPOSE, s, [&] {
-      launch_transpose_tiled((const uint16_t*)hidden, H, rows_p, 0, hdr, L.Npad, H, hT, s);
+      launch_transpose_tiled((const uint16_t*)hidden, H, rows_p, 0, hdr, L.Npad, H, kt_tok, hT,
+                             s);
     }));
   }
   if (grad_hidden) {
     TRY(timed(K_TRANSPOSE, s, [&] {
-      launch_transpose_tiled((const uint16_t*)weight, H, nullptr, V, nullptr, L.Vpad, H, WT, s);
+      launch_transpose_tiled((const uint16_t*)weight, H, nullptr, V, nullptr, L.Vpad, H, kt_voc,
+                             WT, s);
     }));
   }
   for (int64_t c = 0; c < L.nchunks; ++c) {

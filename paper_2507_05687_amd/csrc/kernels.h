@@ -103,15 +103,15 @@ void launch_gather_dot_bf16(const uint16_t* hidden, const uint16_t* W, int64_t H
 void launch_zero_tail(float* g_p, int64_t Npad, const WsHeader* hdr, hipStream_t s);
 // Tiled layout of rows of `in` (row i = in[rows ? rows[i] : i], K columns):
 // r_pad x round_up(K, 32), rows >= the valid count (hdr->num_valid, else
-// n_static) and columns >= K zero.
+// n_static) and columns >= K zero; tile-rows `stride` blocks apart.
 void launch_tile_rows(const uint16_t* in, int64_t ld_in, const int32_t* rows, int64_t n_static,
-                      const WsHeader* hdr, int64_t r_pad, int64_t K, uint16_t* out,
-                      hipStream_t s);
+                      const WsHeader* hdr, int64_t r_pad, int64_t K, int64_t stride,
+                      uint16_t* out, hipStream_t s);
 // Tiled layout of the transpose of those rows: round_up(K, 256) rows x
 // n_pad columns (n_pad a multiple of 64), invalid rows as zero columns.
 void launch_transpose_tiled(const uint16_t* in, int64_t ld_in, const int32_t* rows,
                             int64_t n_static, const WsHeader* hdr, int64_t n_pad, int64_t K,
-                            uint16_t* out, hipStream_t s);
+                            int64_t stride, uint16_t* out, hipStream_t s);
 void launch_zero_masked_rows(const int32_t* pidx, int64_t N, int64_t H, void* out, int out_bf16,
                              hipStream_t s);
 void launch_f32_score(const float* hidden, const float* W, int64_t H, int64_t V,
