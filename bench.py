@@ -6,6 +6,8 @@ backward (Eq. 1 with k3 KL): valid-row packing, LM-head contraction with
 online log-sum-exp, the per-token ratio/clip/KL epilogue, the masked
 aggregation, and dL/dh, dL/dW through a recomputed, chunked logits
 gradient. Inputs are seeded synthetic tensors already resident in HBM.
+`--workload sft_bf16` times the supervised stage instead: the same
+contractions with the mean cross-entropy over the response tokens.
 
 Prints one JSON line (see the contract in the repository documentation).
 """
@@ -25,6 +27,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "rollout tokens/sec for fused log-prob + GRPO loss fwd+bwd; % bf16 MFMA peak"
+METRIC_SFT = "supervised tokens/sec for fused LM-head cross-entropy fwd+bwd (SFT stage); % bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 
@@ -43,9 +46,9 @@ def _gemm_flops(kind: str, w, n_valid: int, vc_sizes: list[int]) -> float:
     return 0.0
 
 
-def _traffic_from_profiles(kernel: str):
+def _traffic_from_profiles(kernel: str, workload: str):
     """HBM bytes per launch from a committed rocprofv3 counter summary, if it
-    was taken on the current kernel source; else None."""
+    was taken on the current kernel source and the same workload; else None."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
@@ -56,6 +59,8 @@ def _traffic_from_profiles(kernel: str):
         src = open(os.path.join(ROOT, "paper_2507_05687_amd", "csrc", "gemm_bf16.hip"),
                    "rb").read()
         if rec.get("gemm_source_sha256") != hashlib.sha256(src).hexdigest():
+            return None
+        if rec.get("workload") != workload:
             return None
         return rec.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")
     except Exception:
@@ -80,9 +85,12 @@ def cpu_baseline(w, W_bits, h_bits, batch, adv, old, ref, sample_tokens: int):
                        for b in range(B)])
     t0 = time.perf_counter()
     lse, logp, _ = oracle.score_rows(hd, Wd, y)
-    c = oracle.seq_weights(counts)
-    ell, g, _ = oracle.token_objective(logp, old[rows], ref[rows], adv[seq], c[seq], None,
-                                       w.clip_eps, w.beta)
+    if w.objective == "sft":  # dL/dlogp of the mean cross-entropy over the supervised rows
+        g = np.full(len(rows), -1.0 / int(batch["mask"].sum()))
+    else:
+        c = oracle.seq_weights(counts)
+        ell, g, _ = oracle.token_objective(logp, old[rows], ref[rows], adv[seq], c[seq], None,
+                                           w.clip_eps, w.beta)
     oracle.grad_hidden_rows(hd, Wd, y, lse, g)
     oracle.grad_weight_rows(hd, Wd, y, lse, g)
     dt = time.perf_counter() - t0
@@ -99,7 +107,8 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="fwdbwd_bf16",
-                    choices=["fwdbwd_bf16", "fwd_bf16", "ragged_bf16", "double_bf16"])
+                    choices=["fwdbwd_bf16", "fwd_bf16", "ragged_bf16", "double_bf16",
+                             "sft_bf16"])
     ap.add_argument("--cpu-sample", type=int, default=128,
                     help="valid tokens timed on the CPU oracle (0 skips the CPU baseline)")
     ap.add_argument("--verbose", action="store_true")
@@ -145,13 +154,17 @@ def main():
     rewards = torch.from_numpy(batch["rewards"]).cuda()
     n_valid = int(batch["mask"].sum())
     N, H, V, B = w.num_tokens, w.hidden, w.vocab, w.num_seqs
-    use_mask = mask if w.ragged else None
+    sft = w.objective == "sft"
+    use_mask = mask if (w.ragged or w.prompt_len) else None
 
     # old/ref log-probs: the policy's own log-prob plus seeded noise
-    base, _ = grpo.logprob_fwd(h, W, tokens, use_mask)
-    old = base + torch.from_numpy(batch["old_noise"]).cuda()
-    ref = base + torch.from_numpy(batch["ref_noise"]).cuda()
-    del base
+    if sft:
+        old = ref = torch.zeros(N, dtype=torch.float32, device="cuda")
+    else:
+        base, _ = grpo.logprob_fwd(h, W, tokens, use_mask)
+        old = base + torch.from_numpy(batch["old_noise"]).cuda()
+        ref = base + torch.from_numpy(batch["ref_noise"]).cuda()
+        del base
     f32 = dict(dtype=torch.float32, device="cuda")
     loss = torch.empty(1, **f32)
     gh = torch.empty(N, H, dtype=torch.bfloat16, device="cuda")
@@ -169,6 +182,11 @@ def main():
     mptr = P(use_mask)
 
     def step():
+        if sft:  # the supervised stage: cross-entropy over the response tokens
+            st = lib.sft_ce_fwd_bwd(grpo.BF16, P(h), P(W), P(tokens), mptr, N, H, V, P(loss),
+                                    None, P(gh), grpo.BF16, P(gw), 0, P(ws), ws.numel(), stream)
+            assert st == 0, st
+            return
         st = lib.group_advantages(P(rewards), w.prompts, w.group, 1e-6, 1, P(adv), stream)
         assert st == 0, st
         if args.workload == "fwd_bf16":
@@ -218,19 +236,21 @@ def main():
     kind, (launches, kms) = max(prof.items(), key=lambda kv: kv[1][1])
     flops = _gemm_flops(kind, w, n_valid, []) * args.steps
     achieved = flops / (kms / 1e3) / 1e12 if flops else None
-    traffic = _traffic_from_profiles(kind)
+    traffic = _traffic_from_profiles(kind, w.name)
     roofline = {"kernel": kind, "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": (achieved / PEAK_BF16_TFLOPS) if achieved else None,
                 "traffic": traffic, "launches_per_step": launches / args.steps,
                 "avg_launch_ms": kms / launches}
-    per_tok = {"fwd_bf16": 2, "fwdbwd_bf16": 6, "ragged_bf16": 6, "double_bf16": 8}[args.workload]
-    executed = {"fwd_bf16": 2, "fwdbwd_bf16": 8, "ragged_bf16": 8, "double_bf16": 10}[args.workload]
+    per_tok = {"fwd_bf16": 2, "fwdbwd_bf16": 6, "ragged_bf16": 6, "double_bf16": 8,
+               "sft_bf16": 6}[args.workload]
+    executed = {"fwd_bf16": 2, "fwdbwd_bf16": 8, "ragged_bf16": 8, "double_bf16": 10,
+                "sft_bf16": 8}[args.workload]
     step_s = ms_per_step / 1e3
     alg_frac = per_tok * n_valid * V * H / step_s / (PEAK_BF16_TFLOPS * 1e12)
     exe_frac = executed * n_valid * V * H / step_s / (PEAK_BF16_TFLOPS * 1e12)
 
     res = {
-        "metric": METRIC,
+        "metric": METRIC_SFT if sft else METRIC,
         "value": tokens_per_s,
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -242,10 +262,14 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded numpy inputs: h RMS-normalised N(0,1), W N(0,0.02), "
-                "uniform token ids, Bernoulli rewards)",
-        "config": {"workload": w.name, "prompts": w.prompts, "group": w.group,
-                   "seq_len": w.seq_len, "valid_tokens": n_valid, "hidden": H, "vocab": V,
-                   "clip_eps": w.clip_eps, "beta": w.beta},
+                "uniform token ids" + (", prompt prefix unsupervised)" if sft else
+                                       ", Bernoulli rewards)"),
+        "config": ({"workload": w.name, "sequences": w.num_seqs, "seq_len": w.seq_len,
+                    "prompt_len": w.prompt_len, "valid_tokens": n_valid, "hidden": H,
+                    "vocab": V} if sft else
+                   {"workload": w.name, "prompts": w.prompts, "group": w.group,
+                    "seq_len": w.seq_len, "valid_tokens": n_valid, "hidden": H, "vocab": V,
+                    "clip_eps": w.clip_eps, "beta": w.beta}),
         "mfma_frac_algorithmic": alg_frac,
         "mfma_frac_executed": exe_frac,
         "roofline": roofline,

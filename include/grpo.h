@@ -78,7 +78,8 @@ typedef enum grpo_agg {
 /* Operation selector for grpo_workspace_bytes(). */
 typedef enum grpo_op {
   GRPO_OP_LOGPROB_FWD = 0,
-  GRPO_OP_LOSS_FWD_BWD = 1
+  GRPO_OP_LOSS_FWD_BWD = 1,
+  GRPO_OP_SFT_FWD_BWD = 2
 } grpo_op;
 
 /*
@@ -186,8 +187,36 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
                               int32_t accumulate_grad_weight, void* workspace,
                               size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * sft_ce_fwd_bwd -- the supervised fine-tuning stage that precedes GRPO
+ * (AutoTriton Sec. 3.2; sequences of up to 16,384 tokens, Sec. 4.1): the
+ * next-token cross-entropy of the LM head, averaged over the supervised
+ * tokens, and its gradients, again without storing the logits:
+ *   loss = -(1 / n_valid) * sum_{valid t} logp_t      (0 when n_valid = 0)
+ * with logp_t as in grpo_logprob_fwd (tokens_t is the target id of row t;
+ * the caller shifts labels). dL/dlogp_t = -1 / n_valid, and dL/dhidden,
+ * dL/dweight follow through the log-softmax exactly as in grpo_loss_fwd_bwd.
+ *
+ *   dt, hidden, weight, tokens, mask, N, H, V   as grpo_logprob_fwd (mask
+ *               marks the supervised rows, e.g. the response tokens).
+ *   loss        [1] fp32 output, fixed-order reduction. Device.
+ *   logp_out    [N] fp32 or NULL (0 on masked rows). Device.
+ *   grad_hidden, grad_hidden_dt, grad_weight, accumulate_grad_weight
+ *               as grpo_loss_fwd_bwd (either gradient may be NULL).
+ * workspace >= grpo_workspace_bytes(GRPO_OP_SFT_FWD_BWD, dt, N, H, V, 1).
+ * Errors as grpo_loss_fwd_bwd (a token id outside [0, V) sets the flag that
+ * grpo_check_error reports).
+ */
+grpo_status sft_ce_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight,
+                           const int64_t* tokens, const uint8_t* mask, int64_t N, int64_t H,
+                           int64_t V, float* loss, float* logp_out, void* grad_hidden,
+                           grpo_dtype grad_hidden_dt, float* grad_weight,
+                           int32_t accumulate_grad_weight, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream);
+
 /* Bytes of workspace an operation needs for these sizes (0 if the sizes are
- * invalid). For GRPO_OP_LOGPROB_FWD pass num_seqs = 1. Host only. */
+ * invalid). For GRPO_OP_LOGPROB_FWD and GRPO_OP_SFT_FWD_BWD pass
+ * num_seqs = 1. Host only. */
 size_t grpo_workspace_bytes(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V,
                             int64_t num_seqs);
 

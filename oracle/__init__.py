@@ -72,6 +72,9 @@ def _load():
                                          _D, _dbl, _dbl, ctypes.c_int, _D, _vp, _vp, _vp, _vp,
                                          _vp, _vp, _vp]
         lib.oracle_grpo_loss.restype = _i64
+        lib.oracle_sft_ce.argtypes = [_D, _D, _I, _vp, _i64, _i64, _i64, _D, _vp, _vp, _vp,
+                                      _vp, _vp]
+        lib.oracle_sft_ce.restype = _i64
         _lib = lib
     return _lib
 
@@ -189,4 +192,22 @@ def grpo_loss(h, W, tokens, mask, cu_seqlens, old, ref, adv_seq, eps: float, bet
         _ptr(out["logp"]), _ptr(out["ell"]), _ptr(out["g"]), _ptr(out["clipped"]), _ptr(dh),
         _ptr(dW))
     out.update(loss=float(loss[0]), dh=dh, dW=dW, nvalid=int(nvalid))
+    return out
+
+
+def sft_ce(h, W, tokens, mask=None, want_dh: bool = True, want_dW: bool = True) -> dict:
+    """SFT cross-entropy (mean of -logp over valid rows) and its gradients."""
+    h = _f64(h)
+    W = _f64(W)
+    N, H = h.shape
+    V = W.shape[0]
+    m = None if mask is None else np.ascontiguousarray(mask, dtype=np.uint8)
+    out = dict(lse=np.empty(N), logp=np.empty(N), g=np.empty(N))
+    dh = np.empty((N, H)) if want_dh else None
+    dW = np.empty((V, H)) if want_dW else None
+    loss = np.zeros(1)
+    n = _load().oracle_sft_ce(h, W, np.ascontiguousarray(tokens, dtype=np.int64), _ptr(m), N, H,
+                              V, loss, _ptr(out["lse"]), _ptr(out["logp"]), _ptr(out["g"]),
+                              _ptr(dh), _ptr(dW))
+    out.update(loss=float(loss[0]), dh=dh, dW=dW, nvalid=int(n))
     return out

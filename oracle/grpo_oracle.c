@@ -18,6 +18,10 @@
  *   - the exact analytic gradients of that loss with respect to the hidden
  *     states h and the LM-head weight W.
  *
+ *   - the supervised stage before it (Sec. 3.2): the mean over supervised
+ *     tokens of the next-token cross-entropy -log pi_theta(y_t), and its
+ *     gradients through the same log-softmax.
+ *
  * Everything is written the slow, direct way: logits rows are materialised
  * in full, sums run in index order, and nothing is blocked or fused.
  * Parallelism is OpenMP over independent tokens or vocabulary rows only.
@@ -275,4 +279,42 @@ int64_t oracle_grpo_loss(const double* h, const double* W, const int64_t* y, con
   free(counts); free(seq); free(cseq); free(lse); free(logp); free(ell); free(g);
   free(a_tok); free(c_tok); free(clipped);
   return nvalid;
+}
+
+/* ------------------------------------------------------- SFT (Sec. 3.2) */
+/* Supervised cross-entropy over the valid rows (mask NULL = all rows):
+ * loss = -(1/n) sum_{valid t} logp_t, n = number of valid rows (loss 0 when
+ * n = 0). dL/dlogp_t = -1/n on valid rows and 0 elsewhere; dh and dW follow
+ * through the log-softmax with the row gradient functions above. Outputs
+ * other than loss may be NULL. Returns n. */
+int64_t oracle_sft_ce(const double* h, const double* W, const int64_t* y, const uint8_t* mask,
+                      int64_t N, int64_t H, int64_t V, double* loss, double* lse_out,
+                      double* logp_out, double* g_out, double* dh, double* dW) {
+  double* lse = (double*)calloc((size_t)N, sizeof(double));
+  double* logp = (double*)calloc((size_t)N, sizeof(double));
+  double* g = (double*)calloc((size_t)N, sizeof(double));
+  int64_t n = 0;
+  for (int64_t t = 0; t < N; ++t)
+    if (mask == NULL || mask[t]) ++n;
+  oracle_score_rows(h, W, y, N, H, V, lse, logp, NULL);
+  double s = 0.0;
+  for (int64_t t = 0; t < N; ++t) {
+    int valid = (mask == NULL || mask[t]);
+    if (valid) {
+      s += logp[t];
+      g[t] = -1.0 / (double)n;
+    } else {
+      lse[t] = 0.0;
+      logp[t] = 0.0;
+      g[t] = 0.0;
+    }
+  }
+  *loss = n > 0 ? -s / (double)n : 0.0;
+  if (lse_out) memcpy(lse_out, lse, sizeof(double) * (size_t)N);
+  if (logp_out) memcpy(logp_out, logp, sizeof(double) * (size_t)N);
+  if (g_out) memcpy(g_out, g, sizeof(double) * (size_t)N);
+  if (dh) oracle_grad_hidden_rows(h, W, y, lse, g, N, H, V, dh);
+  if (dW) oracle_grad_weight_rows(h, W, y, lse, g, N, H, V, NULL, V, dW);
+  free(lse); free(logp); free(g);
+  return n;
 }

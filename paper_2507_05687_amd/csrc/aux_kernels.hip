@@ -321,7 +321,16 @@ __global__ void __launch_bounds__(256) k_token_objective(const TokenArgs a) {
     int32_t j = a.pidx[r];
     float lp = 0.f, l = 0.f, ell = 0.f, g = 0.f;
     uint8_t clipped = 0;
-    if (j >= 0) {
+    if (j >= 0 && a.objective == 1) {
+      // cross-entropy: ell = -logp, dL/dlogp = -1/n_valid
+      const float c = 1.f / (float)a.hdr->num_valid;
+      lp = a.logp_p[j];
+      l = a.lse_p[j];
+      ell = -lp;
+      g = -c;
+      a.g_p[j] = g;
+      contrib = c * ell;
+    } else if (j >= 0) {
       int32_t b = a.seq_p[j];
       int32_t cnt = a.counts[b];
       float c = a.agg == 0 ? 1.f / ((float)a.B * (float)cnt) : 1.f / (float)a.hdr->num_valid;

@@ -275,6 +275,115 @@ grpo_status run_scoring(const Layout& L, void* ws, grpo_dtype dt, const void* hi
   });
 }
 
+// S7: dz recomputed per vocabulary chunk from the scoring's lse and the
+// per-token g = dL/dlogp, then dL/dh = dz.W and dL/dW = dz^T.h. Shared by
+// the GRPO loss and the SFT cross-entropy.
+grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* hidden,
+                         const void* weight, const uint8_t* mask, int64_t N, int64_t H, int64_t V,
+                         void* grad_hidden, grpo_dtype grad_hidden_dt, float* grad_weight,
+                         int32_t accumulate_grad_weight, hipStream_t s) {
+  if (!grad_hidden && !grad_weight) return GRPO_OK;
+  WsHeader* hdr = at<WsHeader>(ws, L.hdr);
+  int32_t* rows_p = at<int32_t>(ws, L.rows);
+  int32_t* y_p = at<int32_t>(ws, L.y);
+  int32_t* pidx = at<int32_t>(ws, L.pidx);
+  float* lse_p = at<float>(ws, L.lse);
+  float* g_p = at<float>(ws, L.g);
+  if (dt == GRPO_F32) {
+    if (grad_hidden) {
+      TRY(timed(K_ZERO_ROWS, s, [&] { launch_zero_masked_rows(pidx, N, H, grad_hidden, 0, s); }));
+      TRY(timed(K_F32_DH, s, [&] {
+        launch_f32_grad_hidden((const float*)hidden, (const float*)weight, H, V, rows_p, y_p,
+                               lse_p, g_p, hdr, (float*)grad_hidden, N, s);
+      }));
+    }
+    if (grad_weight) {
+      TRY(timed(K_F32_DW, s, [&] {
+        launch_f32_grad_weight((const float*)hidden, (const float*)weight, H, V, rows_p, y_p,
+                               lse_p, g_p, hdr, grad_weight, accumulate_grad_weight != 0, s);
+      }));
+    }
+    return GRPO_OK;
+  }
+
+  uint16_t* hT = at<uint16_t>(ws, L.hT);
+  uint16_t* WT = at<uint16_t>(ws, L.WT);
+  uint16_t* dz = at<uint16_t>(ws, L.dz);
+  uint16_t* dzT = at<uint16_t>(ws, L.dzT);
+  float* dhacc = L.nchunks > 1 ? at<float>(ws, L.dhacc) : nullptr;
+  // Intermediates in the tiled layout: h^T [H x tokens], W^T [H x V],
+  // dz [tokens x chunk] and dz^T [chunk x tokens].
+  const int64_t kt_tok = L.sTok, kt_voc = L.sVoc, kt_chunk = L.sChunk, kt_h = L.sK;
+  if (grad_weight) {
+    TRY(timed(K_TRANSPOSE, s, [&] {
+      launch_transpose_tiled((const uint16_t*)hidden, H, rows_p, 0, hdr, L.Npad, H, kt_tok, hT,
+                             s);
+    }));
+  }
+  if (grad_hidden) {
+    TRY(timed(K_TRANSPOSE, s, [&] {
+      launch_transpose_tiled((const uint16_t*)weight, H, nullptr, V, nullptr, L.Vpad, H, kt_voc,
+                             WT, s);
+    }));
+  }
+  for (int64_t c = 0; c < L.nchunks; ++c) {
+    int64_t v0 = c * L.Vc;
+    int64_t Mc = V - v0 < L.Vc ? V - v0 : L.Vc;
+    if (Mc <= 0) break;
+    bool last = (c == L.nchunks - 1) || (v0 + L.Vc >= V);
+    // recompute the logits of this chunk and form dz (both layouts)
+    GemmArgs gz = gemm_args(at<uint16_t>(ws, L.WK) + (v0 / kTile) * kt_h * kTileElems, kt_h, Mc,
+                            at<uint16_t>(ws, L.hK), kt_h, L.Npad, nullptr, &hdr->num_valid, L.Hk,
+                            nullptr);
+    TRY(timed(K_GEMM_DZ, s, [&] {
+      launch_gemm_dz(gz, y_p, lse_p, g_p, dz, kt_chunk, grad_weight ? dzT : nullptr, kt_tok, V, v0,
+                     s);
+    }));
+    if (grad_hidden) {
+      // dh[t, :] (+)= sum_{v in chunk} dz[t, v] W[v, :]
+      GemmArgs gh = gemm_args(dz, kt_chunk, L.Npad, WT, kt_voc, H, &hdr->num_valid, nullptr,
+                              round_up(Mc, kBK), nullptr);
+      gh.b_kb0 = v0 / kBK;
+      StoreArgs sa{};
+      sa.acc_buf = dhacc;
+      sa.ld_acc = round_up(H, kTile);
+      sa.read_acc = c > 0;
+      sa.out = last ? grad_hidden : nullptr;
+      sa.ld_out = H;
+      sa.out_bf16 = grad_hidden_dt == GRPO_BF16;
+      sa.add_out = 0;
+      sa.out_rows = rows_p;
+      sa.m_limit = L.Npad;
+      sa.n_limit = H;
+      TRY(timed(K_GEMM_DH, s, [&] { launch_gemm_store(gh, sa, false, s); }));
+    }
+    if (grad_weight) {
+      // dW[v, :] = sum_t dz[t, v] h[t, :] over the valid tokens
+      GemmArgs gw = gemm_args(dzT, kt_tok, Mc, hT, kt_tok, H, nullptr, nullptr, 0,
+                              &hdr->num_valid);
+      StoreArgs sa{};
+      sa.acc_buf = nullptr;
+      sa.ld_acc = 0;
+      sa.read_acc = 0;
+      sa.out = grad_weight + v0 * H;
+      sa.ld_out = H;
+      sa.out_bf16 = 0;
+      sa.add_out = accumulate_grad_weight != 0;
+      sa.out_rows = nullptr;
+      sa.m_limit = Mc;
+      sa.n_limit = H;
+      TRY(timed(K_GEMM_DW, s, [&] { launch_gemm_store(gw, sa, true, s); }));
+    }
+    if (last) break;
+  }
+  if (grad_hidden && mask) {
+    TRY(timed(K_ZERO_ROWS, s, [&] {
+      launch_zero_masked_rows(pidx, N, H, grad_hidden, grad_hidden_dt == GRPO_BF16, s);
+    }));
+  }
+  return GRPO_OK;
+}
+
 }  // namespace
 
 // ======================================================================
@@ -299,8 +408,10 @@ const char* grpo_status_string(grpo_status st) {
 
 size_t grpo_workspace_bytes(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V,
                             int64_t num_seqs) {
-  if (op != GRPO_OP_LOGPROB_FWD && op != GRPO_OP_LOSS_FWD_BWD) return 0;
+  if (op != GRPO_OP_LOGPROB_FWD && op != GRPO_OP_LOSS_FWD_BWD && op != GRPO_OP_SFT_FWD_BWD)
+    return 0;
   if (check_sizes(dt, N, H, V) != GRPO_OK || num_seqs < 1) return 0;
+  if (op == GRPO_OP_SFT_FWD_BWD) return layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, 1).total;
   return layout(op, dt, N, H, V, num_seqs).total;
 }
 
@@ -417,6 +528,7 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
 
   // S1 consumer, S5, S6: per-token objective, g = dL/dlogp, the loss.
   TokenArgs ta;
+  ta.objective = 0;
   ta.N = N;
   ta.B = num_seqs;
   ta.pidx = pidx;
@@ -444,99 +556,55 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
   if (!grad_hidden && !grad_weight) return GRPO_OK;
 
   // S7: gradients.
-  if (dt == GRPO_F32) {
-    if (grad_hidden) {
-      TRY(timed(K_ZERO_ROWS, s, [&] { launch_zero_masked_rows(pidx, N, H, grad_hidden, 0, s); }));
-      TRY(timed(K_F32_DH, s, [&] {
-        launch_f32_grad_hidden((const float*)hidden, (const float*)weight, H, V, rows_p, y_p,
-                               lse_p, g_p, hdr, (float*)grad_hidden, N, s);
-      }));
-    }
-    if (grad_weight) {
-      TRY(timed(K_F32_DW, s, [&] {
-        launch_f32_grad_weight((const float*)hidden, (const float*)weight, H, V, rows_p, y_p,
-                               lse_p, g_p, hdr, grad_weight, accumulate_grad_weight != 0, s);
-      }));
-    }
-    return GRPO_OK;
-  }
+  return run_backward(L, ws, dt, hidden, weight, mask, N, H, V, grad_hidden, grad_hidden_dt,
+                      grad_weight, accumulate_grad_weight, s);
+}
 
-  uint16_t* hT = at<uint16_t>(ws, L.hT);
-  uint16_t* WT = at<uint16_t>(ws, L.WT);
-  uint16_t* dz = at<uint16_t>(ws, L.dz);
-  uint16_t* dzT = at<uint16_t>(ws, L.dzT);
-  float* dhacc = L.nchunks > 1 ? at<float>(ws, L.dhacc) : nullptr;
-  // Intermediates in the tiled layout: h^T [H x tokens], W^T [H x V],
-  // dz [tokens x chunk] and dz^T [chunk x tokens].
-  const int64_t kt_tok = L.sTok, kt_voc = L.sVoc, kt_chunk = L.sChunk, kt_h = L.sK;
-  if (grad_weight) {
-    TRY(timed(K_TRANSPOSE, s, [&] {
-      launch_transpose_tiled((const uint16_t*)hidden, H, rows_p, 0, hdr, L.Npad, H, kt_tok, hT,
-                             s);
-    }));
-  }
-  if (grad_hidden) {
-    TRY(timed(K_TRANSPOSE, s, [&] {
-      launch_transpose_tiled((const uint16_t*)weight, H, nullptr, V, nullptr, L.Vpad, H, kt_voc,
-                             WT, s);
-    }));
-  }
-  for (int64_t c = 0; c < L.nchunks; ++c) {
-    int64_t v0 = c * L.Vc;
-    int64_t Mc = V - v0 < L.Vc ? V - v0 : L.Vc;
-    if (Mc <= 0) break;
-    bool last = (c == L.nchunks - 1) || (v0 + L.Vc >= V);
-    // recompute the logits of this chunk and form dz (both layouts)
-    GemmArgs gz = gemm_args(at<uint16_t>(ws, L.WK) + (v0 / kTile) * kt_h * kTileElems, kt_h, Mc,
-                            at<uint16_t>(ws, L.hK), kt_h, L.Npad, nullptr, &hdr->num_valid, L.Hk,
-                            nullptr);
-    TRY(timed(K_GEMM_DZ, s, [&] {
-      launch_gemm_dz(gz, y_p, lse_p, g_p, dz, kt_chunk, grad_weight ? dzT : nullptr, kt_tok, V, v0,
-                     s);
-    }));
-    if (grad_hidden) {
-      // dh[t, :] (+)= sum_{v in chunk} dz[t, v] W[v, :]
-      GemmArgs gh = gemm_args(dz, kt_chunk, L.Npad, WT, kt_voc, H, &hdr->num_valid, nullptr,
-                              round_up(Mc, kBK), nullptr);
-      gh.b_kb0 = v0 / kBK;
-      StoreArgs sa{};
-      sa.acc_buf = dhacc;
-      sa.ld_acc = round_up(H, kTile);
-      sa.read_acc = c > 0;
-      sa.out = last ? grad_hidden : nullptr;
-      sa.ld_out = H;
-      sa.out_bf16 = grad_hidden_dt == GRPO_BF16;
-      sa.add_out = 0;
-      sa.out_rows = rows_p;
-      sa.m_limit = L.Npad;
-      sa.n_limit = H;
-      TRY(timed(K_GEMM_DH, s, [&] { launch_gemm_store(gh, sa, false, s); }));
-    }
-    if (grad_weight) {
-      // dW[v, :] = sum_t dz[t, v] h[t, :] over the valid tokens
-      GemmArgs gw = gemm_args(dzT, kt_tok, Mc, hT, kt_tok, H, nullptr, nullptr, 0,
-                              &hdr->num_valid);
-      StoreArgs sa{};
-      sa.acc_buf = nullptr;
-      sa.ld_acc = 0;
-      sa.read_acc = 0;
-      sa.out = grad_weight + v0 * H;
-      sa.ld_out = H;
-      sa.out_bf16 = 0;
-      sa.add_out = accumulate_grad_weight != 0;
-      sa.out_rows = nullptr;
-      sa.m_limit = Mc;
-      sa.n_limit = H;
-      TRY(timed(K_GEMM_DW, s, [&] { launch_gemm_store(gw, sa, true, s); }));
-    }
-    if (last) break;
-  }
-  if (grad_hidden && mask) {
-    TRY(timed(K_ZERO_ROWS, s, [&] {
-      launch_zero_masked_rows(pidx, N, H, grad_hidden, grad_hidden_dt == GRPO_BF16, s);
-    }));
-  }
-  return GRPO_OK;
+grpo_status sft_ce_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight,
+                           const int64_t* tokens, const uint8_t* mask, int64_t N, int64_t H,
+                           int64_t V, float* loss, float* logp_out, void* grad_hidden,
+                           grpo_dtype grad_hidden_dt, float* grad_weight,
+                           int32_t accumulate_grad_weight, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  TRY(check_sizes(dt, N, H, V));
+  if (!hidden || !weight || !tokens || !loss) return GRPO_ERR_NULL;
+  if (grad_hidden && grad_hidden_dt != GRPO_F32 && grad_hidden_dt != GRPO_BF16)
+    return GRPO_ERR_DTYPE;
+  if (grad_hidden && dt == GRPO_F32 && grad_hidden_dt != GRPO_F32) return GRPO_ERR_DTYPE;
+  size_t al = dt == GRPO_BF16 ? 16 : 4;
+  if (!aligned(hidden, al) || !aligned(weight, al) || !aligned(tokens, 8) || !aligned(loss, 4))
+    return GRPO_ERR_ALIGN;
+  if ((logp_out && !aligned(logp_out, 4)) || (grad_hidden && !aligned(grad_hidden, 4)) ||
+      (grad_weight && !aligned(grad_weight, 4)))
+    return GRPO_ERR_ALIGN;
+  Layout L = layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, 1);
+  TRY(check_ws(workspace, workspace_bytes, L));
+  TRY(check_device());
+  void* ws = workspace;
+  hipStream_t s = stream;
+
+  // one "sequence" covering every row; the mask selects the supervised rows
+  TRY(run_pack(L, ws, mask, tokens, V, nullptr, 1, N, nullptr, nullptr, nullptr, s));
+  if (dt == GRPO_BF16) TRY(run_tiles(L, ws, hidden, weight, H, V, s));
+  TRY(run_scoring(L, ws, dt, hidden, weight, N, H, V, s));
+
+  TokenArgs ta{};
+  ta.objective = 1;
+  ta.N = N;
+  ta.B = 1;
+  ta.pidx = at<int32_t>(ws, L.pidx);
+  ta.seq_p = at<int32_t>(ws, L.seq);
+  ta.counts = at<int32_t>(ws, L.counts);
+  ta.hdr = at<WsHeader>(ws, L.hdr);
+  ta.logp_p = at<float>(ws, L.logp);
+  ta.lse_p = at<float>(ws, L.lse);
+  ta.g_p = at<float>(ws, L.g);
+  ta.logp_out = logp_out;
+  ta.loss_part = at<float>(ws, L.lpart);
+  ta.loss = loss;
+  TRY(timed(K_TOKEN, s, [&] { launch_token_objective(ta, s); }));
+  return run_backward(L, ws, dt, hidden, weight, mask, N, H, V, grad_hidden, grad_hidden_dt,
+                      grad_weight, accumulate_grad_weight, s);
 }
 
 grpo_status grpo_check_error(void* workspace, hipStream_t stream) {

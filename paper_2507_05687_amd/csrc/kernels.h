@@ -61,7 +61,10 @@ struct PackArgs {
 void launch_pack(const PackArgs& a, hipStream_t s);
 
 // ------------------------------------------------ token objective (Eq. 1)
+// objective 0: the GRPO surrogate of Eq. 1; objective 1: the supervised
+// cross-entropy of the SFT stage (mean over valid tokens of -logp).
 struct TokenArgs {
+  int objective;
   int64_t N, B;
   const int32_t* pidx;
   const int32_t* seq_p;

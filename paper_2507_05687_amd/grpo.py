@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(_PKG, "libgrpo.so")
 
 F32, BF16 = 0, 1
 AGG_SEQ_MEAN, AGG_TOKEN_MEAN = 0, 1
-OP_LOGPROB_FWD, OP_LOSS_FWD_BWD = 0, 1
+OP_LOGPROB_FWD, OP_LOSS_FWD_BWD, OP_SFT_FWD_BWD = 0, 1, 2
 
 STATUS = {0: "GRPO_OK", 1: "GRPO_ERR_NULL", 2: "GRPO_ERR_SHAPE", 3: "GRPO_ERR_DTYPE",
           4: "GRPO_ERR_PARAM", 5: "GRPO_ERR_ALIGN", 6: "GRPO_ERR_WORKSPACE",
@@ -35,6 +35,8 @@ SIGNATURES = {
     "grpo_loss_fwd_bwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _vp, _vp,
                                  _vp, _f32, _f32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                  _i32, _vp, _i32, _vp, _sz, _vp]),
+    "sft_ce_fwd_bwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp, _i32,
+                              _vp, _i32, _vp, _sz, _vp]),
     "grpo_workspace_bytes": (_sz, [_i32, _i32, _i64, _i64, _i64, _i64]),
     "grpo_check_error": (_i32, [_vp, _vp]),
     "grpo_status_string": (ctypes.c_char_p, [_i32]),
@@ -235,6 +237,46 @@ def loss_fwd_bwd(hidden, weight, tokens, mask, cu_seqlens, old_logp, ref_logp, a
         _dt(out["grad_hidden"]) if grad_hidden else F32, _ptr(g("grad_weight")),
         int(accumulate_grad_weight), _ptr(ws), ws.numel(), _stream())
     _check(st, "grpo_loss_fwd_bwd")
+    if check:
+        check_error(ws)
+    return out
+
+
+def sft_ce_fwd_bwd(hidden, weight, tokens, mask=None, grad_hidden: bool = True,
+                   grad_weight: bool = True, grad_hidden_dtype=None,
+                   grad_weight_out: torch.Tensor | None = None,
+                   accumulate_grad_weight: bool = False, logp_out: bool = True,
+                   check: bool = False) -> dict:
+    """SFT next-token cross-entropy (mean over supervised tokens) and its gradients.
+    Returns loss [1], logp [N] (if logp_out), grad_hidden [N,H], grad_weight [V,H] fp32."""
+    _need(hidden, "hidden")
+    _need(weight, "weight", hidden.dtype)
+    _need(tokens, "tokens", torch.int64)
+    N, H = hidden.shape
+    V = weight.shape[0]
+    dt = _dt(hidden)
+    dev = hidden.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    out = {"loss": torch.empty(1, **f32)}
+    if logp_out:
+        out["logp"] = torch.empty(N, **f32)
+    gh_dt = hidden.dtype if grad_hidden_dtype is None else grad_hidden_dtype
+    if grad_hidden:
+        out["grad_hidden"] = torch.empty(N, H, dtype=gh_dt, device=dev)
+    if grad_weight:
+        if grad_weight_out is not None:
+            out["grad_weight"] = _need(grad_weight_out, "grad_weight_out", torch.float32)
+        else:
+            out["grad_weight"] = torch.empty(V, H, **f32)
+    ws = workspace(workspace_bytes(OP_SFT_FWD_BWD, dt, N, H, V, 1), dev)
+    m = None if mask is None else _need(mask, "mask").view(torch.uint8)
+    g = out.get
+    st = load().sft_ce_fwd_bwd(
+        dt, _ptr(hidden), _ptr(weight), _ptr(tokens), _ptr(m), N, H, V, _ptr(out["loss"]),
+        _ptr(g("logp")), _ptr(g("grad_hidden")),
+        _dt(out["grad_hidden"]) if grad_hidden else F32, _ptr(g("grad_weight")),
+        int(accumulate_grad_weight), _ptr(ws), ws.numel(), _stream())
+    _check(st, "sft_ce_fwd_bwd")
     if check:
         check_error(ws)
     return out

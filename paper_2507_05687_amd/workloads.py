@@ -15,6 +15,10 @@ data, which these seeded synthetic tensors stand in for):
 * ``fwdbwd_bf16``   8 x 8 x 2048 tokens (N=131072), loss fwd+bwd.
 * ``ragged_bf16``   16 x 8 rollouts, lengths U{256..8192}, padded to 8192.
 * ``double_bf16``   16 x 8 x 2048 tokens (N=262144), policy + reference.
+* ``sft_bf16``      the supervised stage before GRPO (Sec. 3.2): one sequence
+                    of 16384 tokens per GPU (the paper's maximum length and
+                    per-device batch of 1, Sec. 4.1), the first 2048 (the
+                    prompt) not supervised.
 """
 from __future__ import annotations
 
@@ -49,6 +53,8 @@ class Workload:
     weight_sigma: float = 0.02
     seed: int = 0
     fwd_only: bool = False
+    objective: str = "grpo"  # "grpo" (Eq. 1) or "sft" (cross-entropy)
+    prompt_len: int = 0  # leading tokens of each sequence left out of the mask
 
     @property
     def num_seqs(self) -> int:
@@ -71,6 +77,8 @@ WORKLOADS = {
                             rms_norm_hidden=True, seed=3),
     "double_bf16": Workload("double_bf16", 16, 8, 2048, 4096, 155136, "bf16", 0.2, 0.001,
                             0.1, "fmt_exec", rms_norm_hidden=True, double_scoring=True, seed=4),
+    "sft_bf16": Workload("sft_bf16", 1, 1, 16384, 4096, 155136, "bf16", rms_norm_hidden=True,
+                         objective="sft", prompt_len=2048, seed=5),
 }
 
 
@@ -167,7 +175,8 @@ def make_batch(w: Workload) -> dict:
         lengths = g.integers(w.min_len, T + 1, size=B, dtype=np.int64)
     else:
         lengths = np.full(B, T, dtype=np.int64)
-    mask = (np.arange(T)[None, :] < lengths[:, None]).astype(np.uint8).reshape(N)
+    pos = np.arange(T)[None, :]
+    mask = ((pos < lengths[:, None]) & (pos >= w.prompt_len)).astype(np.uint8).reshape(N)
     cu = np.arange(B + 1, dtype=np.int64) * T
     if w.reward_kind == "thirds":
         rewards = g.integers(0, 3, size=B).astype(np.float32) * np.float32(0.5)

@@ -31,8 +31,8 @@ def _declared_functions():
 def test_header_declares_the_boundary():
     names = _declared_functions()
     for required in ("group_advantages", "grpo_logprob_fwd", "grpo_loss_fwd_bwd",
-                     "grpo_pack_valid", "grpo_workspace_bytes", "grpo_check_error",
-                     "grpo_status_string"):
+                     "sft_ce_fwd_bwd", "grpo_pack_valid", "grpo_workspace_bytes",
+                     "grpo_check_error", "grpo_status_string"):
         assert required in names
 
 
@@ -62,6 +62,9 @@ def test_workspace_bytes(lib):
     assert ws(0, 0, 10, 60, 1000, 1) > 0       # fp32 does not
     assert ws(0, 7, 10, 64, 1000, 1) == 0      # unknown dtype
     assert ws(9, 1, 10, 64, 1000, 1) == 0      # unknown op
+    # SFT uses the loss layout with one sequence
+    assert ws(2, 1, 100, 64, 1000, 1) == ws(1, 1, 100, 64, 1000, 1)
+    assert ws(2, 1, 100, 60, 1000, 1) == 0
     # full-size loss workspace stays well inside one MI355X's 288 GB
     assert ws(1, 1, 131072, 4096, 155136, 64) < 32 << 30
 
@@ -118,6 +121,28 @@ def test_other_entry_point_errors(lib):
     assert pk(NULL, P, 0, 8, P, P, P, P, 1 << 30, NULL) == 2
     assert pk(NULL, P, 2, 8, P, P, P, NULL, 0, NULL) == 6
     assert lib.grpo_check_error(NULL, NULL) == 1
+
+
+def _sft(lib, **kw):
+    a = dict(dt=1, hidden=P, weight=P, tokens=P, mask=NULL, N=8, H=64, V=100, loss=P,
+             logp=NULL, gh=NULL, gh_dt=1, gw=NULL, acc=0, ws=NULL, ws_bytes=0, stream=NULL)
+    a.update(kw)
+    return lib.sft_ce_fwd_bwd(*a.values())
+
+
+def test_sft_argument_errors(lib):
+    assert _sft(lib, hidden=NULL) == 1
+    assert _sft(lib, tokens=NULL) == 1
+    assert _sft(lib, loss=NULL) == 1
+    assert _sft(lib, N=0) == 2
+    assert _sft(lib, H=60) == 2
+    assert _sft(lib, dt=4) == 3
+    assert _sft(lib, gh=P, gh_dt=7) == 3
+    assert _sft(lib, dt=0, gh=P, gh_dt=1) == 3
+    assert _sft(lib, weight=ctypes.c_void_p(0x1008)) == 5
+    assert _sft(lib, logp=ctypes.c_void_p(0x1002)) == 5
+    assert _sft(lib) == 6                           # no workspace
+    assert _sft(lib, ws=P, ws_bytes=16) == 6        # too small
 
 
 def test_profile_interface_without_launches(lib):

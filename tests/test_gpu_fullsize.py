@@ -8,6 +8,9 @@ configuration bench.py times. GPU only.
 * reduced N (256 tokens) at full H and V: dL/dW rows against the oracle.
 * ragged rollouts with all-equal reward groups, and the two-model
   (policy + reference) scoring sequence, at reduced sizes.
+* the SFT cross-entropy workload (one 16384-token sequence, prompt prefix
+  unsupervised): sampled rows' logp and dL/dh rows, the loss from the
+  per-token log-probs, and the dL/dW identities.
 """
 import math
 
@@ -196,3 +199,43 @@ def test_double_scoring_sequence():
     # device's and the oracle's log-prob
     rho = np.exp(host64(out["logp"]) - old)
     assert np.max(np.abs(rho - 1)) <= 1e-3
+
+
+def test_sft_full_size_sampled_rows_and_identities():
+    w = workloads.WORKLOADS["sft_bf16"]
+    W_bits = workloads.make_weight(w)
+    h_bits = workloads.make_hidden(w)
+    b = workloads.make_batch(w)
+    n_valid = int(b["mask"].sum())
+    rows = workloads.sample_rows(b["mask"], 16, seed=2)
+    Wd = oracle.decode(W_bits, "bf16")
+    hs = oracle.decode(h_bits[rows], "bf16")
+    o_lse, o_logp, _ = oracle.score_rows(hs, Wd, b["tokens"][rows])
+    hd, Wdv = to_dev(h_bits, "bf16"), to_dev(W_bits, "bf16")
+    mask = dev(b["mask"])
+    out = grpo.sft_ce_fwd_bwd(hd, Wdv, dev(b["tokens"]), mask, check=True)
+    torch.cuda.synchronize()
+    assert rel_err(host64(out["logp"])[rows], o_logp) <= TOL
+    o_dh = oracle.grad_hidden_rows(hs, Wd, b["tokens"][rows], o_lse,
+                                   np.full(len(rows), -1.0 / n_valid))
+    dh = host64(out["grad_hidden"][torch.from_numpy(rows).cuda()])
+    for i in range(len(rows)):
+        assert norm_rel(dh[i], o_dh[i]) <= GRAD_TOL, (i, norm_rel(dh[i], o_dh[i]))
+    del Wd
+    # masked rows: zero log-prob and gradient
+    m = mask.bool()
+    assert out["logp"][~m].abs().max().item() == 0.0
+    assert out["grad_hidden"][~m].float().abs().max().item() == 0.0
+    # the loss is minus the mean of the per-token log-probs it also returns
+    want = -float(out["logp"].double().sum()) / n_valid
+    assert abs(out["loss"].item() - want) <= 1e-5 * abs(want)
+    # dL/dW identities (as for the GRPO loss, with g_t = -1/n on valid rows)
+    gw = out["grad_weight"]
+    hf = hd.double()
+    colsum = gw.double().sum(0)
+    bound = 2.0 ** -7 * (hf.abs() * m.double()[:, None]).sum(0) / n_valid + 1e-6
+    assert torch.all(colsum.abs() <= bound), float((colsum.abs() / bound).max())
+    a = float((gw.double() * Wdv.double()).sum())
+    bb = float((out["grad_hidden"].double() * hf).sum())
+    assert abs(a - bb) <= 5e-3 * max(abs(a), abs(bb)), (a, bb)
+

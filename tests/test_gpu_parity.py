@@ -157,7 +157,7 @@ SMALL = {
     # several tiles on every axis, ragged token and vocabulary tails
     "ragged_tiles": dict(prompts=3, group=4, seq_len=50, hidden=320, vocab=3000, ragged=True,
                          min_len=1, forced_equal_groups=1),
-    # H not a multiple of the 64-wide K step
+    # H not a multiple of the 32-wide K step
     "k_tail": dict(prompts=2, group=4, seq_len=40, hidden=200, vocab=1100),
     # several vocabulary chunks in the backward pass
     "multi_chunk": dict(prompts=2, group=4, seq_len=40, hidden=128, vocab=40000),
@@ -285,3 +285,67 @@ def test_all_rows_masked():
     assert out["loss"].item() == 0.0
     assert torch.all(out["logp"] == 0) and torch.all(out["dlogp"] == 0)
     assert torch.all(out["grad_hidden"] == 0) and torch.all(out["grad_weight"] == 0)
+
+
+# ------------------------------------------------------------ SFT cross-entropy
+def _sft_problem(**kw):
+    w = workloads.scaled(workloads.WORKLOADS["sft_bf16"], **kw)
+    return w, workloads.make_weight(w), workloads.make_hidden(w), workloads.make_batch(w)
+
+
+def _sft_compare(w, W, h, b, out, tol, grad_tol):
+    o = oracle.sft_ce(oracle.decode(h, w.dtype), oracle.decode(W, w.dtype), b["tokens"],
+                      b["mask"])
+    m = b["mask"].astype(bool)
+    torch.cuda.synchronize()
+    assert abs(out["loss"].item() - o["loss"]) <= tol * max(abs(o["loss"]), 1e-30), \
+        (out["loss"].item(), o["loss"])
+    lp = host64(out["logp"])
+    assert rel_err(lp[m], o["logp"][m]) <= tol
+    assert np.all(lp[~m] == 0)
+    dh, dW = host64(out["grad_hidden"]), host64(out["grad_weight"])
+    assert norm_rel(dh, o["dh"]) <= grad_tol, norm_rel(dh, o["dh"])
+    assert norm_rel(dW, o["dW"]) <= grad_tol, norm_rel(dW, o["dW"])
+    assert np.all(dh[~m] == 0)
+    return o
+
+
+SFT_SMALL = {
+    # several tiles on every axis, ragged tails, a masked prompt prefix
+    "tiles": dict(prompts=3, group=2, seq_len=90, hidden=320, vocab=3000, prompt_len=17,
+                  ragged=True, min_len=20),
+    # H not a multiple of 32, several vocabulary chunks
+    "chunks": dict(prompts=1, group=2, seq_len=100, hidden=200, vocab=40000, prompt_len=30),
+}
+
+
+@pytest.mark.parametrize("case", list(SFT_SMALL))
+def test_sft_bf16_parity(case):
+    w, W, h, b = _sft_problem(**SFT_SMALL[case], seed=31)
+    out = grpo.sft_ce_fwd_bwd(to_dev(h, "bf16"), to_dev(W, "bf16"), dev(b["tokens"]),
+                              dev(b["mask"]), check=True)
+    _sft_compare(w, W, h, b, out, BF16_TOL, BF16_GRAD_TOL)
+
+
+def test_sft_fp32_parity():
+    w, W, h, b = _sft_problem(seq_len=64, hidden=64, vocab=1000, prompt_len=9, dtype="f32",
+                              rms_norm_hidden=False, seed=32)
+    out = grpo.sft_ce_fwd_bwd(to_dev(h, "f32"), to_dev(W, "f32"), dev(b["tokens"]),
+                              dev(b["mask"]), check=True)
+    _sft_compare(w, W, h, b, out, F32_TOL, F32_TOL)
+
+
+def test_sft_closed_forms():
+    """W = 0 gives loss = ln V exactly up to fp32 and dh = 0; no supervised row
+    gives loss 0 and zero gradients."""
+    w, W, h, b = _sft_problem(**SFT_SMALL["tiles"], seed=33)
+    Wz = torch.zeros(w.vocab, w.hidden, dtype=torch.bfloat16, device="cuda")
+    out = grpo.sft_ce_fwd_bwd(to_dev(h, "bf16"), Wz, dev(b["tokens"]), dev(b["mask"]))
+    assert out["loss"].item() == pytest.approx(math.log(w.vocab), rel=1e-6)
+    assert out["grad_hidden"].abs().max().item() == 0.0
+    none = torch.zeros(w.num_tokens, dtype=torch.uint8, device="cuda")
+    out = grpo.sft_ce_fwd_bwd(to_dev(h, "bf16"), to_dev(W, "bf16"), dev(b["tokens"]), none)
+    assert out["loss"].item() == 0.0
+    assert out["grad_hidden"].abs().max().item() == 0.0
+    assert out["grad_weight"].abs().max().item() == 0.0
+

@@ -382,3 +382,61 @@ def test_pieces_compose_to_the_whole(oracle_lib):
     vr = np.array([0, 3, 10])
     dW = oracle_lib.grad_weight_rows(p["h"][rows], p["W"], p["y"][rows], lse, g, vr)
     np.testing.assert_allclose(dW, p["dW"][vr], rtol=1e-12, atol=1e-15)
+
+
+# ------------------------------------------------------------ SFT (Sec. 3.2)
+@pytest.mark.parametrize("ragged", [False, True])
+def test_sft_matches_torch_cross_entropy(oracle_lib, ragged):
+    """SFT stage: mean next-token cross-entropy over the supervised rows, and its
+    gradients, against torch's fp64 cross_entropy + autograd (a library routine)."""
+    h, W, y, mask, _ = _rand_problem(21, ragged=ragged)
+    r = oracle_lib.sft_ce(h, W, y, mask)
+    ht = torch.from_numpy(h).requires_grad_(True)
+    Wt = torch.from_numpy(W).requires_grad_(True)
+    keep = torch.from_numpy(mask.astype(bool))
+    ce = torch.nn.functional.cross_entropy((ht @ Wt.T)[keep], torch.from_numpy(y)[keep])
+    ce.backward()
+    assert r["nvalid"] == int(mask.sum())
+    assert r["loss"] == pytest.approx(ce.item(), rel=1e-13)
+    np.testing.assert_allclose(r["dh"], ht.grad.numpy(), rtol=1e-10, atol=1e-14)
+    np.testing.assert_allclose(r["dW"], Wt.grad.numpy(), rtol=1e-10, atol=1e-14)
+    assert np.all(r["dh"][mask == 0] == 0.0)
+
+
+def test_sft_closed_forms(oracle_lib):
+    """W = 0: every row is uniform over V, so the loss is exactly ln V and dh = 0;
+    no supervised row: loss and gradients 0; a dominant target logit: loss -> 0."""
+    h, W, y, mask, _ = _rand_problem(22, V=1000)
+    r = oracle_lib.sft_ce(h, np.zeros_like(W), y, mask)
+    assert r["loss"] == pytest.approx(math.log(1000), rel=1e-15)
+    assert np.all(r["dh"] == 0.0)
+    r = oracle_lib.sft_ce(h, W, y, np.zeros_like(mask))
+    assert r["loss"] == 0.0 and r["nvalid"] == 0
+    assert np.all(r["dh"] == 0.0) and np.all(r["dW"] == 0.0)
+    hm = np.zeros_like(h)
+    hm[:, 0] = 1.0
+    Wm = np.zeros_like(W)
+    Wm[y[0], 0] = 60.0  # z = 60 at the target of row 0, 0 elsewhere
+    r = oracle_lib.sft_ce(hm[:1], Wm, y[:1])
+    assert r["loss"] == pytest.approx(math.log1p((1000 - 1) * math.exp(-60.0)), rel=1e-12)
+
+
+def test_sft_finite_differences(oracle_lib):
+    """Central differences of the SFT loss in h and W (fp64, step 1e-6)."""
+    h, W, y, mask, _ = _rand_problem(23, B=3, T=3, H=4, V=6, ragged=True)
+    r = oracle_lib.sft_ce(h, W, y, mask)
+    eps = 1e-6
+    for (i, k) in [(0, 0), (1, 3), (4, 2)]:
+        hp, hm = h.copy(), h.copy()
+        hp[i, k] += eps
+        hm[i, k] -= eps
+        fd = (oracle_lib.sft_ce(hp, W, y, mask)["loss"] -
+              oracle_lib.sft_ce(hm, W, y, mask)["loss"]) / (2 * eps)
+        assert r["dh"][i, k] == pytest.approx(fd, rel=1e-6, abs=1e-9)
+    for (v, k) in [(0, 1), (y[0], 2), (5, 3)]:
+        Wp, Wn = W.copy(), W.copy()
+        Wp[v, k] += eps
+        Wn[v, k] -= eps
+        fd = (oracle_lib.sft_ce(h, Wp, y, mask)["loss"] -
+              oracle_lib.sft_ce(h, Wn, y, mask)["loss"]) / (2 * eps)
+        assert r["dW"][v, k] == pytest.approx(fd, rel=1e-6, abs=1e-9)
