@@ -29,8 +29,20 @@ constexpr int kGN = 8;  // tile-columns per step of the walk
 // expcnt left at its maximum (7 in [6:4]), lgkmcnt 0 ([11:8]).
 constexpr int wait_vm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0070; }
 
-typedef __attribute__((address_space(1))) void* glb_ptr_t;
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// Operand loads go global -> LDS through a buffer resource based at the
+// tile-row's first block: each lane's offset is fixed, the K step goes in the
+// scalar offset, and one instruction moves 16 bytes per lane (1 KiB of
+// consecutive LDS at M0). Offsets stay far below 4 GiB (a tile-row of the
+// largest operand, 2^20 columns, is 512 MiB); the range check is off.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* base) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, -1, 0x00020000);
+}
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, char* lds, uint32_t voff,
+                                           uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)lds, 16, voff, soff, 0, 0);
+}
 
 // Maps a workgroup id to its (tile_m, tile_n); returns false for the
 // padding workgroups of the last band.
@@ -340,23 +352,21 @@ __global__ void __launch_bounds__(64 * kWaves, 1) k_gemm_bf16(GemmArgs g, Epi ep
   // (l%4) ^ ((q/4)%4); one instruction writes 1 KiB of consecutive LDS.
   const int qrow = 16 * w + (lane >> 2);
   const int qch = (lane & 3) ^ ((qrow >> 2) & 3);  // the same for q + 128j
-  const uint16_t* pa = g.A + ((int64_t)tm * g.a_kt + g.a_kb0) * kTileElems + qrow * 32 + qch * 8;
-  const uint16_t* pb = g.B + ((int64_t)tn * g.b_kt + g.b_kb0) * kTileElems + qrow * 32 + qch * 8;
-  // load l of a step: l < kJ is A part l, else B part l - kJ
-  auto load = [&](const uint16_t* a_step, const uint16_t* b_step, char* la, auto l) {
+  // load l of step kt (l < kJ: A part l, else B part l - kJ) into stage bytes la
+  const __amdgpu_buffer_rsrc_t ra = tile_rsrc(g.A + ((int64_t)tm * g.a_kt + g.a_kb0) * kTileElems);
+  const __amdgpu_buffer_rsrc_t rb = tile_rsrc(g.B + ((int64_t)tn * g.b_kt + g.b_kb0) * kTileElems);
+  const uint32_t lofs = (uint32_t)(qrow * 32 + qch * 8) * 2;
+  auto load = [&](int kt, char* la, auto l) {
+    const uint32_t so = (uint32_t)kt * (kTileElems * 2);
     if constexpr (l.value < kJ)
-      __builtin_amdgcn_global_load_lds((glb_ptr_t)(a_step + l.value * 16 * kWaves * 32),
-                                       (lds_ptr_t)(la + l.value * 1024 * kWaves), 16, 0, 0);
+      load_lds16(ra, la + l.value * 1024 * kWaves, lofs + l.value * 16 * kWaves * 64, so);
     else
-      __builtin_amdgcn_global_load_lds(
-          (glb_ptr_t)(b_step + (l.value - kJ) * 16 * kWaves * 32),
-          (lds_ptr_t)(la + kTileElems * 2 + (l.value - kJ) * 1024 * kWaves), 16, 0, 0);
+      load_lds16(rb, la + kTileElems * 2 + (l.value - kJ) * 1024 * kWaves,
+                 lofs + (l.value - kJ) * 16 * kWaves * 64, so);
   };
   auto load_step = [&](int kt, int stage) {
     char* la = smem + stage * kStage + w * 1024;
-    static_for<2 * kJ>([&](auto l) {
-      load(pa + (int64_t)kt * kTileElems, pb + (int64_t)kt * kTileElems, la, l);
-    });
+    static_for<2 * kJ>([&](auto l) { load(kt, la, l); });
   };
 
   // ---- fragment reads: lane reads row l%32 of each 32-row block, logical
@@ -407,28 +417,25 @@ __global__ void __launch_bounds__(64 * kWaves, 1) k_gemm_bf16(GemmArgs g, Epi ep
   // the B half of step kt+4's loads), wait for step kt+1, barrier, sub-step
   // 1 (with the A half of step kt+5's loads and the reads of step kt+1).
   // Past the end the last step is loaded again, into free stages only.
-  const uint16_t* na = pa;
-  const uint16_t* nb = pb;
+  int nkt = 0;
   char* nl = smem;
   for (int kt = 0; kt < nk; ++kt) {
     static_for<kMfmas>([&](auto m) {
       mfma(I0{}, m);
       if constexpr (m.value < 2) fread_half(I1{}, kt, 1, std::integral_constant<int, m.value>{});
       if constexpr (m.value % kSpread == kSpread - 1) {
-        if (kt > 0) load(na, nb, nl, std::integral_constant<int, kJ + m.value / kSpread>{});
+        if (kt > 0) load(nkt, nl, std::integral_constant<int, kJ + m.value / kSpread>{});
       }
       __builtin_amdgcn_sched_barrier(0);
     });
     __builtin_amdgcn_s_waitcnt(wait_vm(3 * kPerStep));  // step kt+1 has landed
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    const int64_t nxt = (int64_t)min(kt + kStages, last) * kTileElems;
-    na = pa + nxt;
-    nb = pb + nxt;
+    nkt = min(kt + kStages, last);
     nl = smem + (kt % kStages) * kStage + w * 1024;
     static_for<kMfmas>([&](auto m) {
       if constexpr (m.value % kSpread == kSpread - 1)
-        load(na, nb, nl, std::integral_constant<int, m.value / kSpread>{});
+        load(nkt, nl, std::integral_constant<int, m.value / kSpread>{});
       mfma(I1{}, m);
       if constexpr (m.value == 1 || m.value == 2)
         fread_half(I0{}, kt + 1, 0, std::integral_constant<int, m.value - 1>{});
@@ -441,10 +448,141 @@ __global__ void __launch_bounds__(64 * kWaves, 1) k_gemm_bf16(GemmArgs g, Epi ep
   epi(acc, f, m_valid, n_valid, smem);
 }
 
+// ---- four-wave variant: one wave per SIMD, each owning 128x128 as 4x4
+// blocks (256 fp32 accumulators per lane, in AGPRs). A wave reads the
+// fragments of a whole K step (both 16-wide sub-steps, 64 VGPRs) into
+// registers one step ahead, so its MFMAs never wait on LDS; the barrier at
+// the end of step kt (after every wave's reads of step kt+1 have returned
+// and its loads of step kt+2 have landed) frees the stage of step kt+1 for
+// the loads of step kt+6. Eight waves of 128x64 read 1.5x the LDS bytes per
+// flop of this layout.
+constexpr int kW4Waves = 4;
+constexpr int kW4J = kTileElems * 2 / 1024 / kW4Waves;  // 1 KiB loads per operand per wave per step
+
+template <class Epi>
+__global__ void __launch_bounds__(64 * kW4Waves, 1) k_gemm_w4(GemmArgs g, Epi epi) {
+  constexpr int NI = 4;
+  __shared__ __attribute__((aligned(16))) char smem[kStages * kStage];
+  int tm, tn;
+  if (!tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn)) return;
+  const int m_valid = g.m_dev ? min(*g.m_dev, g.M) : g.M;
+  const int n_valid = g.n_dev ? min(*g.n_dev, g.N) : g.N;
+  if (tm * kTile >= m_valid || tn * kTile >= n_valid) return;
+  const int K = g.k_dev ? (int)round_up(*g.k_dev, kBK) : g.K;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = w & 1, wn = w >> 1;
+
+  f32x16 acc[4][NI];
+  static_for<4>([&](auto i) {
+    static_for<NI>([&](auto j) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    });
+  });
+
+  const int qrow = 16 * w + (lane >> 2);
+  const int qch = (lane & 3) ^ ((qrow >> 2) & 3);
+  const __amdgpu_buffer_rsrc_t ra = tile_rsrc(g.A + ((int64_t)tm * g.a_kt + g.a_kb0) * kTileElems);
+  const __amdgpu_buffer_rsrc_t rb = tile_rsrc(g.B + ((int64_t)tn * g.b_kt + g.b_kb0) * kTileElems);
+  const uint32_t lofs = (uint32_t)(qrow * 32 + qch * 8) * 2;
+  // load l of step kt (l < kW4J: A part l, else B part l - kW4J) into stage bytes la
+  auto load = [&](int kt, char* la, auto l) {
+    const uint32_t so = (uint32_t)kt * (kTileElems * 2);
+    if constexpr (l.value < kW4J)
+      load_lds16(ra, la + l.value * 1024 * kW4Waves, lofs + l.value * 16 * kW4Waves * 64, so);
+    else
+      load_lds16(rb, la + kTileElems * 2 + (l.value - kW4J) * 1024 * kW4Waves,
+                 lofs + (l.value - kW4J) * 16 * kW4Waves * 64, so);
+  };
+  auto load_step = [&](int kt, int stage) {
+    char* la = smem + stage * kStage + w * 1024;
+    static_for<2 * kW4J>([&](auto l) { load(kt, la, l); });
+  };
+
+  const int fr = lane & 31;
+  const int rd_a = (wm * 128 + fr) * 64;
+  const int rd_b = kTileElems * 2 + (wn * 128 + fr) * 64;
+  int rd_ch[2];
+  static_for<2>([&](auto t) { rd_ch[t] = ((2 * t + (lane >> 5)) ^ ((fr >> 2) & 3)) << 4; });
+  // fragments of one step: q = t*8 + r, r < 4 A block r, else B block r-4
+  bf16x8 fs[2][16];
+  auto fread = [&](auto slot, int kt, auto q) {
+    constexpr int t = q.value / 8, r = q.value % 8;
+    const char* base = smem + (kt % kStages) * kStage;
+    if constexpr (r < 4)
+      fs[slot.value][q.value] = *(const bf16x8*)(base + rd_a + r * 32 * 64 + rd_ch[t]);
+    else
+      fs[slot.value][q.value] = *(const bf16x8*)(base + rd_b + (r - 4) * 32 * 64 + rd_ch[t]);
+  };
+  // MFMA m of a step: sub-step t = m/16, A block i, B block j
+  auto mfma = [&](auto slot, auto m) {
+    constexpr int t = m.value / 16, i = (m.value / 4) % 4, j = m.value % 4;
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fs[slot.value][t * 8 + i],
+                                                        fs[slot.value][t * 8 + 4 + j], acc[i][j],
+                                                        0, 0, 0);
+  };
+  constexpr int kPerStep = 2 * kW4J;   // loads per wave per step
+  constexpr int kMfmas = 32;           // MFMAs per wave per step
+  constexpr int kSpread = kMfmas / kPerStep;
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+
+  const int nk = K / kBK;
+  const int last = nk > 0 ? nk - 1 : 0;
+  static_for<kStages>([&](auto st) { load_step(min((int)st.value, last), st.value); });
+  __builtin_amdgcn_s_waitcnt(wait_vm((kStages - 1) * kPerStep));  // step 0 has landed
+  __builtin_amdgcn_s_barrier();
+  static_for<16>([&](auto q) { fread(I0{}, 0, q); });
+  __builtin_amdgcn_s_waitcnt(wait_vm((kStages - 2) * kPerStep));  // step 1 has landed
+  __builtin_amdgcn_s_barrier();  // and every wave holds step 0: its stage is free
+
+  // step kt from register set `cur`; reads step kt+1 into the other set;
+  // loads step kt+5 into the stage of step kt (free since the last barrier)
+  auto step = [&](int kt, auto cur) {
+    using Nxt = std::integral_constant<int, cur.value ^ 1>;
+    const int nkt = min(kt + kStages, last);
+    char* nl = smem + (kt % kStages) * kStage + w * 1024;
+    static_for<kMfmas>([&](auto m) {
+      mfma(cur, m);
+      if constexpr (m.value < 16) fread(Nxt{}, kt + 1, m);
+      if constexpr (m.value % kSpread == kSpread - 1)
+        load(nkt, nl, std::integral_constant<int, m.value / kSpread>{});
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    // reads of step kt+1 returned; this wave's loads of step kt+2 landed
+    __builtin_amdgcn_s_waitcnt(wait_vm(3 * kPerStep));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    step(kt, I0{});
+    step(kt + 1, I1{});
+  }
+  if (kt < nk) step(kt, I0{});
+  __syncthreads();  // every load has landed before LDS is reused
+
+  Frag f{tm, tn, wm, wn, lane, wn * 128};
+  epi(acc, f, m_valid, n_valid, smem);
+}
+
+// The two gradient products (long K, fp32 store epilogues) run faster on the
+// four-wave loop; the scoring and dz products on the eight-wave one.
+template <class Epi>
+constexpr bool four_waves() {
+  return std::is_same<Epi, EpiGradWeight>::value || std::is_same<Epi, EpiGradHidden>::value;
+}
+
 template <class Epi>
 static void launch_gemm(const GemmArgs& g, const Epi& e, hipStream_t s) {
   int grid = gemm_grid(g.tiles_m, g.tiles_n);
-  hipLaunchKernelGGL((k_gemm_bf16<Epi>), dim3(grid), dim3(64 * kWaves), 0, s, g, e);
+  if constexpr (four_waves<Epi>())
+    hipLaunchKernelGGL((k_gemm_w4<Epi>), dim3(grid), dim3(64 * kW4Waves), 0, s, g, e);
+  else
+    hipLaunchKernelGGL((k_gemm_bf16<Epi>), dim3(grid), dim3(64 * kWaves), 0, s, g, e);
 }
 
 void launch_gemm_lse(const GemmArgs& g, const int32_t* y_p, float* zy, float2* ms, int64_t ldms,
