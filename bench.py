@@ -8,6 +8,7 @@ aggregation, and dL/dh, dL/dW through a recomputed, chunked logits
 gradient. Inputs are seeded synthetic tensors already resident in HBM.
 `--workload sft_bf16` times the supervised stage instead: the same
 contractions with the mean cross-entropy over the response tokens.
+`--workload adamw_lmhead` times the fused AdamW step of the LM head.
 
 Prints one JSON line (see the contract in the repository documentation).
 """
@@ -101,6 +102,82 @@ def cpu_baseline(w, W_bits, h_bits, batch, adv, old, ref, sample_tokens: int):
                       f"({dt:.1f} s)"}
 
 
+def bench_adamw(args):
+    """The fused AdamW step on the LM head's V x H fp32 weights, moments and
+    gradient (plus the bf16 copy): an HBM-bound pass of 30 bytes per parameter."""
+    import torch
+
+    from paper_2507_05687_amd import grpo, workloads
+
+    w = workloads.WORKLOADS["fwdbwd_bf16"]
+    n = w.vocab * w.hidden
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    f32 = dict(dtype=torch.float32, device="cuda")
+    weight = torch.randn(n, generator=gen, **f32) * w.weight_sigma
+    exp_avg = torch.zeros(n, **f32)
+    exp_avg_sq = torch.zeros(n, **f32)
+    grad = torch.randn(n, generator=gen, **f32) * 1e-4
+    wb = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    lr, b1, b2, eps, wd = 1e-6, 0.9, 0.999, 1e-8, 0.01
+    step_no = 0
+
+    def step():
+        nonlocal step_no
+        step_no += 1
+        grpo.adamw_step(weight, exp_avg, exp_avg_sq, grad, step_no, lr, b1, b2, eps, wd,
+                        weight_bf16=wb)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    grpo.profile_reset()
+    grpo.profile_enable(True)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    grpo.profile_enable(False)
+    ms = e0.elapsed_time(e1) / args.steps
+    launches, kms = grpo.profile_read()["adamw"]
+    bytes_per = 4 * 4 + 3 * 4 + 2  # read w, m, v, g; write w, m, v; write the bf16 copy
+    achieved = bytes_per * n / (kms / launches / 1e3) / 1e9
+    res = {
+        "metric": "parameters/sec for the fused AdamW step of the LM head (fp32 state, bf16 copy)",
+        "value": n / (ms / 1e3), "unit": "params/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded torch draws: W N(0,0.02), grad N(0,1e-4))",
+        "config": {"workload": "adamw_lmhead", "params": n, "vocab": w.vocab,
+                   "hidden": w.hidden, "lr": lr, "betas": [b1, b2], "eps": eps,
+                   "weight_decay": wd},
+        "roofline": {"kernel": "adamw", "bound": "hbm", "achieved": achieved,
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
+                     "traffic": None, "bytes_per_param": bytes_per,
+                     "avg_launch_ms": kms / launches},
+    }
+    if args.cpu_sample > 0:
+        import oracle
+
+        k = 1 << 22
+        rng = np.random.default_rng(7)
+        a = [rng.standard_normal(k) * s for s in (0.02, 0.0, 0.0, 1e-4)]
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < 2.0:
+            oracle.adamw(a[0], np.abs(a[1]), np.abs(a[2]), a[3], 1, lr, b1, b2, eps, wd)
+            reps += 1
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": reps * k / dt, "unit": "params/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"{reps} oracle steps on {k} parameters ({dt:.1f} s)"}
+    else:
+        res["cpu_baseline"] = None
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,7 +185,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="fwdbwd_bf16",
                     choices=["fwdbwd_bf16", "fwd_bf16", "ragged_bf16", "double_bf16",
-                             "sft_bf16"])
+                             "sft_bf16", "adamw_lmhead"])
     ap.add_argument("--cpu-sample", type=int, default=128,
                     help="valid tokens timed on the CPU oracle (0 skips the CPU baseline)")
     ap.add_argument("--verbose", action="store_true")
@@ -137,6 +214,8 @@ def main():
                           "launches": 3}), flush=True)
         return
     grpo.load()
+    if args.workload == "adamw_lmhead":
+        return bench_adamw(args)
     w = workloads.WORKLOADS[args.workload]
     log = (lambda *a: print(*a, file=sys.stderr, flush=True)) if args.verbose else (lambda *a: None)
 

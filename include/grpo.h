@@ -214,6 +214,27 @@ grpo_status sft_ce_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight
                            int32_t accumulate_grad_weight, void* workspace,
                            size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * adamw_step -- the optimiser step applied to the LM head after its gradient
+ * (AutoTriton Sec. 4.1 trains the actor with learning rate 1e-6; the
+ * optimiser is not named, AdamW with decoupled weight decay is taken). For
+ * every element, with t = step >= 1:
+ *   m = beta1*m + (1-beta1)*g
+ *   v = beta2*v + (1-beta2)*g^2
+ *   w = w*(1 - lr*weight_decay) - (lr/(1-beta1^t)) * m / (sqrt(v)/sqrt(1-beta2^t) + eps)
+ * in one HBM pass, in fp32, in place.
+ *   weight, exp_avg, exp_avg_sq [n] fp32, device, read and overwritten;
+ *   grad [n] fp32, device (e.g. grad_weight of grpo_loss_fwd_bwd);
+ *   weight_bf16 [n] bf16 output (round to nearest even of the new weight), or
+ *   NULL: the copy the next forward pass reads.
+ * Requires n >= 1, step >= 1, 0 <= beta1, beta2 < 1, eps > 0, lr >= 0,
+ * weight_decay >= 0 (finite); fp32 arrays 16-byte and the bf16 copy 8-byte
+ * aligned. Enqueued on `stream`, no workspace.
+ */
+grpo_status adamw_step(float* weight, float* exp_avg, float* exp_avg_sq, const float* grad,
+                       uint16_t* weight_bf16, int64_t n, float lr, float beta1, float beta2,
+                       float eps, float weight_decay, int64_t step, hipStream_t stream);
+
 /* Bytes of workspace an operation needs for these sizes (0 if the sizes are
  * invalid). For GRPO_OP_LOGPROB_FWD and GRPO_OP_SFT_FWD_BWD pass
  * num_seqs = 1. Host only. */

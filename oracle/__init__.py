@@ -211,3 +211,18 @@ def sft_ce(h, W, tokens, mask=None, want_dh: bool = True, want_dW: bool = True) 
                               _ptr(dh), _ptr(dW))
     out.update(loss=float(loss[0]), dh=dh, dW=dW, nvalid=int(n))
     return out
+
+
+def adamw(w, m, v, g, step: int, lr: float, beta1: float, beta2: float, eps: float,
+          weight_decay: float):
+    """One AdamW step (Adam with decoupled weight decay, Loshchilov & Hutter), written
+    out in float64 the way the algorithm states it: moments, bias corrections,
+    decay of the previous weight, then the normalised step. Returns (w, m, v)."""
+    w, m, v, g = (np.asarray(x, np.float64) for x in (w, m, v, g))
+    m = beta1 * m + (1.0 - beta1) * g
+    v = beta2 * v + (1.0 - beta2) * g * g
+    m_hat = m / (1.0 - beta1 ** step)
+    v_hat = v / (1.0 - beta2 ** step)
+    w = w - lr * weight_decay * w - lr * m_hat / (np.sqrt(v_hat) + eps)
+    return w, m, v
+

@@ -563,6 +563,61 @@ void launch_zero_masked_rows(const int32_t* pidx, int64_t N, int64_t H, void* ou
                      out_bf16);
 }
 
+// ------------------------------------------------------- AdamW step
+// One pass over the parameters: each thread updates 4 consecutive elements
+// (16-byte loads and stores of w, m, v, g; an 8-byte store of the bf16
+// copy), grid-stride over the array; the last n % 4 elements are done one by
+// one by the first threads.
+__device__ __forceinline__ void adamw_one(float& w, float& m, float& v, float g,
+                                          const AdamArgs& a) {
+  m = a.beta1 * m + (1.f - a.beta1) * g;
+  v = a.beta2 * v + (1.f - a.beta2) * g * g;
+  const float denom = sqrtf(v) * a.inv_sqrt_bc2 + a.eps;
+  w = w * a.decay - a.step_size * (m / denom);
+}
+
+__global__ void __launch_bounds__(256) k_adamw(AdamArgs a) {
+  const int64_t n4 = a.n >> 2;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += stride) {
+    f32x4 w = ((const f32x4*)a.w)[i];
+    f32x4 m = ((const f32x4*)a.m)[i];
+    f32x4 v = ((const f32x4*)a.v)[i];
+    const f32x4 g = ((const f32x4*)a.g)[i];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float we = w[e], me = m[e], ve = v[e];
+      adamw_one(we, me, ve, g[e], a);
+      w[e] = we;
+      m[e] = me;
+      v[e] = ve;
+    }
+    ((f32x4*)a.w)[i] = w;
+    ((f32x4*)a.m)[i] = m;
+    ((f32x4*)a.v)[i] = v;
+    if (a.w_bf16) {
+      uint2 b = make_uint2(bf16_pack2(w[0], w[1]), bf16_pack2(w[2], w[3]));
+      ((uint2*)a.w_bf16)[i] = b;
+    }
+  }
+  const int64_t t = n4 * 4 + threadIdx.x;  // the last n % 4 elements
+  if (blockIdx.x == 0 && t < a.n) {
+    float w = a.w[t], m = a.m[t], v = a.v[t];
+    adamw_one(w, m, v, a.g[t], a);
+    a.w[t] = w;
+    a.m[t] = m;
+    a.v[t] = v;
+    if (a.w_bf16) a.w_bf16[t] = bf16_bits(w);
+  }
+}
+
+void launch_adamw(const AdamArgs& a, hipStream_t s) {
+  const int64_t n4 = a.n >> 2;
+  int64_t blocks = ceil_div(n4 > 0 ? n4 : 1, 256);
+  if (blocks > 256 * 32) blocks = 256 * 32;  // 32 resident workgroups per CU, grid-stride beyond
+  hipLaunchKernelGGL(k_adamw, dim3((unsigned)blocks), dim3(256), 0, s, a);
+}
+
 // ------------------------------------------------- plain fp32 path
 // Scoring: one block per packed token; the hidden row sits in LDS and each
 // thread walks a strided subset of the vocabulary with its own online

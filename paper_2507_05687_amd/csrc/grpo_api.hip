@@ -19,12 +19,12 @@ namespace {
 // --------------------------------------------------------- kernel timing
 enum Kind {
   K_PACK, K_ADV, K_GEMM_LSE, K_LSE_FIN, K_TOKEN, K_TRANSPOSE, K_GEMM_DZ, K_GEMM_DH, K_GEMM_DW,
-  K_F32_SCORE, K_F32_DH, K_F32_DW, K_ZERO_ROWS, K_GATHER_DOT, K_TILE, K_NUM_KINDS
+  K_F32_SCORE, K_F32_DH, K_F32_DW, K_ZERO_ROWS, K_GATHER_DOT, K_TILE, K_ADAMW, K_NUM_KINDS
 };
 const char* kKindNames[K_NUM_KINDS] = {
     "pack_valid",  "group_advantages", "gemm_logits_lse", "lse_finalize",   "token_objective",
     "transpose",   "gemm_recompute_dz", "gemm_grad_hidden", "gemm_grad_weight", "f32_score",
-    "f32_grad_hidden", "f32_grad_weight", "zero_masked_rows", "gather_dot", "tile"};
+    "f32_grad_hidden", "f32_grad_weight", "zero_masked_rows", "gather_dot", "tile", "adamw"};
 
 struct Prof {
   std::mutex mu;
@@ -605,6 +605,38 @@ grpo_status sft_ce_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight
   TRY(timed(K_TOKEN, s, [&] { launch_token_objective(ta, s); }));
   return run_backward(L, ws, dt, hidden, weight, mask, N, H, V, grad_hidden, grad_hidden_dt,
                       grad_weight, accumulate_grad_weight, s);
+}
+
+grpo_status adamw_step(float* weight, float* exp_avg, float* exp_avg_sq, const float* grad,
+                       uint16_t* weight_bf16, int64_t n, float lr, float beta1, float beta2,
+                       float eps, float weight_decay, int64_t step, hipStream_t stream) {
+  if (!weight || !exp_avg || !exp_avg_sq || !grad) return GRPO_ERR_NULL;
+  if (n < 1 || step < 1) return GRPO_ERR_SHAPE;
+  if (!(lr >= 0.f) || isinf(lr) || !(beta1 >= 0.f && beta1 < 1.f) ||
+      !(beta2 >= 0.f && beta2 < 1.f) || !(eps > 0.f) || isinf(eps) || !(weight_decay >= 0.f) ||
+      isinf(weight_decay))
+    return GRPO_ERR_PARAM;
+  if (!aligned(weight, 16) || !aligned(exp_avg, 16) || !aligned(exp_avg_sq, 16) ||
+      !aligned(grad, 16) || (weight_bf16 && !aligned(weight_bf16, 8)))
+    return GRPO_ERR_ALIGN;
+  TRY(check_device());
+  AdamArgs a;
+  a.w = weight;
+  a.m = exp_avg;
+  a.v = exp_avg_sq;
+  a.g = grad;
+  a.w_bf16 = weight_bf16;
+  a.n = n;
+  a.beta1 = beta1;
+  a.beta2 = beta2;
+  a.eps = eps;
+  // bias corrections in double on the host, then rounded once to fp32
+  const double bc1 = 1.0 - pow((double)beta1, (double)step);
+  const double bc2 = 1.0 - pow((double)beta2, (double)step);
+  a.decay = (float)(1.0 - (double)lr * (double)weight_decay);
+  a.step_size = (float)((double)lr / bc1);
+  a.inv_sqrt_bc2 = (float)(1.0 / sqrt(bc2));
+  return timed(K_ADAMW, stream, [&] { launch_adamw(a, stream); });
 }
 
 grpo_status grpo_check_error(void* workspace, hipStream_t stream) {

@@ -89,6 +89,21 @@ struct TokenArgs {
 int64_t token_objective_blocks(int64_t N);
 void launch_token_objective(const TokenArgs& a, hipStream_t s);
 
+// ------------------------------------------------------------ AdamW
+struct AdamArgs {
+  float* w;
+  float* m;
+  float* v;
+  const float* g;
+  uint16_t* w_bf16;  // optional
+  int64_t n;
+  float beta1, beta2, eps;
+  float decay;         // 1 - lr * weight_decay
+  float step_size;     // lr / (1 - beta1^t)
+  float inv_sqrt_bc2;  // 1 / sqrt(1 - beta2^t)
+};
+void launch_adamw(const AdamArgs& a, hipStream_t s);
+
 // ------------------------------------------------------------ others
 void launch_group_advantages(const float* rewards, int64_t num_prompts, int group, float eps,
                              int unbiased, float* adv, hipStream_t s);

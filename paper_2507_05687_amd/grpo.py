@@ -37,6 +37,8 @@ SIGNATURES = {
                                  _i32, _vp, _i32, _vp, _sz, _vp]),
     "sft_ce_fwd_bwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp, _i32,
                               _vp, _i32, _vp, _sz, _vp]),
+    "adamw_step": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _f32, _f32, _f32, _f32, _f32, _i64,
+                          _vp]),
     "grpo_workspace_bytes": (_sz, [_i32, _i32, _i64, _i64, _i64, _i64]),
     "grpo_check_error": (_i32, [_vp, _vp]),
     "grpo_status_string": (ctypes.c_char_p, [_i32]),
@@ -280,6 +282,26 @@ def sft_ce_fwd_bwd(hidden, weight, tokens, mask=None, grad_hidden: bool = True,
     if check:
         check_error(ws)
     return out
+
+
+def adamw_step(weight, exp_avg, exp_avg_sq, grad, step: int, lr: float = 1e-6,
+               beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
+               weight_decay: float = 0.01, weight_bf16: torch.Tensor | None = None):
+    """In-place fused AdamW step on fp32 weight/moments; optionally writes a bf16 copy."""
+    for t, name in ((weight, "weight"), (exp_avg, "exp_avg"), (exp_avg_sq, "exp_avg_sq"),
+                    (grad, "grad")):
+        _need(t, name, torch.float32)
+    n = weight.numel()
+    if any(t.numel() != n for t in (exp_avg, exp_avg_sq, grad)):
+        raise ValueError("weight, exp_avg, exp_avg_sq and grad must have the same size")
+    if weight_bf16 is not None:
+        _need(weight_bf16, "weight_bf16", torch.bfloat16)
+        if weight_bf16.numel() != n:
+            raise ValueError("weight_bf16 must have the size of weight")
+    st = load().adamw_step(_ptr(weight), _ptr(exp_avg), _ptr(exp_avg_sq), _ptr(grad),
+                           _ptr(weight_bf16), n, lr, beta1, beta2, eps, weight_decay, int(step),
+                           _stream())
+    _check(st, "adamw_step")
 
 
 def check_error(ws: torch.Tensor):

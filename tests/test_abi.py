@@ -31,7 +31,7 @@ def _declared_functions():
 def test_header_declares_the_boundary():
     names = _declared_functions()
     for required in ("group_advantages", "grpo_logprob_fwd", "grpo_loss_fwd_bwd",
-                     "sft_ce_fwd_bwd", "grpo_pack_valid", "grpo_workspace_bytes",
+                     "sft_ce_fwd_bwd", "adamw_step", "grpo_pack_valid", "grpo_workspace_bytes",
                      "grpo_check_error", "grpo_status_string"):
         assert required in names
 
@@ -143,6 +143,28 @@ def test_sft_argument_errors(lib):
     assert _sft(lib, logp=ctypes.c_void_p(0x1002)) == 5
     assert _sft(lib) == 6                           # no workspace
     assert _sft(lib, ws=P, ws_bytes=16) == 6        # too small
+
+
+def test_adamw_argument_errors(lib):
+    f = lib.adamw_step
+    a = [P, P, P, P, NULL, 10, 1e-3, 0.9, 0.999, 1e-8, 0.01, 1, NULL]
+
+    def call(i, x):
+        b = list(a)
+        b[i] = x
+        return f(*b)
+
+    assert call(0, NULL) == 1
+    assert call(3, NULL) == 1
+    assert call(5, 0) == 2                # n
+    assert call(11, 0) == 2               # step
+    assert call(6, -1.0) == 4             # lr
+    assert call(7, 1.0) == 4              # beta1
+    assert call(8, -0.1) == 4             # beta2
+    assert call(9, 0.0) == 4              # eps
+    assert call(10, float("inf")) == 4    # weight decay
+    assert call(1, ctypes.c_void_p(0x1004)) == 5
+    assert call(4, ctypes.c_void_p(0x1002)) == 5
 
 
 def test_profile_interface_without_launches(lib):

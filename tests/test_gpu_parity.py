@@ -349,3 +349,40 @@ def test_sft_closed_forms():
     assert out["grad_hidden"].abs().max().item() == 0.0
     assert out["grad_weight"].abs().max().item() == 0.0
 
+
+# ------------------------------------------------------------ AdamW step
+@pytest.mark.parametrize("n,lr,wd", [(1_000_003, 1e-6, 0.01), (4096, 1e-3, 0.1), (3, 1e-2, 0.0)])
+def test_adamw_parity(n, lr, wd):
+    """Three fused steps against the float64 oracle; the bf16 copy is the
+    round-to-nearest-even of the kernel's own fp32 weight, bit for bit."""
+    g = np.random.default_rng(n)
+    w = (g.standard_normal(n) * 0.02).astype(np.float32)
+    m = np.zeros(n, np.float32)
+    v = np.zeros(n, np.float32)
+    wt, mt, vt = dev(w), dev(m), dev(v)
+    wb = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    b1, b2, eps = 0.9, 0.999, 1e-8
+    # the boundary takes fp32 hyper-parameters: the oracle gets the same values
+    f = lambda x: float(np.float32(x))  # noqa: E731
+    for step in (1, 2, 3):
+        gr = (g.standard_normal(n) * 10.0 ** g.uniform(-4, 0)).astype(np.float32)
+        w_in, m_in, v_in = host64(wt), host64(mt), host64(vt)
+        grpo.adamw_step(wt, mt, vt, dev(gr), step, lr, b1, b2, eps, wd,
+                        weight_bf16=wb if step != 2 else None)
+        torch.cuda.synchronize()
+        ow, om, ov = oracle.adamw(w_in, m_in, v_in, gr, step, f(lr), f(b1), f(b2), f(eps), f(wd))
+        kw, km, kv = host64(wt), host64(mt), host64(vt)
+        # the first moment is a sum that can cancel: measure against its terms
+        scale_m = f(b1) * np.abs(m_in) + (1 - f(b1)) * np.abs(gr.astype(np.float64))
+        assert np.all(np.abs(km - om) <= 2e-6 * scale_m + 1e-37)
+        np.testing.assert_allclose(kv, ov, rtol=2e-6, atol=1e-37)
+        # the new fp32 weight is within about one fp32 spacing of the exact one
+        # plus 1e-5 of the step (with lr = 1e-6 the step itself is close to
+        # that spacing, so a relative check of the weight is the right scale)
+        ulp = np.spacing(np.abs(ow).astype(np.float32)).astype(np.float64)
+        assert np.all(np.abs(kw - ow) <= 1.5 * ulp + 1e-5 * np.abs(ow - w_in))
+        if step != 2:
+            want = workloads.bf16_bits(wt.cpu().numpy())
+            got = wb.view(torch.int16).cpu().numpy().view(np.uint16)
+            assert np.array_equal(got, want)
+

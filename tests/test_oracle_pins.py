@@ -440,3 +440,36 @@ def test_sft_finite_differences(oracle_lib):
         fd = (oracle_lib.sft_ce(h, Wp, y, mask)["loss"] -
               oracle_lib.sft_ce(h, Wn, y, mask)["loss"]) / (2 * eps)
         assert r["dW"][v, k] == pytest.approx(fd, rel=1e-6, abs=1e-9)
+
+
+# ------------------------------------------------ AdamW step (after the gradient)
+def test_adamw_matches_torch(oracle_lib):
+    """Three steps against torch.optim.AdamW in float64 (a library routine)."""
+    g0 = np.random.default_rng(41)
+    w0 = g0.standard_normal(1000)
+    grads = [g0.standard_normal(1000) * s for s in (1.0, 1e-3, 30.0)]
+    p = torch.nn.Parameter(torch.from_numpy(w0.copy()))
+    opt = torch.optim.AdamW([p], lr=1e-3, betas=(0.9, 0.95), eps=1e-8, weight_decay=0.1)
+    w, m, v = w0.copy(), np.zeros(1000), np.zeros(1000)
+    for t, gr in enumerate(grads, start=1):
+        p.grad = torch.from_numpy(gr.copy())
+        opt.step()
+        w, m, v = oracle_lib.adamw(w, m, v, gr, t, 1e-3, 0.9, 0.95, 1e-8, 0.1)
+        st = opt.state[p]
+        np.testing.assert_allclose(w, p.detach().numpy(), rtol=1e-14, atol=1e-15)
+        np.testing.assert_allclose(m, st["exp_avg"].numpy(), rtol=1e-14, atol=1e-300)
+        np.testing.assert_allclose(v, st["exp_avg_sq"].numpy(), rtol=1e-14, atol=1e-300)
+
+
+def test_adamw_closed_forms(oracle_lib):
+    """Zero gradient from zero moments: pure decay w(1 - lr*wd). First step: the
+    bias-corrected moments are g and g^2, so the step is lr*g/(|g| + eps)."""
+    w = np.array([1.0, -2.0, 0.5])
+    z = np.zeros(3)
+    w1, m1, v1 = oracle_lib.adamw(w, z, z, z, 1, 1e-2, 0.9, 0.999, 1e-8, 0.5)
+    np.testing.assert_array_equal(w1, w * (1 - 1e-2 * 0.5))
+    assert np.all(m1 == 0) and np.all(v1 == 0)
+    g = np.array([3.0, -1e-3, 0.25])
+    w1, _, _ = oracle_lib.adamw(w, z, z, g, 1, 1e-2, 0.9, 0.999, 1e-8, 0.0)
+    np.testing.assert_allclose(w1, w - 1e-2 * g / (np.abs(g) + 1e-8), rtol=1e-14)
+
