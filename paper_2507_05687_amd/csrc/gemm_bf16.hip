@@ -23,8 +23,14 @@
 
 namespace grpo {
 
-constexpr int kGM = 4;  // tile-rows per XCD band
-constexpr int kGN = 8;  // tile-columns per step of the walk
+#ifndef GRPO_GEMM_GM
+#define GRPO_GEMM_GM 4
+#endif
+#ifndef GRPO_GEMM_GN
+#define GRPO_GEMM_GN 8
+#endif
+constexpr int kGM = GRPO_GEMM_GM;  // tile-rows per XCD band
+constexpr int kGN = GRPO_GEMM_GN;  // tile-columns per step of the walk
 // s_waitcnt immediate: vmcnt <= n (6 bits, split over [3:0] and [15:14]),
 // expcnt left at its maximum (7 in [6:4]), lgkmcnt 0 ([11:8]).
 constexpr int wait_vm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0070; }

@@ -86,8 +86,14 @@ grpo_status check_device() {
 
 // --------------------------------------------------------- workspace
 constexpr size_t kAlign = 256;
-constexpr int64_t kDzBudget = 8ll << 30;  // bytes for the two bf16 dz chunk buffers
-constexpr int64_t kVcMax = 16384;
+#ifndef GRPO_DZ_BUDGET_GIB
+#define GRPO_DZ_BUDGET_GIB 8
+#endif
+#ifndef GRPO_VC_MAX
+#define GRPO_VC_MAX 16384
+#endif
+constexpr int64_t kDzBudget = (int64_t)GRPO_DZ_BUDGET_GIB << 30;  // bytes for the two bf16 dz buffers
+constexpr int64_t kVcMax = GRPO_VC_MAX;
 
 struct Layout {
   int64_t Npad = 0, Vpad = 0, tiles_v = 0, Vc = 0, nchunks = 0;
