@@ -83,61 +83,57 @@ struct Frag {
 struct EpiLse {
   const int32_t* y_p;  // sampled id of each packed token
   float* zy;           // z at the sampled id, per packed token
-  float2* ms;          // [tiles_m][ldms] partial (max, sum-exp)
+  float2* ms;          // [2 * tiles_m][ldms] partial (max, sum-exp) per 128-row half tile
   int64_t ldms;
   int64_t V;
 
+  // Reduces this lane's 64 rows of column ni (rows with offset >= vlim are
+  // past the vocabulary) to (max, sum exp(z - max)) and picks out z at y.
+  template <bool FULL, int NI, class Acc>
+  __device__ __forceinline__ void column(const Acc& acc, int ni, float& m_out, float& s_out,
+                                         int vlim, int y, float* zy_t) const {
+    float m = -INFINITY;
+    static_for<4>([&](auto mi) {
+      static_for<16>([&](auto r) {
+        constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
+        if (FULL || o < vlim) m = fmaxf(m, acc[mi][ni][r.value]);
+      });
+    });
+    float s = 0.f;
+    const float m2l = m * kLog2e;
+    static_for<4>([&](auto mi) {
+      static_for<16>([&](auto r) {
+        constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
+        if (FULL || o < vlim) s += __builtin_amdgcn_exp2f(fmaf(acc[mi][ni][r.value], kLog2e, -m2l));
+        if (o == y) *zy_t = acc[mi][ni][r.value];
+      });
+    });
+    m_out = m;
+    s_out = s;
+  }
+
   template <int NI>
   __device__ __forceinline__ void operator()(f32x16 (&acc)[4][NI], const Frag& f, int m_valid,
-                                             int n_valid,
-                             char* smem) const {
-    float pm[NI], ps[NI];
+                                             int n_valid, char*) const {
     const int vbase = f.tm * kTile + f.wm * 128 + (f.lane >> 5) * 4;
     const int vlim = (int)(V - vbase);  // rows r of this lane are valid iff row offset < vlim
+    const bool full = (int64_t)f.tm * kTile + f.wm * 128 + 128 <= V;  // wave-uniform
     static_for<NI>([&](auto ni) {
       const int64_t t = (int64_t)f.tn * kTile + f.col(ni);
       const int y = t < n_valid ? y_p[t] - vbase : -1;  // y as a row offset of this lane
-      float m = -INFINITY;
-      static_for<4>([&](auto mi) {
-        static_for<16>([&](auto r) {
-          constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
-          if (o < vlim) m = fmaxf(m, acc[mi][ni][r.value]);
-        });
-      });
-      float s = 0.f;
-      const float m2l = m * kLog2e;
-      static_for<4>([&](auto mi) {
-        static_for<16>([&](auto r) {
-          constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
-          if (o < vlim) s += __builtin_amdgcn_exp2f(fmaf(acc[mi][ni][r.value], kLog2e, -m2l));
-          if (o == y) zy[t] = acc[mi][ni][r.value];
-        });
-      });
-      // merge with the lane holding the other 64 rows of this column
+      float m, s;
+      if (full)
+        column<true, NI>(acc, ni, m, s, vlim, y, zy + t);
+      else
+        column<false, NI>(acc, ni, m, s, vlim, y, zy + t);
+      // merge with the lane holding the other 64 rows of this column; each
+      // 128-row half tile (wave row wm) writes its own partial
       float m2 = __shfl_xor(m, 32, 64), s2 = __shfl_xor(s, 32, 64);
       float mm = fmaxf(m, m2);
       float sm = (s == 0.f ? 0.f : s * __expf(m - mm)) + (s2 == 0.f ? 0.f : s2 * __expf(m2 - mm));
-      pm[ni] = mm;
-      ps[ni] = sm;
+      if (f.lane < 32 && t < n_valid)
+        ms[(int64_t)(2 * f.tm + f.wm) * ldms + t] = make_float2(mm, sm);
     });
-    // merge the two waves that share these columns (wm = 0 and 1)
-    float2* xch = (float2*)smem;  // [256 tile columns]
-    if (f.wm == 1 && f.lane < 32) {
-      static_for<NI>([&](auto ni) {
-        xch[f.cbase + ni * 32 + f.lane] = make_float2(pm[ni], ps[ni]);
-      });
-    }
-    __syncthreads();
-    if (f.wm == 0 && f.lane < 32) {
-      static_for<NI>([&](auto ni) {
-        float2 o = xch[f.cbase + ni * 32 + f.lane];
-        float mm = fmaxf(pm[ni], o.x);
-        float sm = (ps[ni] == 0.f ? 0.f : ps[ni] * __expf(pm[ni] - mm)) +
-                   (o.y == 0.f ? 0.f : o.y * __expf(o.x - mm));
-        int64_t t = (int64_t)f.tn * kTile + f.col(ni);
-        if (t < n_valid) ms[(int64_t)f.tm * ldms + t] = make_float2(mm, sm);
-      });
-    }
   }
 };
 
@@ -158,6 +154,18 @@ struct EpiDz {
     const int hi = (f.lane >> 5) * 4;
     const int64_t vbase = v0 + (int64_t)f.tm * kTile + f.wm * 128 + hi;
     const int vlim = (int)((V - vbase) < (1 << 20) ? (V - vbase) : (1 << 20));
+    // every row of this wave is inside the vocabulary: no per-element bound
+    const bool full = v0 + (int64_t)f.tm * kTile + f.wm * 128 + 128 <= V;  // wave-uniform
+    if (full)
+      body(acc, f, n_valid, vbase, vlim, std::true_type{});
+    else
+      body(acc, f, n_valid, vbase, vlim, std::false_type{});
+  }
+
+  template <int NI, class Full>
+  __device__ __forceinline__ void body(f32x16 (&acc)[4][NI], const Frag& f, int n_valid,
+                                       int64_t vbase, int vlim, Full) const {
+    const int hi = (f.lane >> 5) * 4;
     static_for<NI>([&](auto ni) {
       const int64_t t = (int64_t)f.tn * kTile + f.col(ni);
       const bool tv = t < n_valid;
@@ -179,7 +187,7 @@ struct EpiDz {
             constexpr int o = mi * 32 + q * 8 + e;
             const float p = __builtin_amdgcn_exp2f(fmaf(acc[mi][ni][r], kLog2e, -l2));
             const float dv = g * ((o == y ? 1.f : 0.f) - p);
-            d[e] = o < vlim ? dv : 0.f;
+            d[e] = (Full::value || o < vlim) ? dv : 0.f;
           });
           const uint32_t w0 = bf16_pack2(d[0], d[1]), w1 = bf16_pack2(d[2], d[3]);
           if (pzt) {
@@ -217,64 +225,66 @@ struct EpiStore {
     const bool full = (int64_t)f.tm * kTile + kTile <= mlim &&
                       (int64_t)f.tn * kTile + kTile <= n_limit;
     float* pacc = acc_buf ? acc_buf + m0 * ld_acc + n0 : nullptr;
-    // Batches of 32 values (8 rows x 4 columns of this lane): each batch is
-    // loaded, combined and stored before the next starts, so the loads of a
-    // batch are in flight together and its registers die right after.
-    // (mi, r) -> row offset mi*32 + (r/4)*8 + r%4; ni -> column offset ni*32.
-    static_for<8>([&](auto bq) {
-      constexpr int mi = bq / 2, r0 = (bq % 2) * 8;
-      float v[8][NI];
-      static_for<8>([&](auto rr) {
+    // Batches of RB rows x NI columns of this lane (16 or 32 values): each
+    // batch is loaded, combined and stored before the next starts, so the
+    // loads of a batch are in flight together and its registers die right
+    // after. (mi, r) -> row offset mi*32 + (r/4)*8 + r%4; ni -> column ni*32.
+    constexpr int RB = NI >= 4 ? 4 : 8;
+    constexpr int kPerMi = 16 / RB;
+    static_for<4 * kPerMi>([&](auto bq) {
+      constexpr int mi = bq / kPerMi, r0 = (bq % kPerMi) * RB;
+      float v[RB][NI];
+      static_for<RB>([&](auto rr) {
         static_for<NI>([&](auto ni) { v[rr][ni] = acc[mi][ni][r0 + rr]; });
       });
       if (read_acc) {  // the accumulation buffer holds every row/column of the tile
-        float prev[8][NI];
-        static_for<8>([&](auto rr) {
+        float prev[RB][NI];
+        static_for<RB>([&](auto rr) {
           constexpr int r = r0 + rr;
           constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
           const float* pr = pacc + o * ld_acc;
           static_for<NI>([&](auto ni) { prev[rr][ni] = pr[ni * 32]; });
         });
-        static_for<8>([&](auto rr) {
+        static_for<RB>([&](auto rr) {
           static_for<NI>([&](auto ni) { v[rr][ni] += prev[rr][ni]; });
         });
       }
       if (out == nullptr) {
-        static_for<8>([&](auto rr) {
+        static_for<RB>([&](auto rr) {
           constexpr int r = r0 + rr;
           constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
           float* pr = pacc + o * ld_acc;
           static_for<NI>([&](auto ni) { pr[ni * 32] = v[rr][ni]; });
         });
       } else if (full) {
-        int64_t orow[8];
-        static_for<8>([&](auto rr) {
+        int64_t orow[RB];
+        static_for<RB>([&](auto rr) {
           constexpr int r = r0 + rr;
           constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
           orow[rr] = (out_rows ? (int64_t)out_rows[m0 + o] : m0 + o) * ld_out + n0;
         });
         if (out_bf16) {
           uint16_t* ob = (uint16_t*)out;
-          static_for<8>([&](auto rr) {
+          static_for<RB>([&](auto rr) {
             static_for<NI>([&](auto ni) { ob[orow[rr] + ni * 32] = bf16_bits(v[rr][ni]); });
           });
         } else {
           float* of = (float*)out;
           if (add_out) {
-            float prev[8][NI];
-            static_for<8>([&](auto rr) {
+            float prev[RB][NI];
+            static_for<RB>([&](auto rr) {
               static_for<NI>([&](auto ni) { prev[rr][ni] = of[orow[rr] + ni * 32]; });
             });
-            static_for<8>([&](auto rr) {
+            static_for<RB>([&](auto rr) {
               static_for<NI>([&](auto ni) { v[rr][ni] += prev[rr][ni]; });
             });
           }
-          static_for<8>([&](auto rr) {
+          static_for<RB>([&](auto rr) {
             static_for<NI>([&](auto ni) { of[orow[rr] + ni * 32] = v[rr][ni]; });
           });
         }
       } else {  // edge tile: per-element bounds
-        static_for<8>([&](auto rr) {
+        static_for<RB>([&](auto rr) {
           constexpr int r = r0 + rr;
           constexpr int o = mi * 32 + (r >> 2) * 8 + (r & 3);
           const int64_t m = m0 + o;

@@ -151,7 +151,7 @@ Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_
   L.g = take(c, 4 * L.Npad);
   L.lpart = take(c, 4 * token_objective_blocks(N));
   if (dt == GRPO_BF16) {
-    L.ms = take(c, 8 * L.tiles_v * L.Npad);
+    L.ms = take(c, 8 * 2 * L.tiles_v * L.Npad);  // one partial per 128-row half tile
     // tiled copies of W and of the valid hidden rows (K = H contiguous blocks)
     L.Hk = round_up(H, kBK);
     L.sK = tile_stride(H);
@@ -277,7 +277,7 @@ grpo_status run_scoring(const Layout& L, void* ws, grpo_dtype dt, const void* hi
                          nullptr, &hdr->num_valid, L.Hk, nullptr);
   TRY(timed(K_GEMM_LSE, s, [&] { launch_gemm_lse(g, y_p, zy, ms, L.Npad, V, s); }));
   return timed(K_LSE_FIN, s, [&] {
-    launch_lse_finalize(ms, L.Npad, (int)L.tiles_v, zy, hdr, lse_p, logp_p, N, s);
+    launch_lse_finalize(ms, L.Npad, (int)(2 * L.tiles_v), zy, hdr, lse_p, logp_p, N, s);
   });
 }
 
