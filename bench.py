@@ -48,18 +48,17 @@ def _gemm_flops(kind: str, w, n_valid: int, vc_sizes: list[int]) -> float:
 
 
 def _traffic_from_profiles(kernel: str, workload: str):
-    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
-    was taken on the current kernel source and the same workload; else None."""
-    path = os.path.join(ROOT, "profiles", "traffic.json")
+    """HBM bytes per launch from the committed rocprofv3 counter summary of this
+    workload, if it was taken on the current source of its kernels; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     try:
-        rec = json.load(open(path))
         import hashlib
 
-        src = open(os.path.join(ROOT, "paper_2507_05687_amd", "csrc", "gemm_bf16.hip"),
-                   "rb").read()
-        if rec.get("gemm_source_sha256") != hashlib.sha256(src).hexdigest():
+        rec = json.load(open(path))
+        src = open(os.path.join(ROOT, *rec["source"].split("/")), "rb").read()
+        if rec.get("source_sha256") != hashlib.sha256(src).hexdigest():
             return None
         if rec.get("workload") != workload:
             return None
@@ -155,7 +154,8 @@ def bench_adamw(args):
                    "weight_decay": wd},
         "roofline": {"kernel": "adamw", "bound": "hbm", "achieved": achieved,
                      "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
-                     "traffic": None, "bytes_per_param": bytes_per,
+                     "traffic": _traffic_from_profiles("adamw", "adamw_lmhead"),
+                     "bytes_per_param": bytes_per,
                      "avg_launch_ms": kms / launches},
     }
     if args.cpu_sample > 0:
@@ -166,7 +166,7 @@ def bench_adamw(args):
         a = [rng.standard_normal(k) * s for s in (0.02, 0.0, 0.0, 1e-4)]
         t0 = time.perf_counter()
         reps = 0
-        while time.perf_counter() - t0 < 2.0:
+        while time.perf_counter() - t0 < 10.0:
             oracle.adamw(a[0], np.abs(a[1]), np.abs(a[2]), a[3], 1, lr, b1, b2, eps, wd)
             reps += 1
         dt = time.perf_counter() - t0

@@ -1,15 +1,17 @@
 """rocprofv3 driver for the benchmark: kernel timings and HBM byte counters.
 
-    python -m paper_2507_05687_amd.profiling trace    [--raw DIR] [--out DIR]
-    python -m paper_2507_05687_amd.profiling counters [--raw DIR] [--out DIR]
+    python -m paper_2507_05687_amd.profiling trace    [--workload W] [--raw DIR] [--out DIR]
+    python -m paper_2507_05687_amd.profiling counters [--workload W] [--raw DIR] [--out DIR]
 
-`trace` runs ``rocprofv3 --kernel-trace --stats`` over ``bench.py`` and writes
-a per-kernel duration table. `counters` takes FETCH_SIZE and WRITE_SIZE (one
-counter pass each) over one benchmark step and over a plain 1 GiB device
-copy; the copy's readings calibrate the counters (bytes the copy must move /
-what the counter reports), and the GEMM kernels' readings, scaled by that
-factor, give their HBM bytes per launch. Raw rocprofv3 output stays in
---raw; the text summaries and traffic.json go to --out.
+`trace` runs ``rocprofv3 --kernel-trace --stats`` over ``bench.py --workload W``
+and writes a per-kernel duration table. `counters` takes FETCH_SIZE and
+WRITE_SIZE (one counter pass each) over one benchmark step and over a plain
+1 GiB device copy; the copy's readings calibrate the counters (bytes the copy
+must move / what the counter reports), and the workload's main kernels'
+readings, scaled by that factor, give their HBM bytes per launch. Raw
+rocprofv3 output stays in --raw; the text summaries and traffic_W.json (with
+the SHA-256 of the kernels' source, so that a stale record is never used) go
+to --out.
 """
 from __future__ import annotations
 
@@ -24,11 +26,27 @@ import subprocess
 import sys
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-GEMM_SRC = os.path.join(ROOT, "paper_2507_05687_amd", "csrc", "gemm_bf16.hip")
-WORKLOAD = "fwdbwd_bf16"
+CSRC = os.path.join("paper_2507_05687_amd", "csrc")
 # library kernel kind -> substring of the kernel symbol
-KINDS = {"gemm_logits_lse": "EpiLse", "gemm_recompute_dz": "EpiDz",
-         "gemm_grad_hidden": "EpiGradHidden", "gemm_grad_weight": "EpiGradWeight"}
+GEMM_KINDS = {"gemm_logits_lse": "EpiLse", "gemm_recompute_dz": "EpiDz",
+              "gemm_grad_hidden": "EpiGradHidden", "gemm_grad_weight": "EpiGradWeight"}
+# workload -> bench.py arguments, kernels of interest, their source file, description
+PROFILED = {
+    "fwdbwd_bf16": dict(
+        args=[], kinds=GEMM_KINDS, source=os.path.join(CSRC, "gemm_bf16.hip"),
+        desc="N=131072, H=4096, V=155136, bf16",
+        note="the warm-up step and the setup scoring call are included: 5 scoring launches"),
+    "sft_bf16": dict(
+        args=["--workload", "sft_bf16"], kinds=GEMM_KINDS,
+        source=os.path.join(CSRC, "gemm_bf16.hip"),
+        desc="one 16384-token sequence, 14336 supervised tokens, H=4096, V=155136, bf16",
+        note="the warm-up step is included"),
+    "adamw_lmhead": dict(
+        args=["--workload", "adamw_lmhead"], kinds={"adamw": "k_adamw"},
+        source=os.path.join(CSRC, "aux_kernels.hip"),
+        desc="155136 x 4096 fp32 parameters, moments and gradient, bf16 copy",
+        note="the warm-up step is included"),
+}
 COPY_BYTES = 1 << 30
 
 
@@ -56,43 +74,43 @@ def _counter(d: str, name: str) -> dict:
     return out
 
 
-def _source_sha() -> str:
-    return hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()
+def source_sha(rel: str) -> str:
+    return hashlib.sha256(open(os.path.join(ROOT, rel), "rb").read()).hexdigest()
 
 
-def trace(raw: str, out: str, run: bool = True):
-    d = os.path.join(raw, "trace")
-    cmd = ["rocprofv3", "--kernel-trace", "--stats", "-d", d, "-o", "bench", "--", sys.executable,
-           "bench.py", "--steps", "3", "--warmup", "1", "--cpu-sample", "0"]
+def trace(wl: str, raw: str, out: str, run: bool = True):
+    cfg = PROFILED[wl]
+    d = os.path.join(raw, f"trace_{wl}")
+    bench = ["bench.py", *cfg["args"], "--steps", "3", "--warmup", "1", "--cpu-sample", "0"]
     if run:
-        _run(cmd, os.path.join(raw, "trace.log"), 600)
+        _run(["rocprofv3", "--kernel-trace", "--stats", "-d", d, "-o", "bench", "--",
+              sys.executable, *bench], os.path.join(raw, f"trace_{wl}.log"), 600)
     rows = _db(d).execute("select name, total_calls, total_duration, average, percentage "
                           "from top_kernels").fetchall()
-    lines = [f"# rocprofv3 kernel trace of bench.py, workload {WORKLOAD} (N=131072, H=4096, "
-             "V=155136, bf16)",
+    lines = [f"# rocprofv3 kernel trace of bench.py, workload {wl} ({cfg['desc']})",
              "# command: " + " ".join(["rocprofv3", "--kernel-trace", "--stats", "-d", "<raw>",
-                                      "-o", "bench", "--", "python", "bench.py", "--steps", "3",
-                                      "--warmup", "1", "--cpu-sample", "0"]),
-             "# (the warm-up step and the setup scoring call are included: 5 scoring launches)",
-             f"# gemm source sha256: {_source_sha()}",
+                                      "-o", "bench", "--", "python", *bench]),
+             f"# ({cfg['note']})",
+             f"# source sha256 ({os.path.basename(cfg['source'])}): {source_sha(cfg['source'])}",
              f"{'calls':>6} {'total_ms':>10} {'avg_ms':>9} {'pct':>6}  kernel"]
     for name, calls, tot, avg, pct in rows:
         if pct < 0.01:
             continue
         # top_kernels reports microseconds
         lines.append(f"{calls:6d} {tot / 1e3:10.3f} {avg / 1e3:9.4f} {pct:6.2f}  {name[:110]}")
-    path = os.path.join(out, f"kernels_{WORKLOAD}.txt")
+    path = os.path.join(out, f"kernels_{wl}.txt")
     open(path, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
 
-def counters(raw: str, out: str):
+def counters(wl: str, raw: str, out: str):
+    cfg = PROFILED[wl]
+    bench = ["bench.py", *cfg["args"], "--steps", "1", "--warmup", "0", "--cpu-sample", "0"]
     res = {}
     for name in ("FETCH_SIZE", "WRITE_SIZE"):
-        d = os.path.join(raw, f"pmc_{name.lower()}")
-        _run(["rocprofv3", "--pmc", name, "-d", d, "-o", "bench", "--", sys.executable, "bench.py",
-              "--steps", "1", "--warmup", "0", "--cpu-sample", "0"],
-             os.path.join(raw, f"pmc_{name.lower()}.log"), 600)
+        d = os.path.join(raw, f"pmc_{wl}_{name.lower()}")
+        _run(["rocprofv3", "--pmc", name, "-d", d, "-o", "bench", "--", sys.executable, *bench],
+             os.path.join(raw, f"pmc_{wl}_{name.lower()}.log"), 600)
         dc = os.path.join(raw, f"pmc_copy_{name.lower()}")
         _run(["rocprofv3", "--pmc", name, "-d", dc, "-o", "copy", "--", sys.executable, "bench.py",
               "--copy-calibration"], os.path.join(raw, f"pmc_copy_{name.lower()}.log"), 300)
@@ -102,18 +120,18 @@ def counters(raw: str, out: str):
     kib = COPY_BYTES / 1024
     f_scale = kib / (sum(copy_f) / len(copy_f))
     w_scale = kib / (sum(copy_w) / len(copy_w))
-    rec = {"workload": WORKLOAD, "gemm_source_sha256": _source_sha(), "fetch_scale": f_scale,
-           "write_scale": w_scale,
-           "command": "python -m paper_2507_05687_amd.profiling counters", "kernels": {}}
-    lines = [f"# HBM traffic per launch, workload {WORKLOAD}, from rocprofv3 --pmc FETCH_SIZE and "
-             "--pmc WRITE_SIZE (one pass each) over `python bench.py --steps 1 --warmup 0 "
-             "--cpu-sample 0`",
+    sha = source_sha(cfg["source"])
+    cmd = f"python -m paper_2507_05687_amd.profiling counters --workload {wl}"
+    rec = {"workload": wl, "source": cfg["source"].replace(os.sep, "/"), "source_sha256": sha,
+           "fetch_scale": f_scale, "write_scale": w_scale, "command": cmd, "kernels": {}}
+    lines = [f"# HBM traffic per launch, workload {wl}, from rocprofv3 --pmc FETCH_SIZE and "
+             f"--pmc WRITE_SIZE (one pass each) over `python {' '.join(bench)}`",
              "# calibration: `python bench.py --copy-calibration` (1 GiB device copy): "
              f"FETCH_SIZE x{f_scale:.4f}, WRITE_SIZE x{w_scale:.4f} to reach the bytes it moves",
-             "# command: python -m paper_2507_05687_amd.profiling counters",
-             f"# gemm source sha256: {_source_sha()}",
+             f"# command: {cmd}",
+             f"# source sha256 ({os.path.basename(cfg['source'])}): {sha}",
              f"{'kind':22s} {'launches':>8} {'fetch_GB':>10} {'write_GB':>10} {'total_GB':>10}"]
-    for kind, sym in KINDS.items():
+    for kind, sym in cfg["kinds"].items():
         f = [v for k, v in res["FETCH_SIZE"][0].items() if sym in k]
         w = [v for k, v in res["WRITE_SIZE"][0].items() if sym in k]
         if not f or not w:
@@ -125,14 +143,15 @@ def counters(raw: str, out: str):
                                 "hbm_bytes_per_launch": fb + wb}
         lines.append(f"{kind:22s} {len(f[0]):8d} {fb / 1e9:10.3f} {wb / 1e9:10.3f} "
                      f"{(fb + wb) / 1e9:10.3f}")
-    json.dump(rec, open(os.path.join(out, "traffic.json"), "w"), indent=1)
-    open(os.path.join(out, f"traffic_{WORKLOAD}.txt"), "w").write("\n".join(lines) + "\n")
+    json.dump(rec, open(os.path.join(out, f"traffic_{wl}.json"), "w"), indent=1)
+    open(os.path.join(out, f"traffic_{wl}.txt"), "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("what", choices=["trace", "counters", "all"])
+    ap.add_argument("--workload", default="fwdbwd_bf16", choices=sorted(PROFILED))
     ap.add_argument("--raw", default=os.path.join(ROOT, "gpurun_out", "prof"))
     ap.add_argument("--out", default=os.path.join(ROOT, "profiles"))
     ap.add_argument("--summarize-only", action="store_true",
@@ -142,9 +161,9 @@ def main():
     os.makedirs(a.out, exist_ok=True)
     os.environ.setdefault("TMPDIR", "/tmp")
     if a.what in ("trace", "all"):
-        trace(a.raw, a.out, run=not a.summarize_only)
+        trace(a.workload, a.raw, a.out, run=not a.summarize_only)
     if a.what in ("counters", "all"):
-        counters(a.raw, a.out)
+        counters(a.workload, a.raw, a.out)
 
 
 if __name__ == "__main__":
