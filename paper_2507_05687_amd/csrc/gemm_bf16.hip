@@ -36,6 +36,8 @@ constexpr int kGN = GRPO_GEMM_GN;  // tile-columns per step of the walk
 constexpr int wait_vm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0070; }
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4* lds_i16x4_ptr_t;
 
 // Operand loads go global -> LDS through a buffer resource based at the
 // tile-row's first block: each lane's offset is fixed, the K step goes in the
@@ -112,15 +114,30 @@ struct EpiLse {
     s_out = s;
   }
 
+  // the sampled id of each of this lane's columns, loaded before the main
+  // loop so that the loop hides its latency (the per-token arrays hold a
+  // value for every column of the grid; those past the valid tokens are
+  // ignored)
+  template <int NI>
+  struct Pre {
+    int y[NI];
+  };
+  template <int NI>
+  __device__ __forceinline__ Pre<NI> prefetch(const Frag& f, int) const {
+    Pre<NI> p;
+    static_for<NI>([&](auto ni) { p.y[ni] = y_p[(int64_t)f.tn * kTile + f.col(ni)]; });
+    return p;
+  }
+
   template <int NI>
   __device__ __forceinline__ void operator()(f32x16 (&acc)[4][NI], const Frag& f, int m_valid,
-                                             int n_valid, char*) const {
+                                             int n_valid, char*, const Pre<NI>& pre) const {
     const int vbase = f.tm * kTile + f.wm * 128 + (f.lane >> 5) * 4;
     const int vlim = (int)(V - vbase);  // rows r of this lane are valid iff row offset < vlim
     const bool full = (int64_t)f.tm * kTile + f.wm * 128 + 128 <= V;  // wave-uniform
     static_for<NI>([&](auto ni) {
       const int64_t t = (int64_t)f.tn * kTile + f.col(ni);
-      const int y = t < n_valid ? y_p[t] - vbase : -1;  // y as a row offset of this lane
+      const int y = t < n_valid ? pre.y[ni] - vbase : -1;  // y as a row offset of this lane
       float m, s;
       if (full)
         column<true, NI>(acc, ni, m, s, vlim, y, zy + t);
@@ -148,37 +165,110 @@ struct EpiDz {
   int64_t V;       // vocabulary size
   int64_t v0;      // first vocabulary row of this chunk
 
+  // per column of this lane: sampled id, lse and g, loaded before the main
+  // loop so that the loop hides their latency (the per-token arrays hold a
+  // value for every column of the grid; those past the valid tokens are
+  // ignored)
+  template <int NI>
+  struct Pre {
+    int y[NI];
+    float lse[NI], g[NI];
+  };
+  template <int NI>
+  __device__ __forceinline__ Pre<NI> prefetch(const Frag& f, int) const {
+    Pre<NI> p;
+    static_for<NI>([&](auto ni) {
+      const int64_t t = (int64_t)f.tn * kTile + f.col(ni);
+      p.y[ni] = y_p[t];
+      p.lse[ni] = lse_p[t];
+      p.g[ni] = g_p[t];
+    });
+    return p;
+  }
+
   template <int NI>
   __device__ __forceinline__ void operator()(f32x16 (&acc)[4][NI], const Frag& f, int m_valid,
-                                             int n_valid, char*) const {
+                                             int n_valid, char* smem, const Pre<NI>& pre) const {
     const int hi = (f.lane >> 5) * 4;
     const int64_t vbase = v0 + (int64_t)f.tm * kTile + f.wm * 128 + hi;
     const int vlim = (int)((V - vbase) < (1 << 20) ? (V - vbase) : (1 << 20));
     // every row of this wave is inside the vocabulary: no per-element bound
     const bool full = v0 + (int64_t)f.tm * kTile + f.wm * 128 + 128 <= V;  // wave-uniform
+    // this wave's staging area: its 128 x (32 NI) part of the tile as four
+    // 32-wide vocabulary blocks of 32 NI token rows (64 bytes each)
+    char* stage = smem + (f.wn * 2 + f.wm) * (NI * 8192);
     if (full)
-      body(acc, f, n_valid, vbase, vlim, std::true_type{});
+      body(acc, f, pre, n_valid, vbase, vlim, stage, std::true_type{});
     else
-      body(acc, f, n_valid, vbase, vlim, std::false_type{});
+      body(acc, f, pre, n_valid, vbase, vlim, stage, std::false_type{});
+    // The LDS operations of one wave complete in order; the wait only makes
+    // the staged values visible before any lane reads another lane's.
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+    const int64_t t0 = (int64_t)f.tn * kTile + f.cbase;  // the wave's first token
+    // Token-major dz: the wave's part of each vocabulary block is 32 NI
+    // consecutive 64-byte rows of one tiled block, written 16 bytes per lane
+    // in whole lines.
+    static_for<4>([&](auto mi) {
+      uint16_t* pb = dz + ((t0 >> 8) * dz_kt + f.tm * 8 + f.wm * 4 + mi) * kTileElems;
+      static_for<2 * NI>([&](auto it) {
+        const int tl = it * 16 + (f.lane >> 2), c = f.lane & 3;
+        const u32x4 v = *(const u32x4*)(stage + mi * (NI * 2048) + tl * 64 + (stage_chunk(tl, c) << 4));
+        *(u32x4*)(pb + ((t0 & 255) + tl) * 32 + c * 8) = v;
+      });
+    });
+    if (dzT == nullptr) return;
+    // Vocabulary-major dzT: transposing LDS reads (ds_read_b64_tr_b16: within
+    // each 16 lanes, lane i receives element i%4 of lanes i/4, 4 + i/4,
+    // 8 + i/4, 12 + i/4) give each lane 8 consecutive tokens of one vocabulary
+    // row; one store covers 16 rows x 32 tokens of a tiled block, 1 KiB.
+    const int g4 = f.lane >> 4, i16 = f.lane & 15;
+    const int jr = (f.lane >> 2) & 3, qv = f.lane & 3;  // source row / vocabulary quad
+    static_for<NI>([&](auto ni) {
+      uint16_t* pbt = dzT + ((int64_t)f.tm * dzT_kt + ((t0 >> 5) + ni)) * kTileElems +
+                      (f.wm * 128) * 32;
+      static_for<4>([&](auto mi) {
+        static_for<2>([&](auto vh) {
+          i16x4 r[2];
+          static_for<2>([&](auto h) {
+            const int tl = ni * 32 + g4 * 8 + h * 4 + jr;
+            const int vq = vh * 16 + qv * 4;  // first of the 4 vocabulary entries read
+            r[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_i16x4_ptr_t)(stage + mi * (NI * 2048) + tl * 64 +
+                                  (stage_chunk(tl, vq >> 3) << 4) + (vq & 7) * 2));
+          });
+          const u32x4 v = {__builtin_bit_cast(uint32_t, __builtin_shufflevector(r[0], r[0], 0, 1)),
+                           __builtin_bit_cast(uint32_t, __builtin_shufflevector(r[0], r[0], 2, 3)),
+                           __builtin_bit_cast(uint32_t, __builtin_shufflevector(r[1], r[1], 0, 1)),
+                           __builtin_bit_cast(uint32_t, __builtin_shufflevector(r[1], r[1], 2, 3))};
+          *(u32x4*)(pbt + (mi * 32 + vh * 16 + i16) * 32 + g4 * 8) = v;
+        });
+      });
+    });
   }
 
+  // Physical 16-byte chunk of logical chunk c in staging row tl: a row-dependent
+  // XOR that keeps the staging writes at two lanes per bank and both readbacks
+  // (16-byte row reads and transposing reads of four consecutive rows) free of
+  // bank conflicts.
+  static __device__ __forceinline__ int stage_chunk(int tl, int c) {
+    const int m = (tl >> 1) & 3;
+    return c ^ m ^ ((m & 1) << 1);
+  }
+
+  // dz of this lane's columns, in bf16, staged in LDS (token-major)
   template <int NI, class Full>
-  __device__ __forceinline__ void body(f32x16 (&acc)[4][NI], const Frag& f, int n_valid,
-                                       int64_t vbase, int vlim, Full) const {
+  __device__ __forceinline__ void body(f32x16 (&acc)[4][NI], const Frag& f, const Pre<NI>& pre,
+                                       int n_valid, int64_t vbase, int vlim, char* stage,
+                                       Full) const {
     const int hi = (f.lane >> 5) * 4;
     static_for<NI>([&](auto ni) {
       const int64_t t = (int64_t)f.tn * kTile + f.col(ni);
       const bool tv = t < n_valid;
-      const int y = tv ? (int)(y_p[t] - vbase) : -1;  // y as a row offset of this lane
+      const int y = tv ? (int)(pre.y[ni] - vbase) : -1;  // y as a row offset of this lane
       // p = exp(z - lse) = exp2(z*log2e - lse*log2e); invalid columns get g = 0
-      const float l2 = tv ? lse_p[t] * kLog2e : 0.f;
-      const float g = tv ? g_p[t] : 0.f;
-      // element (t, vl) of dz lives in block (t/256, vl/32), row t%256, column vl%32
-      uint16_t* pz = dz + ((t >> 8) * dz_kt + f.tm * 8 + f.wm * 4) * kTileElems + (t & 255) * 32 + hi;
-      // element (vl, t) of dzT lives in block (vl/256, t/32), row vl%256, column t%32
-      uint16_t* pzt = dzT ? dzT + ((int64_t)f.tm * dzT_kt + (t >> 5)) * kTileElems + (t & 31) +
-                                (f.wm * 128 + hi) * 32
-                          : nullptr;
+      const float l2 = tv ? pre.lse[ni] * kLog2e : 0.f;
+      const float g = tv ? pre.g[ni] : 0.f;
+      const int tl = ni * 32 + (f.lane & 31);  // this column's row in the staging blocks
       static_for<4>([&](auto mi) {
         static_for<4>([&](auto q) {
           float d[4];
@@ -190,14 +280,8 @@ struct EpiDz {
             d[e] = (Full::value || o < vlim) ? dv : 0.f;
           });
           const uint32_t w0 = bf16_pack2(d[0], d[1]), w1 = bf16_pack2(d[2], d[3]);
-          if (pzt) {
-            constexpr int o = mi * 32 + q * 8;
-            pzt[o * 32] = (uint16_t)w0;
-            pzt[(o + 1) * 32] = (uint16_t)(w0 >> 16);
-            pzt[(o + 2) * 32] = (uint16_t)w1;
-            pzt[(o + 3) * 32] = (uint16_t)(w1 >> 16);
-          }
-          *(uint2*)(pz + mi * kTileElems + q * 8) = make_uint2(w0, w1);
+          *(uint2*)(stage + mi * (NI * 2048) + tl * 64 + (stage_chunk(tl, q) << 4) + hi * 2) =
+              make_uint2(w0, w1);
         });
       });
     });
@@ -217,8 +301,15 @@ struct EpiStore {
   int64_t n_limit;       // columns >= n_limit are not stored
 
   template <int NI>
+  struct Pre {};
+  template <int NI>
+  __device__ __forceinline__ Pre<NI> prefetch(const Frag&, int) const {
+    return {};
+  }
+
+  template <int NI>
   __device__ __forceinline__ void operator()(f32x16 (&acc)[4][NI], const Frag& f, int m_valid,
-                                             int n_valid, char*) const {
+                                             int n_valid, char*, const Pre<NI>&) const {
     const int64_t mlim = m_limit < m_valid ? m_limit : m_valid;
     const int64_t m0 = (int64_t)f.tm * kTile + f.wm * 128 + (f.lane >> 5) * 4;
     const int64_t n0 = (int64_t)f.tn * kTile + f.cbase + (f.lane & 31);
@@ -354,6 +445,8 @@ __global__ void __launch_bounds__(64 * kWaves, 1) k_gemm_bf16(GemmArgs g, Epi ep
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = w & 1, wn = w >> 1;
+  const Frag f{tm, tn, wm, wn, lane, wn * kWN};
+  const auto pre = epi.template prefetch<NI>(f, n_valid);
 
   f32x16 acc[4][NI];
   static_for<4>([&](auto i) {
@@ -460,8 +553,7 @@ __global__ void __launch_bounds__(64 * kWaves, 1) k_gemm_bf16(GemmArgs g, Epi ep
   }
   __syncthreads();  // every load has landed before LDS is reused
 
-  Frag f{tm, tn, wm, wn, lane, wn * kWN};
-  epi(acc, f, m_valid, n_valid, smem);
+  epi(acc, f, m_valid, n_valid, smem, pre);
 }
 
 // ---- four-wave variant: one wave per SIMD, each owning 128x128 as 4x4
@@ -490,6 +582,8 @@ __global__ void __launch_bounds__(64 * kW4Waves, 1) k_gemm_w4(GemmArgs g, Epi ep
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = w & 1, wn = w >> 1;
+  const Frag f{tm, tn, wm, wn, lane, wn * 128};
+  const auto pre = epi.template prefetch<NI>(f, n_valid);
 
   f32x16 acc[4][NI];
   static_for<4>([&](auto i) {
@@ -581,8 +675,7 @@ __global__ void __launch_bounds__(64 * kW4Waves, 1) k_gemm_w4(GemmArgs g, Epi ep
   if (kt < nk) step(kt, I0{});
   __syncthreads();  // every load has landed before LDS is reused
 
-  Frag f{tm, tn, wm, wn, lane, wn * 128};
-  epi(acc, f, m_valid, n_valid, smem);
+  epi(acc, f, m_valid, n_valid, smem, pre);
 }
 
 // The two gradient products (long K, fp32 store epilogues) run faster on the
