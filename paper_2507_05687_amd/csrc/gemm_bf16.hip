@@ -53,7 +53,8 @@ __device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, char* lds, 
 }
 
 // Maps a workgroup id to its (tile_m, tile_n); returns false for the
-// padding workgroups of the last band.
+// padding workgroups of the last band. With fewer than 8 kGM tile-rows there
+// are not enough rows for a band per XCD (column_tile_of).
 __device__ inline bool tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
   int xcd = bid & 7, loc = bid >> 3;
   int per_band = kGM * tiles_n;
@@ -66,9 +67,33 @@ __device__ inline bool tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& 
   return tm < tiles_m;
 }
 
+// Few tile-rows: each XCD takes an eighth of the tile-columns that hold valid
+// columns (tiles_n, known only on the device when the column count is), all
+// rows, walking them column by column; false for workgroups without a tile.
+__device__ inline bool column_tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int xcd = bid & 7, loc = bid >> 3;
+  const int cols = (tiles_n + 7) >> 3;  // tile-columns per XCD
+  if (loc >= tiles_m * cols) return false;
+  tm = loc % tiles_m;
+  tn = xcd * cols + loc / tiles_m;
+  return tn < tiles_n;
+}
+
+// Tile of this workgroup, or false if it has none (or only rows or columns
+// past the valid counts). The mapping is chosen by the grid's tile-rows.
+__device__ inline bool gemm_tile(const GemmArgs& g, int m_valid, int n_valid, int& tm, int& tn) {
+  if (g.tiles_m < 8 * kGM) {
+    if (m_valid <= 0 || n_valid <= 0) return false;
+    return column_tile_of(blockIdx.x, min(g.tiles_m, (int)ceil_div(m_valid, kTile)),
+                          min(g.tiles_n, (int)ceil_div(n_valid, kTile)), tm, tn);
+  }
+  return tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn) && tm * kTile < m_valid &&
+         tn * kTile < n_valid;
+}
+
 int gemm_grid(int tiles_m, int tiles_n) {
-  int bands = (int)ceil_div(tiles_m, 8 * kGM);
-  return bands * 8 * kGM * tiles_n;
+  if (tiles_m < 8 * kGM) return 8 * tiles_m * (int)ceil_div(tiles_n, 8);
+  return (int)ceil_div(tiles_m, 8 * kGM) * 8 * kGM * tiles_n;
 }
 
 // ------------------------------------------------------------ epilogues
@@ -434,11 +459,10 @@ template <class Epi>
 __global__ void __launch_bounds__(64 * kWaves, 1) k_gemm_bf16(GemmArgs g, Epi epi) {
   constexpr int NI = kNI;
   __shared__ __attribute__((aligned(16))) char smem[kStages * kStage];
-  int tm, tn;
-  if (!tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn)) return;
   const int m_valid = g.m_dev ? min(*g.m_dev, g.M) : g.M;
   const int n_valid = g.n_dev ? min(*g.n_dev, g.N) : g.N;
-  if (tm * kTile >= m_valid || tn * kTile >= n_valid) return;
+  int tm, tn;
+  if (!gemm_tile(g, m_valid, n_valid, tm, tn)) return;
   const int K = g.k_dev ? (int)round_up(*g.k_dev, kBK) : g.K;
 
   const int tid = threadIdx.x;
@@ -571,11 +595,10 @@ template <class Epi>
 __global__ void __launch_bounds__(64 * kW4Waves, 1) k_gemm_w4(GemmArgs g, Epi epi) {
   constexpr int NI = 4;
   __shared__ __attribute__((aligned(16))) char smem[kStages * kStage];
-  int tm, tn;
-  if (!tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn)) return;
   const int m_valid = g.m_dev ? min(*g.m_dev, g.M) : g.M;
   const int n_valid = g.n_dev ? min(*g.n_dev, g.N) : g.N;
-  if (tm * kTile >= m_valid || tn * kTile >= n_valid) return;
+  int tm, tn;
+  if (!gemm_tile(g, m_valid, n_valid, tm, tn)) return;
   const int K = g.k_dev ? (int)round_up(*g.k_dev, kBK) : g.K;
 
   const int tid = threadIdx.x;

@@ -87,13 +87,19 @@ grpo_status check_device() {
 // --------------------------------------------------------- workspace
 constexpr size_t kAlign = 256;
 #ifndef GRPO_DZ_BUDGET_GIB
-#define GRPO_DZ_BUDGET_GIB 8
+#define GRPO_DZ_BUDGET_GIB 12
 #endif
 #ifndef GRPO_VC_MAX
-#define GRPO_VC_MAX 16384
+#define GRPO_VC_MAX 8192
+#endif
+#ifndef GRPO_DH_GROUP
+#define GRPO_DH_GROUP 2
 #endif
 constexpr int64_t kDzBudget = (int64_t)GRPO_DZ_BUDGET_GIB << 30;  // bytes for the two bf16 dz buffers
 constexpr int64_t kVcMax = GRPO_VC_MAX;
+// dz chunks per dL/dh product: dz and dL/dW run per chunk, dL/dh once per
+// group of chunks (fewer passes over its fp32 accumulator)
+constexpr int64_t kDhGroup = GRPO_DH_GROUP;
 
 struct Layout {
   int64_t Npad = 0, Vpad = 0, tiles_v = 0, Vc = 0, nchunks = 0;
@@ -120,11 +126,12 @@ size_t take(size_t& cur, size_t bytes) {
   return at;
 }
 
-// Vocabulary chunk for the backward pass: the two bf16 dz buffers
-// (token-major and vocabulary-major) together stay within kDzBudget, chunks
-// are at most kVcMax rows, and all chunks but the last have equal size.
+// Vocabulary chunk for the backward pass: the two bf16 dz buffers (token-major
+// for a group of kDhGroup chunks, vocabulary-major for one chunk) together
+// stay within kDzBudget, chunks are at most kVcMax rows, and all chunks but
+// the last have equal size.
 void chunking(int64_t Npad, int64_t Vpad, int64_t& Vc, int64_t& nchunks) {
-  int64_t cap = kDzBudget / (4 * Npad) / kTile * kTile;
+  int64_t cap = kDzBudget / (2 * (kDhGroup + 1) * Npad) / kTile * kTile;
   if (cap < kTile) cap = kTile;
   if (cap > kVcMax) cap = kVcMax;
   nchunks = ceil_div(Vpad, cap);
@@ -162,13 +169,13 @@ Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_
       int64_t Hpad = round_up(H, kTile);
       L.sTok = tile_stride(L.Npad);
       L.sVoc = tile_stride(L.Vpad);
-      L.sChunk = tile_stride(L.Vc);
+      L.sChunk = tile_stride(kDhGroup * L.Vc);
       L.hT = take(c, 2 * Hpad * L.sTok * kBK);
       L.WT = take(c, 2 * Hpad * L.sVoc * kBK);
       L.dz = take(c, 2 * L.Npad * L.sChunk * kBK);
       L.dzT = take(c, 2 * L.Vc * L.sTok * kBK);
       // fp32 dh accumulator with every row and column of every tile present
-      if (L.nchunks > 1) L.dhacc = take(c, 4 * L.Npad * Hpad);
+      if (L.nchunks > kDhGroup) L.dhacc = take(c, 4 * L.Npad * Hpad);
     }
   }
   L.total = c;
@@ -316,9 +323,9 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
   uint16_t* WT = at<uint16_t>(ws, L.WT);
   uint16_t* dz = at<uint16_t>(ws, L.dz);
   uint16_t* dzT = at<uint16_t>(ws, L.dzT);
-  float* dhacc = L.nchunks > 1 ? at<float>(ws, L.dhacc) : nullptr;
+  float* dhacc = L.nchunks > kDhGroup ? at<float>(ws, L.dhacc) : nullptr;
   // Intermediates in the tiled layout: h^T [H x tokens], W^T [H x V],
-  // dz [tokens x chunk] and dz^T [chunk x tokens].
+  // dz [tokens x group of chunks] and dz^T [chunk x tokens].
   const int64_t kt_tok = L.sTok, kt_voc = L.sVoc, kt_chunk = L.sChunk, kt_h = L.sK;
   if (grad_weight) {
     TRY(timed(K_TRANSPOSE, s, [&] {
@@ -337,32 +344,18 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
     int64_t Mc = V - v0 < L.Vc ? V - v0 : L.Vc;
     if (Mc <= 0) break;
     bool last = (c == L.nchunks - 1) || (v0 + L.Vc >= V);
-    // recompute the logits of this chunk and form dz (both layouts)
+    const int64_t j = c % kDhGroup;    // position of the chunk in its dL/dh group
+    const int64_t vg = v0 - j * L.Vc;  // first vocabulary row of the group
+    // recompute the logits of this chunk and form dz (both layouts; the
+    // token-major copy at the chunk's place in the group buffer)
     GemmArgs gz = gemm_args(at<uint16_t>(ws, L.WK) + (v0 / kTile) * kt_h * kTileElems, kt_h, Mc,
                             at<uint16_t>(ws, L.hK), kt_h, L.Npad, nullptr, &hdr->num_valid, L.Hk,
                             nullptr);
+    uint16_t* dz_c = dz + j * (L.Vc / kBK) * kTileElems;
     TRY(timed(K_GEMM_DZ, s, [&] {
-      launch_gemm_dz(gz, y_p, lse_p, g_p, dz, kt_chunk, grad_weight ? dzT : nullptr, kt_tok, V, v0,
-                     s);
+      launch_gemm_dz(gz, y_p, lse_p, g_p, dz_c, kt_chunk, grad_weight ? dzT : nullptr, kt_tok, V,
+                     v0, s);
     }));
-    if (grad_hidden) {
-      // dh[t, :] (+)= sum_{v in chunk} dz[t, v] W[v, :]
-      GemmArgs gh = gemm_args(dz, kt_chunk, L.Npad, WT, kt_voc, H, &hdr->num_valid, nullptr,
-                              round_up(Mc, kBK), nullptr);
-      gh.b_kb0 = v0 / kBK;
-      StoreArgs sa{};
-      sa.acc_buf = dhacc;
-      sa.ld_acc = round_up(H, kTile);
-      sa.read_acc = c > 0;
-      sa.out = last ? grad_hidden : nullptr;
-      sa.ld_out = H;
-      sa.out_bf16 = grad_hidden_dt == GRPO_BF16;
-      sa.add_out = 0;
-      sa.out_rows = rows_p;
-      sa.m_limit = L.Npad;
-      sa.n_limit = H;
-      TRY(timed(K_GEMM_DH, s, [&] { launch_gemm_store(gh, sa, false, s); }));
-    }
     if (grad_weight) {
       // dW[v, :] = sum_t dz[t, v] h[t, :] over the valid tokens
       GemmArgs gw = gemm_args(dzT, kt_tok, Mc, hT, kt_tok, H, nullptr, nullptr, 0,
@@ -379,6 +372,24 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
       sa.m_limit = Mc;
       sa.n_limit = H;
       TRY(timed(K_GEMM_DW, s, [&] { launch_gemm_store(gw, sa, true, s); }));
+    }
+    if (grad_hidden && (j == kDhGroup - 1 || last)) {
+      // dh[t, :] (+)= sum_{v in group} dz[t, v] W[v, :]
+      GemmArgs gh = gemm_args(dz, kt_chunk, L.Npad, WT, kt_voc, H, &hdr->num_valid, nullptr,
+                              round_up(v0 + Mc - vg, kBK), nullptr);
+      gh.b_kb0 = vg / kBK;
+      StoreArgs sa{};
+      sa.acc_buf = dhacc;
+      sa.ld_acc = round_up(H, kTile);
+      sa.read_acc = vg > 0;
+      sa.out = last ? grad_hidden : nullptr;
+      sa.ld_out = H;
+      sa.out_bf16 = grad_hidden_dt == GRPO_BF16;
+      sa.add_out = 0;
+      sa.out_rows = rows_p;
+      sa.m_limit = L.Npad;
+      sa.n_limit = H;
+      TRY(timed(K_GEMM_DH, s, [&] { launch_gemm_store(gh, sa, false, s); }));
     }
     if (last) break;
   }
