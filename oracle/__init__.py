@@ -20,6 +20,8 @@ What each function follows (AutoTriton, Sec. 3.3):
   grad_hidden_rows  dL/dh, exact chain rule through the log-softmax
   grad_weight_rows  dL/dW, same
   grpo_loss         the whole loss and gradients for small problems
+  rule_rewards      Eq. 3: is_Triton (the @triton.jit rule of Sec. 4, plain
+                    Python in rule_reward.py) combined with test_passed
 """
 from __future__ import annotations
 
@@ -226,3 +228,5 @@ def adamw(w, m, v, g, step: int, lr: float, beta1: float, beta2: float, eps: flo
     w = w - lr * weight_decay * w - lr * m_hat / (np.sqrt(v_hat) + eps)
     return w, m, v
 
+
+from .rule_reward import is_triton, rule_rewards  # noqa: E402,F401

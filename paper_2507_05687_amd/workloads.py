@@ -198,3 +198,124 @@ def sample_rows(mask: np.ndarray, count: int, seed: int = 0) -> np.ndarray:
     g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 99])))
     k = min(count, valid.size)
     return np.sort(g.choice(valid, size=k, replace=False)).astype(np.int64)
+
+
+# ------------------------------------------------------------ completions
+# Seeded synthetic completions for the rule-based reward (Sec. 3.3, Eq. 3):
+# Python sources assembled from small fragments written for this purpose
+# (an elementwise Triton kernel, its launcher, a PyTorch fallback, filler
+# statements), with the variations the rule has to tell apart: decorator
+# present, commented out, misspelt, with arguments, after other decorators,
+# not followed by a function; the kernel launched, launched through a module,
+# never launched, or a different name launched. They stand in for the
+# paper's rollouts, whose benchmark items are not used.
+
+_HEADER = "import torch\nimport triton\nimport triton.language as tl\n\n"
+_KERNEL = (
+    "def {name}(x_ptr, y_ptr, out_ptr, n_elements, BLOCK: tl.constexpr):\n"
+    "    pid = tl.program_id(axis=0)\n"
+    "    offs = pid * BLOCK + tl.arange(0, BLOCK)\n"
+    "    mask = offs < n_elements\n"
+    "    x = tl.load(x_ptr + offs, mask=mask)\n"
+    "    y = tl.load(y_ptr + offs, mask=mask)\n"
+    "    tl.store(out_ptr + offs, x {op} y, mask=mask)\n\n")
+_LAUNCHER = (
+    "def {fn}(x, y):\n"
+    "    out = torch.empty_like(x)\n"
+    "    n = out.numel()\n"
+    "    grid = lambda meta: (triton.cdiv(n, meta['BLOCK']),)\n"
+    "    {call}\n"
+    "    return out\n\n")
+_TORCH = "def {fn}(x, y):\n    return x {op} y\n\n"
+_FILLER = [
+    "scale = {k} * 0.5\n", "# keep the block size a power of two ({k})\n",
+    "values = [i * {k} for i in range(8)]\n", "assert {k} >= 0\n",
+    "config = dict(block={k}, warps=4)\n", "total = sum(values) + {k}\n",
+]
+_VALID_DECOS = ["@triton.jit", "@triton.jit()", "@triton.jit(do_not_specialize=['n_elements'])",
+                "@triton.jit(\n    debug=False,\n)", "@triton.autotune(configs=[], key=['n_elements'])\n@triton.jit",
+                "@triton.jit\n# the kernel\n", "    @triton.jit"]
+_DECOY_DECOS = ["# @triton.jit", "@triton.jitted", "@triton.jit.fn", "@triton.heuristics({})"]
+_BROKEN_DECOS = ["@triton.jit x", "@triton.jit(", "y = 1 @triton.jit"]
+
+
+def _ident(rng, prefix: str) -> str:
+    return prefix + "_" + "".join(rng.choice(list("abcdefghijklmnopqrstuvwxyz"), size=5))
+
+
+def _completion(rng, target_len: int, valid: bool) -> bytes:
+    name = _ident(rng, "kernel")
+    other = _ident(rng, "helper")
+    op = str(rng.choice(["+", "-", "*"]))
+    parts = [_HEADER]
+    # the kernel, with a decorator variant (or none)
+    r = rng.random()
+    if r < 0.55:
+        deco = str(rng.choice(_VALID_DECOS))
+    elif r < 0.75:
+        deco = str(rng.choice(_DECOY_DECOS))
+    elif r < 0.85 or valid:
+        deco = ""
+    else:
+        deco = str(rng.choice(_BROKEN_DECOS))
+    kernel = _KERNEL.format(name=name, op=op)
+    if deco.startswith("    "):  # a kernel defined inside a class body
+        kernel = "class Ops:\n" + deco + "\n" + "".join("    " + ln + "\n" if ln else "\n"
+                                                       for ln in kernel.split("\n"))
+    elif deco:
+        kernel = deco.rstrip("\n") + "\n" + kernel
+    if not valid and rng.random() < 0.05:  # decorator left without a function
+        kernel = "@triton.jit\nvalue = 3\n\n" + kernel
+    parts.append(kernel)
+    # the launcher, with a launch variant (or a PyTorch fallback)
+    r = rng.random()
+    launches = [f"{name}[grid](x, y, out, n, BLOCK=1024)",
+                f"{name} [grid] (x, y, out, n, BLOCK=1024)",
+                f"{name}[(triton.cdiv(n, 256), 1)](x, y, out, n, BLOCK=256)"]
+    if deco.startswith("    "):
+        launches = [f"Ops.{name}[grid](x, y, out, n, BLOCK=1024)"]
+    if r < 0.6:
+        call = str(rng.choice(launches))
+    elif r < 0.7:
+        call = f"{other}[grid](x, y, out, n, BLOCK=1024)"
+    elif r < 0.8:
+        call = f"spec = {name}[grid]"
+    elif r < 0.85 and not valid:
+        call = f"{name}[grid(x, y, out, n)"
+    else:
+        call = f"out = x {op} y"
+    if rng.random() < 0.3:
+        parts.append(_TORCH.format(fn=_ident(rng, "torch_ref"), op=op))
+    parts.append(_LAUNCHER.format(fn=_ident(rng, "run"), call=call))
+    text = "".join(parts)
+    while len(text) < target_len:
+        text += str(rng.choice(_FILLER)).format(k=int(rng.integers(0, 1000)))
+    if not valid and rng.random() < 0.1:
+        text = text.replace("\n", "\r\n")
+    if not valid and rng.random() < 0.05:
+        text = text[: int(rng.integers(0, len(text) + 1))]  # cut off mid-completion
+    data = text.encode("utf-8")
+    if not valid and rng.random() < 0.05:
+        data += "  # π ≈ 3.14, ü\n".encode("utf-8")
+    return data
+
+
+def make_completions(count: int, seed: int, mean_len: int = 2000, max_len: int = 16384,
+                     valid: bool = False, pass_rate: float = 0.5):
+    """count seeded synthetic completions (bytes, lengths drawn around
+    mean_len up to max_len) and test_passed flags (u8). With valid=True every
+    completion is a syntactically valid Python module."""
+    rng = np.random.default_rng(seed)
+    lens = np.minimum(rng.exponential(mean_len, size=count).astype(np.int64) + 200, max_len)
+    texts = [_completion(rng, int(n), valid) for n in lens]
+    passed = (rng.random(count) < pass_rate).astype(np.uint8)
+    return texts, passed
+
+
+def pack_completions(texts):
+    """Concatenated bytes (u8) and offsets (int64 [count + 1]) of completions."""
+    offsets = np.zeros(len(texts) + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum([len(t) for t in texts])
+    data = np.frombuffer(b"".join(texts), dtype=np.uint8).copy() if offsets[-1] else np.zeros(
+        0, dtype=np.uint8)
+    return data, offsets
