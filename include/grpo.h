@@ -235,6 +235,40 @@ grpo_status adamw_step(float* weight, float* exp_avg, float* exp_avg_sq, const f
                        uint16_t* weight_bf16, int64_t n, float lr, float beta1, float beta2,
                        float eps, float weight_decay, int64_t step, hipStream_t stream);
 
+/*
+ * triton_rule_reward -- the reward of the RL stage (AutoTriton Sec. 3.3,
+ * Eq. 3): R = 1 if is_Triton(completion) and test_passed, else 0; or, with
+ * weighted = 1, R = rule_weight * is_Triton + exec_weight * test_passed (the
+ * rule-based reward given alongside the execution reward, Sec. 4), in fp32.
+ * is_Triton is the lexical rule Sec. 4 describes -- a function decorated
+ * with @triton.jit -- and, with require_launch = 1, that function launched
+ * as name[grid](...) somewhere in the completion (Sec. 4's hack of a kernel
+ * that is never called). Exact rule: a decorator is "@triton.jit" with only
+ * blanks (space, tab, CR) before it on its line and no identifier byte or "."
+ * after it, optional balanced "(...)" arguments, then only blanks or a "#"
+ * comment to the newline; blank, comment and other decorator lines may
+ * follow; then a line "def NAME(" (blanks allowed around NAME). A launch is
+ * NAME not preceded by an identifier byte, blanks, "[", a bracket-balanced
+ * run, "]", blanks, "(". Strings and comments are not otherwise parsed.
+ *   text        the completions' bytes, concatenated. Device.
+ *   offsets     [num_completions + 1] int64: completion b is
+ *               text[offsets[b], offsets[b+1]); a decreasing pair counts as
+ *               an empty completion. Device.
+ *   test_passed [num_completions] u8, nonzero = the execution harness's
+ *               tests passed (that harness is outside this library). Device.
+ *   is_triton   [num_completions] u8 output (0/1). Device.
+ *   reward      [num_completions] fp32 output, the input of
+ *               group_advantages. Device.
+ * Requires require_launch, weighted in {0, 1}, finite weights. Enqueued on
+ * `stream`, no workspace; num_completions = 0 does nothing (no pointer is
+ * read).
+ */
+grpo_status triton_rule_reward(const uint8_t* text, const int64_t* offsets,
+                               int64_t num_completions, const uint8_t* test_passed,
+                               int32_t require_launch, int32_t weighted, float rule_weight,
+                               float exec_weight, uint8_t* is_triton, float* reward,
+                               hipStream_t stream);
+
 /* Bytes of workspace an operation needs for these sizes (0 if the sizes are
  * invalid). For GRPO_OP_LOGPROB_FWD and GRPO_OP_SFT_FWD_BWD pass
  * num_seqs = 1. Host only. */

@@ -19,12 +19,14 @@ namespace {
 // --------------------------------------------------------- kernel timing
 enum Kind {
   K_PACK, K_ADV, K_GEMM_LSE, K_LSE_FIN, K_TOKEN, K_TRANSPOSE, K_GEMM_DZ, K_GEMM_DH, K_GEMM_DW,
-  K_F32_SCORE, K_F32_DH, K_F32_DW, K_ZERO_ROWS, K_GATHER_DOT, K_TILE, K_ADAMW, K_NUM_KINDS
+  K_F32_SCORE, K_F32_DH, K_F32_DW, K_ZERO_ROWS, K_GATHER_DOT, K_TILE, K_ADAMW,
+  K_RULE_REWARD, K_NUM_KINDS
 };
 const char* kKindNames[K_NUM_KINDS] = {
     "pack_valid",  "group_advantages", "gemm_logits_lse", "lse_finalize",   "token_objective",
     "transpose",   "gemm_recompute_dz", "gemm_grad_hidden", "gemm_grad_weight", "f32_score",
-    "f32_grad_hidden", "f32_grad_weight", "zero_masked_rows", "gather_dot", "tile", "adamw"};
+    "f32_grad_hidden", "f32_grad_weight", "zero_masked_rows", "gather_dot", "tile", "adamw",
+    "rule_reward"};
 
 struct Prof {
   std::mutex mu;
@@ -654,6 +656,31 @@ grpo_status adamw_step(float* weight, float* exp_avg, float* exp_avg_sq, const f
   a.step_size = (float)((double)lr / bc1);
   a.inv_sqrt_bc2 = (float)(1.0 / sqrt(bc2));
   return timed(K_ADAMW, stream, [&] { launch_adamw(a, stream); });
+}
+
+grpo_status triton_rule_reward(const uint8_t* text, const int64_t* offsets,
+                               int64_t num_completions, const uint8_t* test_passed,
+                               int32_t require_launch, int32_t weighted, float rule_weight,
+                               float exec_weight, uint8_t* is_triton, float* reward,
+                               hipStream_t stream) {
+  if (num_completions < 0 || num_completions > 0x7fffffff) return GRPO_ERR_SHAPE;
+  if ((require_launch != 0 && require_launch != 1) || (weighted != 0 && weighted != 1) ||
+      !isfinite(rule_weight) || !isfinite(exec_weight))
+    return GRPO_ERR_PARAM;
+  if (num_completions == 0) return GRPO_OK;
+  if (!text || !offsets || !test_passed || !is_triton || !reward) return GRPO_ERR_NULL;
+  TRY(check_device());
+  RewardArgs a;
+  a.text = text;
+  a.offsets = offsets;
+  a.test_passed = test_passed;
+  a.require_launch = require_launch;
+  a.weighted = weighted;
+  a.w_rule = rule_weight;
+  a.w_exec = exec_weight;
+  a.is_triton = is_triton;
+  a.reward = reward;
+  return timed(K_RULE_REWARD, stream, [&] { launch_rule_reward(a, num_completions, stream); });
 }
 
 grpo_status grpo_check_error(void* workspace, hipStream_t stream) {

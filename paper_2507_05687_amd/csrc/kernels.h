@@ -104,6 +104,19 @@ struct AdamArgs {
 };
 void launch_adamw(const AdamArgs& a, hipStream_t s);
 
+// ------------------------------------------------------------ rule reward
+struct RewardArgs {
+  const uint8_t* text;         // completions, concatenated
+  const int64_t* offsets;      // [count + 1]
+  const uint8_t* test_passed;  // [count]
+  int require_launch;          // is_Triton also needs a launch of the kernel
+  int weighted;                // reward = w_rule*is_Triton + w_exec*passed (else the product)
+  float w_rule, w_exec;
+  uint8_t* is_triton;  // [count]
+  float* reward;       // [count]
+};
+void launch_rule_reward(const RewardArgs& a, int64_t count, hipStream_t s);
+
 // ------------------------------------------------------------ others
 void launch_group_advantages(const float* rewards, int64_t num_prompts, int group, float eps,
                              int unbiased, float* adv, hipStream_t s);

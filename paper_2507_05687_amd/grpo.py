@@ -39,6 +39,7 @@ SIGNATURES = {
                               _vp, _i32, _vp, _sz, _vp]),
     "adamw_step": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _f32, _f32, _f32, _f32, _f32, _i64,
                           _vp]),
+    "triton_rule_reward": (_i32, [_vp, _vp, _i64, _vp, _i32, _i32, _f32, _f32, _vp, _vp, _vp]),
     "grpo_workspace_bytes": (_sz, [_i32, _i32, _i64, _i64, _i64, _i64]),
     "grpo_check_error": (_i32, [_vp, _vp]),
     "grpo_status_string": (ctypes.c_char_p, [_i32]),
@@ -302,6 +303,29 @@ def adamw_step(weight, exp_avg, exp_avg_sq, grad, step: int, lr: float = 1e-6,
                            _ptr(weight_bf16), n, lr, beta1, beta2, eps, weight_decay, int(step),
                            _stream())
     _check(st, "adamw_step")
+
+
+def triton_rule_reward(text, offsets, test_passed, require_launch: bool = False,
+                       weighted: bool = False, rule_weight: float = 0.0,
+                       exec_weight: float = 0.0):
+    """(is_triton u8, reward f32) per completion: Eq. 3's product of the
+    @triton.jit rule and test_passed, or the weighted sum. text: u8 device
+    bytes of the concatenated completions; offsets: int64 [B + 1]."""
+    _need(text, "text", torch.uint8)
+    _need(offsets, "offsets", torch.int64)
+    _need(test_passed, "test_passed", torch.uint8)
+    b = offsets.numel() - 1
+    if b < 0 or test_passed.numel() != b:
+        raise ValueError("offsets must have one entry more than test_passed")
+    flags = torch.empty(b, dtype=torch.uint8, device=text.device)
+    reward = torch.empty(b, dtype=torch.float32, device=text.device)
+    if text.numel() == 0:  # every completion is empty: any valid pointer will do
+        text = torch.zeros(1, dtype=torch.uint8, device=offsets.device)
+    st = load().triton_rule_reward(_ptr(text), _ptr(offsets), b, _ptr(test_passed),
+                                   int(require_launch), int(weighted), rule_weight, exec_weight,
+                                   _ptr(flags), _ptr(reward), _stream())
+    _check(st, "triton_rule_reward")
+    return flags, reward
 
 
 def check_error(ws: torch.Tensor):

@@ -31,7 +31,8 @@ def _declared_functions():
 def test_header_declares_the_boundary():
     names = _declared_functions()
     for required in ("group_advantages", "grpo_logprob_fwd", "grpo_loss_fwd_bwd",
-                     "sft_ce_fwd_bwd", "adamw_step", "grpo_pack_valid", "grpo_workspace_bytes",
+                     "sft_ce_fwd_bwd", "adamw_step", "triton_rule_reward", "grpo_pack_valid",
+                     "grpo_workspace_bytes",
                      "grpo_check_error", "grpo_status_string"):
         assert required in names
 
@@ -165,6 +166,30 @@ def test_adamw_argument_errors(lib):
     assert call(10, float("inf")) == 4    # weight decay
     assert call(1, ctypes.c_void_p(0x1004)) == 5
     assert call(4, ctypes.c_void_p(0x1002)) == 5
+
+
+def test_rule_reward_argument_errors(lib):
+    f = lib.triton_rule_reward
+    a = [P, P, 4, P, 0, 0, 0.0, 0.0, P, P, NULL]
+
+    def call(i, x):
+        b = list(a)
+        b[i] = x
+        return f(*b)
+
+    assert call(2, -1) == 2                  # count
+    assert call(2, 1 << 31) == 2
+    assert call(0, NULL) == 1
+    assert call(1, NULL) == 1
+    assert call(3, NULL) == 1
+    assert call(8, NULL) == 1
+    assert call(9, NULL) == 1
+    assert call(4, 2) == 4                   # require_launch
+    assert call(5, -1) == 4                  # weighted
+    assert call(6, float("nan")) == 4
+    assert call(7, float("inf")) == 4
+    assert call(2, 0) == 0                   # nothing to do: no launch, no device needed
+    assert f(NULL, NULL, 0, NULL, 0, 0, 0.0, 0.0, NULL, NULL, NULL) == 0
 
 
 def test_profile_interface_without_launches(lib):

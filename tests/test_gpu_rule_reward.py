@@ -1,0 +1,102 @@
+"""GPU parity of the rule-based reward (Sec. 3.3, Eq. 3) against the oracle:
+flags and rewards bit-exact on seeded synthetic completions, hand-written
+cases and edge cases, through the C-ABI."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2507_05687_amd import grpo, workloads
+
+from test_rule_reward_pins import CASES
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(texts, passed, **kw):
+    data, offsets = workloads.pack_completions(texts)
+    flags, reward = grpo.triton_rule_reward(torch.from_numpy(data).cuda(),
+                                            torch.from_numpy(offsets).cuda(),
+                                            torch.from_numpy(np.asarray(passed, np.uint8)).cuda(),
+                                            **kw)
+    torch.cuda.synchronize()
+    return flags.cpu().numpy(), reward.cpu().numpy()
+
+
+def _check(texts, passed, **kw):
+    for launch in (False, True):
+        got_f, got_r = _run(texts, passed, require_launch=launch, **kw)
+        want_f, want_r = oracle.rule_rewards(texts, passed, require_launch=launch, **kw)
+        bad = np.flatnonzero(got_f != want_f)
+        assert bad.size == 0, (launch, bad[:5], texts[bad[0]][:400])
+        assert np.array_equal(got_r.view(np.uint32), want_r.view(np.uint32)), launch
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_generated_completions(seed):
+    texts, passed = workloads.make_completions(300, seed=seed, mean_len=1500)
+    _check(texts, passed)
+    _check(texts, passed, weighted=True, rule_weight=0.1, exec_weight=0.9)
+
+
+def test_hand_written_cases():
+    texts = [c[0].encode() for c in CASES]
+    passed = np.ones(len(texts), np.uint8)
+    f0, _ = _run(texts, passed)
+    f1, _ = _run(texts, passed, require_launch=True)
+    assert np.array_equal(f0, np.array([c[1] for c in CASES], np.uint8))
+    assert np.array_equal(f1, np.array([c[2] for c in CASES], np.uint8))
+
+
+def test_full_size_batch():
+    # 8 prompts x G = 8 completions of up to 16,384 tokens (about 4 bytes each)
+    texts, passed = workloads.make_completions(64, seed=7, mean_len=30000, max_len=65536)
+    assert max(len(t) for t in texts) > 60000
+    _check(texts, passed)
+
+
+def test_edges():
+    kernel = b"@triton.jit\ndef k(x):\n    pass\n"
+    long_filler = b"x = 1\n" * 200000  # 1.2 MB
+    texts = [
+        b"", b"@", b"@triton.jit", kernel, kernel + b"k[(1,)](0)\n",
+        b"k[(1,)](0)\n" + long_filler + kernel,           # launch far before the kernel
+        kernel + long_filler + b"k[" + b"[" * 5000,         # unclosed brackets to the end
+        kernel.replace(b"\n", b"\r\n") + "# é ü\n".encode() + b"\x00\xff k [g]\t(1)",
+        b"@triton.jit\n" * 300 + b"def k(x):\n    pass\nk[1](2)\n",  # decorators stacked
+    ]
+    passed = np.array([1, 0] * 4 + [1], np.uint8)
+    _check(texts, passed)
+    # no completions; only empty ones
+    f, r = _run([], [])
+    assert f.size == 0 and r.size == 0
+    f, r = _run([b"", b""], [1, 1])
+    assert np.array_equal(f, [0, 0]) and np.array_equal(r, [0.0, 0.0])
+
+
+def test_decreasing_offsets_count_as_empty():
+    data = np.frombuffer(b"@triton.jit\ndef k(x):\n    pass\n", np.uint8).copy()
+    offsets = np.array([0, len(data), 5], np.int64)
+    flags, reward = grpo.triton_rule_reward(torch.from_numpy(data).cuda(),
+                                            torch.from_numpy(offsets).cuda(),
+                                            torch.ones(2, dtype=torch.uint8, device="cuda"))
+    assert flags.cpu().tolist() == [1, 0]
+    assert reward.cpu().tolist() == [1.0, 0.0]
+
+
+def test_many_small_completions():
+    texts, passed = workloads.make_completions(4096, seed=3, mean_len=300, max_len=2000)
+    _check(texts, passed)
+
+
+def test_reward_feeds_group_advantages():
+    # Eq. 3 rewards of G = 8 rollouts per prompt into Eq. 2
+    texts, passed = workloads.make_completions(64, seed=5, mean_len=800)
+    data, offsets = workloads.pack_completions(texts)
+    _, reward = grpo.triton_rule_reward(torch.from_numpy(data).cuda(),
+                                        torch.from_numpy(offsets).cuda(),
+                                        torch.from_numpy(passed).cuda())
+    adv = grpo.group_advantages(reward, 8).cpu().numpy()
+    _, want_r = oracle.rule_rewards(texts, passed)
+    want = oracle.advantages(want_r.astype(np.float64), 8)
+    assert np.max(np.abs(adv - want)) <= 1e-5 * max(1.0, np.max(np.abs(want)))

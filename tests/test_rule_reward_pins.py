@@ -100,8 +100,8 @@ def test_reward_forms():
     assert np.array_equal(flags, deco.astype(np.uint8))
     # Eq. 3: 1 exactly when both checks pass
     assert np.array_equal(r, (deco & (passed != 0)).astype(np.float32))
-    flags2, r2 = rr.rule_rewards(texts, passed, require_launch=True, weighted=True, w_rule=0.1,
-                                 w_exec=0.9)
+    flags2, r2 = rr.rule_rewards(texts, passed, require_launch=True, weighted=True, rule_weight=0.1,
+                                 exec_weight=0.9)
     launch = np.array([c[2] for c in CASES])
     assert np.array_equal(flags2, launch.astype(np.uint8))
     want = np.where(launch, np.float32(0.1), np.float32(0)) + np.where(passed != 0, np.float32(0.9),
