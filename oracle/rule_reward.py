@@ -9,7 +9,7 @@ an execution harness outside this library), else 0. Sec. 4 names the rule
 that is checked (the @triton.jit decorator) and a way it is gamed: a
 decorated kernel that is never launched. Sec. 4 also reports training with
 the rule-based reward *alongside* the execution reward, hence the weighted
-form w_rule * is_Triton + w_exec * test_passed offered next to Eq. 3.
+form rule_weight * is_Triton + exec_weight * test_passed offered next to Eq. 3.
 
 The check is lexical, over the bytes of the completion (no parsing of
 strings or comments beyond what is stated here):
@@ -161,15 +161,15 @@ def is_triton(t: bytes, require_launch: bool = False) -> bool:
 
 
 def rule_rewards(texts, test_passed, require_launch: bool = False, weighted: bool = False,
-                 w_rule: float = 0.0, w_exec: float = 0.0):
+                 rule_weight: float = 0.0, exec_weight: float = 0.0):
     """(is_Triton flags u8, rewards f32) for a batch of completions: Eq. 3's
-    product of the two checks, or w_rule * is_Triton + w_exec * test_passed
+    product of the two checks, or rule_weight * is_Triton + exec_weight * test_passed
     in fp32."""
     flags = np.array([is_triton(bytes(t), require_launch) for t in texts], dtype=np.uint8)
     passed = np.asarray(test_passed).astype(bool)
     if weighted:
-        r = (np.float32(w_rule) * flags.astype(np.float32) +
-             np.float32(w_exec) * passed.astype(np.float32)).astype(np.float32)
+        r = (np.float32(rule_weight) * flags.astype(np.float32) +
+             np.float32(exec_weight) * passed.astype(np.float32)).astype(np.float32)
     else:
         r = ((flags != 0) & passed).astype(np.float32)
     return flags, r
