@@ -250,7 +250,8 @@ grpo_status adamw_step(float* weight, float* exp_avg, float* exp_avg_sq, const f
  * follow; then a line "def NAME(" (blanks allowed around NAME). A launch is
  * NAME not preceded by an identifier byte, blanks, "[", a bracket-balanced
  * run, "]", blanks, "(". Strings and comments are not otherwise parsed.
- *   text        the completions' bytes, concatenated. Device.
+ *   text        the completions' bytes, concatenated; 16-byte aligned.
+ *               Device.
  *   offsets     [num_completions + 1] int64: completion b is
  *               text[offsets[b], offsets[b+1]); a decreasing pair counts as
  *               an empty completion. Device.

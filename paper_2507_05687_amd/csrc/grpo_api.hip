@@ -669,6 +669,7 @@ grpo_status triton_rule_reward(const uint8_t* text, const int64_t* offsets,
     return GRPO_ERR_PARAM;
   if (num_completions == 0) return GRPO_OK;
   if (!text || !offsets || !test_passed || !is_triton || !reward) return GRPO_ERR_NULL;
+  if (!aligned(text, 16) || !aligned(offsets, 8)) return GRPO_ERR_ALIGN;
   TRY(check_device());
   RewardArgs a;
   a.text = text;

@@ -17,18 +17,36 @@
 //   launch: the name, not preceded by an identifier byte, blanks, "[", a
 //     bracket-balanced run to the matching "]", blanks, "(".
 //
-// One wave per completion. Lanes test 64 consecutive positions at a time for
-// a decorator; each decorator found is followed up by the whole wave in text
-// order (the function after it, then a launch search over the completion with
-// one position per lane), so the result does not depend on timing.
+// One 256-thread workgroup per completion. The completion is first copied
+// into LDS (when it fits; a longer one is read from global memory by the
+// same code), so the byte-at-a-time parsing below runs at LDS latency.
+// Phase 1: each thread tests one position in 256 for a decorator and parses
+// the function after it; the names go to a list in LDS. Phase 2: all threads
+// search the completion for a launch of each name, 256 positions at a time.
+// is_Triton is an "exists" over decorators, so the order in which threads
+// find them does not change the result. If more decorated functions are
+// found than the list holds, one wave goes through all decorators in text
+// order instead.
 #include "kernels.h"
 
 namespace grpo {
 namespace {
 
-struct Text {
+// A completion: n bytes, in global memory (at t) or in the LDS copy (byte i
+// at base[i + sh], the copy 16-byte aligned and readable to a multiple of 16
+// bytes), where long scans read 16 bytes at a time.
+struct GlobalText {
+  static constexpr bool kLds = false;
   const uint8_t* t;
   int64_t n;
+  __device__ __forceinline__ uint8_t operator[](int64_t i) const { return t[i]; }
+};
+struct LdsText {
+  static constexpr bool kLds = true;
+  const uint8_t* base;
+  int64_t sh;
+  int64_t n;
+  __device__ __forceinline__ uint8_t operator[](int64_t i) const { return base[i + sh]; }
 };
 
 __device__ __forceinline__ bool is_blank(uint8_t c) { return c == ' ' || c == '\t' || c == '\r'; }
@@ -36,133 +54,237 @@ __device__ __forceinline__ bool is_ident(uint8_t c) {
   return (c >= 'a' && c <= 'z') || (c >= 'A' && c <= 'Z') || (c >= '0' && c <= '9') || c == '_';
 }
 
-__device__ int64_t skip_blanks(const Text& T, int64_t i) {
-  while (i < T.n && is_blank(T.t[i])) ++i;
+template <class T>
+__device__ __forceinline__ int64_t skip_blanks(const T& X, int64_t i) {
+  while (i < X.n && is_blank(X[i])) ++i;
   return i;
 }
 
-// index of the newline that ends the line holding i (or n)
-__device__ int64_t line_end(const Text& T, int64_t i) {
-  while (i < T.n && T.t[i] != '\n') ++i;
-  return i;
+// 0x80 in each byte of x equal to v, 0 elsewhere
+__device__ __forceinline__ uint32_t bytes_eq(uint32_t x, uint8_t v) {
+  const uint32_t t = x ^ (0x01010101u * v);
+  return ~(((t & 0x7f7f7f7fu) + 0x7f7f7f7fu) | t | 0x7f7f7f7fu);
+}
+__device__ __forceinline__ int count_eq(const u32x4& w, uint8_t v) {
+  return __builtin_popcount(bytes_eq(w[0], v)) + __builtin_popcount(bytes_eq(w[1], v)) +
+         __builtin_popcount(bytes_eq(w[2], v)) + __builtin_popcount(bytes_eq(w[3], v));
 }
 
-// T.t[i] opens a bracket pair (o, c): index just past its match, or -1
-__device__ int64_t match_close(const Text& T, int64_t i, uint8_t o, uint8_t c) {
-  int64_t depth = 0;
-  for (int64_t j = i; j < T.n; ++j) {
-    if (T.t[j] == o) {
-      ++depth;
-    } else if (T.t[j] == c) {
-      if (--depth == 0) return j + 1;
+// index of the newline that ends the line holding i (or n). In LDS, whole
+// 16-byte chunks without a newline are skipped at once.
+template <class T>
+__device__ __forceinline__ int64_t line_end(const T& X, int64_t i) {
+  if constexpr (T::kLds) {
+    for (; i < X.n && ((i + X.sh) & 15) != 0; ++i)
+      if (X[i] == '\n') return i;
+    for (; i + 16 <= X.n; i += 16) {
+      const u32x4 w = *(const u32x4*)(X.base + i + X.sh);
+      if (count_eq(w, '\n') != 0) break;
     }
+  }
+  while (i < X.n && X[i] != '\n') ++i;
+  return i;
+}
+
+// X[i] opens a bracket pair (o, c): index just past its match, or -1. In
+// LDS, a whole 16-byte chunk is skipped at once when its closing brackets
+// cannot bring the depth to 0 (depth before it > closings in it).
+template <class T>
+__device__ __forceinline__ int64_t match_close(const T& X, int64_t i, uint8_t o, uint8_t c) {
+  int64_t depth = 0;
+  while (i < X.n) {
+    if constexpr (T::kLds) {
+      if (((i + X.sh) & 15) == 0 && i + 16 <= X.n && depth > 0) {
+        const u32x4 w = *(const u32x4*)(X.base + i + X.sh);
+        const int closes = count_eq(w, c);
+        if (depth > closes) {
+          depth += count_eq(w, o) - closes;
+          i += 16;
+          continue;
+        }
+      }
+    }
+    const uint8_t b = X[i];
+    if (b == o) {
+      ++depth;
+    } else if (b == c) {
+      if (--depth == 0) return i + 1;
+    }
+    ++i;
   }
   return -1;
 }
 
 // From i: an optional parenthesised run, then blanks or a comment to the
 // newline. Start of the next line, or -1 if the line holds other text.
-__device__ int64_t finish_line(const Text& T, int64_t i) {
-  i = skip_blanks(T, i);
-  if (i < T.n && T.t[i] == '(') {
-    i = match_close(T, i, '(', ')');
+template <class T>
+__device__ __forceinline__ int64_t finish_line(const T& X, int64_t i) {
+  i = skip_blanks(X, i);
+  if (i < X.n && X[i] == '(') {
+    i = match_close(X, i, '(', ')');
     if (i < 0) return -1;
-    i = skip_blanks(T, i);
+    i = skip_blanks(X, i);
   }
-  if (i < T.n && T.t[i] != '\n' && T.t[i] != '#') return -1;
-  return line_end(T, i) + 1;
+  if (i < X.n && X[i] != '\n' && X[i] != '#') return -1;
+  return line_end(X, i) + 1;
 }
 
 constexpr char kDeco[] = "@triton.jit";
 constexpr int kDecoLen = 11;
 
-// a decorator starts at p (T.t[p] == '@' already known)
-__device__ bool decorator_at(const Text& T, int64_t p) {
-  if (p + kDecoLen > T.n) return false;
+// a decorator starts at p (X[p] == '@' already known)
+template <class T>
+__device__ __forceinline__ bool decorator_at(const T& X, int64_t p) {
+  if (p + kDecoLen > X.n) return false;
   for (int k = 1; k < kDecoLen; ++k)
-    if (T.t[p + k] != (uint8_t)kDeco[k]) return false;
+    if (X[p + k] != (uint8_t)kDeco[k]) return false;
   const int64_t q = p + kDecoLen;
-  if (q < T.n && (is_ident(T.t[q]) || T.t[q] == '.')) return false;
-  for (int64_t j = p - 1; j >= 0 && T.t[j] != '\n'; --j)
-    if (!is_blank(T.t[j])) return false;
+  if (q < X.n && (is_ident(X[q]) || X[q] == '.')) return false;
+  for (int64_t j = p - 1; j >= 0 && X[j] != '\n'; --j)
+    if (!is_blank(X[j])) return false;
   return true;
 }
 
 // name [ns, ns + nl) of the function decorated by the decorator at p
-__device__ bool decorated_name(const Text& T, int64_t p, int64_t& ns, int64_t& nl) {
-  int64_t i = finish_line(T, p + kDecoLen);
+template <class T>
+__device__ __forceinline__ bool decorated_name(const T& X, int64_t p, int64_t& ns, int64_t& nl) {
+  int64_t i = finish_line(X, p + kDecoLen);
   while (i >= 0) {
-    if (i >= T.n) return false;
-    const int64_t j = skip_blanks(T, i);
-    if (j >= T.n) return false;
-    const uint8_t c = T.t[j];
+    if (i >= X.n) return false;
+    const int64_t j = skip_blanks(X, i);
+    if (j >= X.n) return false;
+    const uint8_t c = X[j];
     if (c == '\n' || c == '#') {  // blank or comment line
-      i = line_end(T, j) + 1;
+      i = line_end(X, j) + 1;
       continue;
     }
     if (c == '@') {  // another decorator
       int64_t k = j + 1;
-      while (k < T.n && T.t[k] != '(' && T.t[k] != '\n') ++k;
-      i = (k < T.n && T.t[k] == '(') ? finish_line(T, k) : line_end(T, k) + 1;
+      while (k < X.n && X[k] != '(' && X[k] != '\n') ++k;
+      i = (k < X.n && X[k] == '(') ? finish_line(X, k) : line_end(X, k) + 1;
       continue;
     }
-    if (!(j + 3 < T.n && T.t[j] == 'd' && T.t[j + 1] == 'e' && T.t[j + 2] == 'f' &&
-          is_blank(T.t[j + 3])))
+    if (!(j + 3 < X.n && X[j] == 'd' && X[j + 1] == 'e' && X[j + 2] == 'f' && is_blank(X[j + 3])))
       return false;
-    int64_t k = skip_blanks(T, j + 3);
-    if (k >= T.n || !is_ident(T.t[k]) || (T.t[k] >= '0' && T.t[k] <= '9')) return false;
+    int64_t k = skip_blanks(X, j + 3);
+    if (k >= X.n || !is_ident(X[k]) || (X[k] >= '0' && X[k] <= '9')) return false;
     ns = k;
-    while (k < T.n && is_ident(T.t[k])) ++k;
+    while (k < X.n && is_ident(X[k])) ++k;
     nl = k - ns;
-    k = skip_blanks(T, k);
-    return k < T.n && T.t[k] == '(';
+    k = skip_blanks(X, k);
+    return k < X.n && X[k] == '(';
   }
   return false;
 }
 
-// some position holds name[...]( -- one position per lane, 64 at a time
-__device__ bool launched(const Text& T, int64_t ns, int64_t nl, int lane) {
-  for (int64_t base = 0; base < T.n; base += 64) {
-    const int64_t r = base + lane;
-    bool hit = false;
-    if (r + nl <= T.n && T.t[r] == T.t[ns] && (r == 0 || !is_ident(T.t[r - 1]))) {
-      bool eq = true;
-      for (int64_t k = 1; k < nl && eq; ++k) eq = T.t[r + k] == T.t[ns + k];
-      if (eq) {
-        const int64_t s = skip_blanks(T, r + nl);
-        if (s < T.n && T.t[s] == '[') {
-          int64_t e = match_close(T, s, '[', ']');
-          if (e >= 0) {
-            e = skip_blanks(T, e);
-            hit = e < T.n && T.t[e] == '(';
+// a launch name[...]( of the name at [ns, ns + nl) starts at r
+template <class T>
+__device__ __forceinline__ bool launch_at(const T& X, int64_t r, int64_t ns, int64_t nl) {
+  if (!(r + nl <= X.n && X[r] == X[ns] && (r == 0 || !is_ident(X[r - 1])))) return false;
+  for (int64_t k = 1; k < nl; ++k)
+    if (X[r + k] != X[ns + k]) return false;
+  const int64_t s = skip_blanks(X, r + nl);
+  if (!(s < X.n && X[s] == '[')) return false;
+  int64_t e = match_close(X, s, '[', ']');
+  if (e < 0) return false;
+  e = skip_blanks(X, e);
+  return e < X.n && X[e] == '(';
+}
+
+constexpr int kRrThreads = 256;
+constexpr int kRrLds = 128 * 1024;  // completions up to this size (less 15 bytes) go to LDS
+constexpr int kRrNames = 64;        // decorated functions listed per completion
+
+struct RrShared {
+  int count;  // decorated functions found (may exceed kRrNames)
+  int found;
+  int64_t ns[kRrNames];
+  int64_t nl[kRrNames];
+};
+
+// Eq. 3's is_Triton for the completion X, the same in every thread of the
+// workgroup.
+template <class T>
+__device__ __forceinline__ bool is_triton_block(const T& X, int require_launch, RrShared& sh) {
+  const int tid = threadIdx.x;
+  // phase 1: decorators and the functions they decorate
+  for (int64_t base = 0; base < X.n; base += kRrThreads) {
+    const int64_t p = base + tid;
+    int64_t ns = 0, nl = 0;
+    if (p < X.n && X[p] == '@' && decorator_at(X, p) && decorated_name(X, p, ns, nl)) {
+      const int slot = atomicAdd(&sh.count, 1);
+      if (slot < kRrNames) {
+        sh.ns[slot] = ns;
+        sh.nl[slot] = nl;
+      }
+    }
+  }
+  __syncthreads();
+  const int count = sh.count;
+  if (!require_launch || count == 0) return count > 0;
+  if (count <= kRrNames) {
+    // phase 2: a launch of any listed name
+    for (int i = 0; i < count; ++i) {
+      const int64_t ns = sh.ns[i], nl = sh.nl[i];
+      for (int64_t base = 0; base < X.n; base += kRrThreads)
+        if (__syncthreads_or(base + tid < X.n && launch_at(X, base + tid, ns, nl))) return true;
+    }
+    return false;
+  }
+  // too many to list: wave 0 takes the decorators in text order
+  if (tid < 64) {
+    bool found = false;
+    for (int64_t base = 0; base < X.n && !found; base += 64) {
+      const int64_t p = base + tid;
+      uint64_t m = __ballot(p < X.n && X[p] == '@' && decorator_at(X, p));
+      while (m != 0 && !found) {
+        const int64_t pp = base + (__ffsll((unsigned long long)m) - 1);
+        m &= m - 1;
+        int64_t ns = 0, nl = 0;
+        if (!decorated_name(X, pp, ns, nl)) continue;
+        for (int64_t b2 = 0; b2 < X.n; b2 += 64) {
+          if (__ballot(b2 + tid < X.n && launch_at(X, b2 + tid, ns, nl)) != 0) {
+            found = true;
+            break;
           }
         }
       }
     }
-    if (__ballot(hit) != 0) return true;
+    if (tid == 0 && found) sh.found = 1;
   }
-  return false;
+  __syncthreads();
+  return sh.found != 0;
 }
 
-__global__ void __launch_bounds__(64) k_rule_reward(RewardArgs a) {
+__global__ void __launch_bounds__(kRrThreads) k_rule_reward(RewardArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kRrLds];
+  __shared__ RrShared sh;
   const int64_t b = blockIdx.x;
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x;
   const int64_t s0 = a.offsets[b], s1 = a.offsets[b + 1];
-  const Text T{a.text + s0, s1 > s0 ? s1 - s0 : 0};
-  bool found = false;
-  for (int64_t base = 0; base < T.n && !found; base += 64) {
-    const int64_t p = base + lane;
-    const bool cand = p < T.n && T.t[p] == '@' && decorator_at(T, p);
-    uint64_t m = __ballot(cand);
-    while (m != 0 && !found) {  // decorators of this stretch, in text order
-      const int64_t pp = base + (__ffsll((unsigned long long)m) - 1);
-      m &= m - 1;
-      int64_t ns = 0, nl = 0;
-      if (!decorated_name(T, pp, ns, nl)) continue;
-      found = !a.require_launch || launched(T, ns, nl, lane);
-    }
+  const int64_t n = s1 > s0 ? s1 - s0 : 0;
+  if (tid == 0) {
+    sh.count = 0;
+    sh.found = 0;
   }
-  if (lane == 0) {
+  bool found;
+  // 16-byte aligned (text is), at most 15 bytes before s0
+  const int64_t start = s0 & ~(int64_t)15;
+  if (n + (s0 - start) <= kRrLds) {
+    // copy [start, s1) to LDS: 16-byte loads up to the last whole 16 bytes
+    // below s1, single bytes after that (nothing past s1 is read)
+    const int64_t mid = n > 0 ? (s1 & ~(int64_t)15) : start;
+    for (int64_t g = start + 16 * tid; g < mid; g += 16 * kRrThreads)
+      *(u32x4*)(lds + (g - start)) = *(const u32x4*)(a.text + g);
+    for (int64_t g = (mid > start ? mid : start) + tid; g < s1; g += kRrThreads)
+      lds[g - start] = a.text[g];
+    __syncthreads();
+    found = is_triton_block(LdsText{lds, s0 - start, n}, a.require_launch, sh);
+  } else {
+    __syncthreads();
+    found = is_triton_block(GlobalText{a.text + s0, n}, a.require_launch, sh);
+  }
+  if (tid == 0) {
     const bool passed = a.test_passed[b] != 0;
     a.is_triton[b] = found ? 1 : 0;
     a.reward[b] = a.weighted ? a.w_rule * (found ? 1.f : 0.f) + a.w_exec * (passed ? 1.f : 0.f)
@@ -173,7 +295,7 @@ __global__ void __launch_bounds__(64) k_rule_reward(RewardArgs a) {
 }  // namespace
 
 void launch_rule_reward(const RewardArgs& a, int64_t count, hipStream_t s) {
-  hipLaunchKernelGGL(k_rule_reward, dim3((unsigned)count), dim3(64), 0, s, a);
+  hipLaunchKernelGGL(k_rule_reward, dim3((unsigned)count), dim3(kRrThreads), 0, s, a);
 }
 
 }  // namespace grpo

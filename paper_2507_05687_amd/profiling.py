@@ -24,6 +24,7 @@ import os
 import sqlite3
 import subprocess
 import sys
+import tempfile
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join("paper_2507_05687_amd", "csrc")
@@ -152,7 +153,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("what", choices=["trace", "counters", "all"])
     ap.add_argument("--workload", default="fwdbwd_bf16", choices=sorted(PROFILED))
-    ap.add_argument("--raw", default=os.path.join(ROOT, "gpurun_out", "prof"))
+    ap.add_argument("--raw", default=os.path.join(tempfile.gettempdir(), "grpo_prof_raw"))
     ap.add_argument("--out", default=os.path.join(ROOT, "profiles"))
     ap.add_argument("--summarize-only", action="store_true",
                     help="rewrite the trace summary from an existing --raw directory")

@@ -303,11 +303,14 @@ def _completion(rng, target_len: int, valid: bool) -> bytes:
 def make_completions(count: int, seed: int, mean_len: int = 2000, max_len: int = 16384,
                      valid: bool = False, pass_rate: float = 0.5):
     """count seeded synthetic completions (bytes, lengths drawn around
-    mean_len up to max_len) and test_passed flags (u8). With valid=True every
-    completion is a syntactically valid Python module."""
+    mean_len, at most max_len bytes) and test_passed flags (u8). With
+    valid=True every completion is a syntactically valid Python module (and
+    may run a little past max_len)."""
     rng = np.random.default_rng(seed)
     lens = np.minimum(rng.exponential(mean_len, size=count).astype(np.int64) + 200, max_len)
     texts = [_completion(rng, int(n), valid) for n in lens]
+    if not valid:
+        texts = [t[:max_len] for t in texts]
     passed = (rng.random(count) < pass_rate).astype(np.uint8)
     return texts, passed
 

@@ -188,6 +188,8 @@ def test_rule_reward_argument_errors(lib):
     assert call(5, -1) == 4                  # weighted
     assert call(6, float("nan")) == 4
     assert call(7, float("inf")) == 4
+    assert call(0, ctypes.c_void_p(0x1008)) == 5   # text not 16-byte aligned
+    assert call(1, ctypes.c_void_p(0x1004)) == 5
     assert call(2, 0) == 0                   # nothing to do: no launch, no device needed
     assert f(NULL, NULL, 0, NULL, 0, 0, 0.0, 0.0, NULL, NULL, NULL) == 0
 

@@ -65,7 +65,15 @@ def test_edges():
         kernel.replace(b"\n", b"\r\n") + "# é ü\n".encode() + b"\x00\xff k [g]\t(1)",
         b"@triton.jit\n" * 300 + b"def k(x):\n    pass\nk[1](2)\n",  # decorators stacked
     ]
-    passed = np.array([1, 0] * 4 + [1], np.uint8)
+    # more decorated functions than the per-completion list holds
+    many = b"".join(b"@triton.jit\ndef k%d(x):\n    pass\n" % i for i in range(100))
+    texts += [many, many + b"k99[1](0)\n", many + b"k100[1](0)\n"]
+    # long bracket runs: nested, balanced and not, over lines
+    texts += [kernel + b"k[" + b"[]" * 3000 + b"](0)",
+              kernel + b"k[" + b"x]" * 50 + b"[" * 40 + b"]" * 41 + b"(1)",
+              kernel + b"k [" + b"[[]]\n" * 1000 + b"]\t(1)",
+              b"@triton.jit(" + b"(" * 100 + b")" * 101 + b"\ndef q(x):\n  pass\nq[0](1)"]
+    passed = np.array([1, 0] * 8, np.uint8)
     _check(texts, passed)
     # no completions; only empty ones
     f, r = _run([], [])
