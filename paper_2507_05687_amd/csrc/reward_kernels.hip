@@ -194,16 +194,20 @@ __device__ __forceinline__ bool launch_at(const T& X, int64_t r, int64_t ns, int
 constexpr int kRrThreads = 256;
 constexpr int kRrLds = 128 * 1024;  // completions up to this size (less 15 bytes) go to LDS
 constexpr int kRrNames = 64;        // decorated functions listed per completion
+constexpr int kRrList = 256;        // decorators / launch candidates listed per completion
 
 struct RrShared {
   int count;  // decorated functions found (may exceed kRrNames)
   int found;
+  int nlist;  // entries of `list` found (may exceed kRrList)
   int64_t ns[kRrNames];
   int64_t nl[kRrNames];
+  int64_t list[kRrList];
 };
 
 // Eq. 3's is_Triton for the completion X, the same in every thread of the
-// workgroup.
+// workgroup; each thread follows up the decorators and launch candidates it
+// finds by itself (global-memory completions, and lists that overflow).
 template <class T>
 __device__ __forceinline__ bool is_triton_block(const T& X, int require_launch, RrShared& sh) {
   const int tid = threadIdx.x;
@@ -256,6 +260,214 @@ __device__ __forceinline__ bool is_triton_block(const T& X, int require_launch, 
   return sh.found != 0;
 }
 
+// ---- wave-cooperative scans over an LDS completion: every lane of the wave
+// calls them with the same arguments and gets the same result; each lane
+// takes one 16-byte chunk, 1 KiB per step.
+
+// bit k set where byte k of the chunk w equals v
+__device__ __forceinline__ uint32_t mask16(const u32x4& w, uint8_t v) {
+  uint32_t r = 0;
+  static_for<4>([&](auto d) {
+    const uint32_t m = bytes_eq(w[d.value], v);
+    r |= (((m >> 7) & 1) | ((m >> 14) & 2) | ((m >> 21) & 4) | ((m >> 28) & 8)) << (4 * d.value);
+  });
+  return r;
+}
+// bit k set where lo <= cs + k < hi
+__device__ __forceinline__ uint32_t range16(int64_t cs, int64_t lo, int64_t hi) {
+  const int64_t a = lo - cs > 0 ? lo - cs : 0, b = hi - cs < 16 ? hi - cs : 16;
+  return b <= a ? 0u : ((1u << b) - 1u) & ~((1u << a) - 1u);
+}
+
+// first j >= i with X[j] equal to v1 or v2, else n
+__device__ int64_t wave_find(const LdsText& X, int64_t i, uint8_t v1, uint8_t v2) {
+  const int lane = threadIdx.x & 63;
+  for (int64_t c0 = ((i + X.sh) & ~(int64_t)15) - X.sh; c0 < X.n; c0 += 1024) {
+    const int64_t cs = c0 + 16 * lane;
+    uint32_t hit = 0;
+    if (cs < X.n && cs + 16 > i) {
+      const u32x4 w = *(const u32x4*)(X.base + cs + X.sh);
+      hit = (mask16(w, v1) | mask16(w, v2)) & range16(cs, i, X.n);
+    }
+    const uint64_t any = __ballot(hit != 0);
+    if (any != 0) {
+      const int l = __ffsll((unsigned long long)any) - 1;
+      const int k = __shfl(hit != 0 ? __builtin_ctz(hit) : 0, l, 64);
+      return c0 + 16 * l + k;
+    }
+  }
+  return X.n;
+}
+
+// X[i] opens a bracket pair (o, c): index just past its match, or -1. Each
+// lane takes the depth change and the lowest running depth of its chunk; a
+// prefix sum over the wave gives the depth at each chunk's start, and the
+// first chunk whose running depth reaches 0 holds the match.
+__device__ int64_t wave_match_close(const LdsText& X, int64_t i, uint8_t o, uint8_t c) {
+  const int lane = threadIdx.x & 63;
+  int carry = 0;  // depth before this step's kibibyte
+  for (int64_t c0 = ((i + X.sh) & ~(int64_t)15) - X.sh; c0 < X.n; c0 += 1024) {
+    const int64_t cs = c0 + 16 * lane;
+    int net = 0, low = 1 << 30;
+    uint32_t mo = 0, mc = 0, valid = 0;
+    if (cs < X.n && cs + 16 > i) {
+      const u32x4 w = *(const u32x4*)(X.base + cs + X.sh);
+      valid = range16(cs, i, X.n);
+      mo = mask16(w, o) & valid;
+      mc = mask16(w, c) & valid;
+      static_for<16>([&](auto k) {
+        net += (int)((mo >> k.value) & 1) - (int)((mc >> k.value) & 1);
+        if ((valid >> k.value) & 1) low = net < low ? net : low;
+      });
+    }
+    int incl = net;
+    static_for<6>([&](auto s) {
+      const int t = __shfl_up(incl, 1 << s.value, 64);
+      if (lane >= (1 << s.value)) incl += t;
+    });
+    const int before = carry + incl - net;  // depth at the start of this lane's chunk
+    const uint64_t any = __ballot(valid != 0 && before + low <= 0);
+    if (any != 0) {
+      const int l = __ffsll((unsigned long long)any) - 1;
+      int at = 0;
+      if (lane == l) {
+        int d = before;
+        for (int k = 0; k < 16; ++k) {
+          d += (int)((mo >> k) & 1) - (int)((mc >> k) & 1);
+          if (((valid >> k) & 1) && d == 0) {
+            at = k;
+            break;
+          }
+        }
+      }
+      return c0 + 16 * l + __shfl(at, l, 64) + 1;
+    }
+    carry += __shfl(incl, 63, 64);
+  }
+  return -1;
+}
+
+__device__ int64_t wave_line_end(const LdsText& X, int64_t i) { return wave_find(X, i, '\n', '\n'); }
+
+__device__ int64_t wave_finish_line(const LdsText& X, int64_t i) {
+  i = skip_blanks(X, i);
+  if (i < X.n && X[i] == '(') {
+    i = wave_match_close(X, i, '(', ')');
+    if (i < 0) return -1;
+    i = skip_blanks(X, i);
+  }
+  if (i < X.n && X[i] != '\n' && X[i] != '#') return -1;
+  return wave_line_end(X, i) + 1;
+}
+
+// decorated_name with the long scans shared by the wave
+__device__ bool wave_decorated_name(const LdsText& X, int64_t p, int64_t& ns, int64_t& nl) {
+  int64_t i = wave_finish_line(X, p + kDecoLen);
+  while (i >= 0) {
+    if (i >= X.n) return false;
+    const int64_t j = skip_blanks(X, i);
+    if (j >= X.n) return false;
+    const uint8_t c = X[j];
+    if (c == '\n' || c == '#') {
+      i = wave_line_end(X, j) + 1;
+      continue;
+    }
+    if (c == '@') {
+      const int64_t k = wave_find(X, j + 1, '(', '\n');
+      i = (k < X.n && X[k] == '(') ? wave_finish_line(X, k) : k + 1;
+      continue;
+    }
+    if (!(j + 3 < X.n && X[j] == 'd' && X[j + 1] == 'e' && X[j + 2] == 'f' && is_blank(X[j + 3])))
+      return false;
+    int64_t k = skip_blanks(X, j + 3);
+    if (k >= X.n || !is_ident(X[k]) || (X[k] >= '0' && X[k] <= '9')) return false;
+    ns = k;
+    while (k < X.n && is_ident(X[k])) ++k;
+    nl = k - ns;
+    k = skip_blanks(X, k);
+    return k < X.n && X[k] == '(';
+  }
+  return false;
+}
+
+// position of the "[" of a launch candidate name [ at r, or -1
+__device__ __forceinline__ int64_t launch_open(const LdsText& X, int64_t r, int64_t ns, int64_t nl) {
+  if (!(r + nl <= X.n && X[r] == X[ns] && (r == 0 || !is_ident(X[r - 1])))) return -1;
+  for (int64_t k = 1; k < nl; ++k)
+    if (X[r + k] != X[ns + k]) return -1;
+  const int64_t s = skip_blanks(X, r + nl);
+  return s < X.n && X[s] == '[' ? s : -1;
+}
+
+// is_Triton of an LDS completion, the same in every thread: decorators and
+// launch candidates are listed by all threads, then followed up by whole
+// waves; an overflowing list falls back to is_triton_block.
+__device__ bool is_triton_waves(const LdsText& X, int require_launch, RrShared& sh) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  constexpr int kWaves = kRrThreads / 64;
+  for (int64_t base = 0; base < X.n; base += kRrThreads) {
+    const int64_t p = base + tid;
+    if (p < X.n && X[p] == '@' && decorator_at(X, p)) {
+      const int slot = atomicAdd(&sh.nlist, 1);
+      if (slot < kRrList) sh.list[slot] = p;
+    }
+  }
+  __syncthreads();
+  const int ndeco = sh.nlist;
+  bool overflow = ndeco > kRrList;
+  if (!overflow) {
+    for (int d = wave; d < ndeco; d += kWaves) {
+      int64_t ns = 0, nl = 0;
+      if (wave_decorated_name(X, sh.list[d], ns, nl) && lane == 0) {
+        const int slot = atomicAdd(&sh.count, 1);
+        if (slot < kRrNames) {
+          sh.ns[slot] = ns;
+          sh.nl[slot] = nl;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const int count = sh.count;
+  overflow = overflow || count > kRrNames;
+  bool found = false;
+  if (!overflow && (!require_launch || count == 0)) return count > 0;
+  for (int i = 0; i < count && !overflow && !found; ++i) {
+    const int64_t ns = sh.ns[i], nl = sh.nl[i];
+    if (tid == 0) sh.nlist = 0;
+    __syncthreads();
+    for (int64_t base = 0; base < X.n; base += kRrThreads) {
+      const int64_t s = base + tid < X.n ? launch_open(X, base + tid, ns, nl) : -1;
+      if (s >= 0) {
+        const int slot = atomicAdd(&sh.nlist, 1);
+        if (slot < kRrList) sh.list[slot] = s;
+      }
+    }
+    __syncthreads();
+    const int nc = sh.nlist;
+    overflow = nc > kRrList;
+    bool hit = false;
+    if (!overflow) {
+      for (int q = wave; q < nc && !hit; q += kWaves) {
+        int64_t e = wave_match_close(X, sh.list[q], '[', ']');
+        if (e >= 0) {
+          e = skip_blanks(X, e);
+          hit = e < X.n && X[e] == '(';
+        }
+      }
+    }
+    found = __syncthreads_or(hit);
+  }
+  if (!overflow) return found;
+  __syncthreads();
+  if (tid == 0) {
+    sh.count = 0;
+    sh.found = 0;
+  }
+  __syncthreads();
+  return is_triton_block(X, require_launch, sh);
+}
+
 __global__ void __launch_bounds__(kRrThreads) k_rule_reward(RewardArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[kRrLds];
   __shared__ RrShared sh;
@@ -266,6 +478,7 @@ __global__ void __launch_bounds__(kRrThreads) k_rule_reward(RewardArgs a) {
   if (tid == 0) {
     sh.count = 0;
     sh.found = 0;
+    sh.nlist = 0;
   }
   bool found;
   // 16-byte aligned (text is), at most 15 bytes before s0
@@ -279,7 +492,7 @@ __global__ void __launch_bounds__(kRrThreads) k_rule_reward(RewardArgs a) {
     for (int64_t g = (mid > start ? mid : start) + tid; g < s1; g += kRrThreads)
       lds[g - start] = a.text[g];
     __syncthreads();
-    found = is_triton_block(LdsText{lds, s0 - start, n}, a.require_launch, sh);
+    found = is_triton_waves(LdsText{lds, s0 - start, n}, a.require_launch, sh);
   } else {
     __syncthreads();
     found = is_triton_block(GlobalText{a.text + s0, n}, a.require_launch, sh);

@@ -47,6 +47,11 @@ PROFILED = {
         source=os.path.join(CSRC, "aux_kernels.hip"),
         desc="155136 x 4096 fp32 parameters, moments and gradient, bf16 copy",
         note="the warm-up step is included"),
+    "rule_reward": dict(
+        args=["--workload", "rule_reward"], kinds={"rule_reward": "k_rule_reward"},
+        source=os.path.join(CSRC, "reward_kernels.hip"),
+        desc="8 prompts x G = 8 generated completions of up to 65,536 bytes, launch check on",
+        note="the warm-up step is included"),
 }
 COPY_BYTES = 1 << 30
 
