@@ -611,6 +611,30 @@ __global__ void __launch_bounds__(256) k_adamw(AdamArgs a) {
   }
 }
 
+// ------------------------------------------------------------ split-K sum
+__global__ void k_sum_splits(const float* __restrict__ part, int splits, int64_t stride,
+                             int64_t ld_part, float* __restrict__ out, int64_t ld_out,
+                             int64_t rows, int64_t cols, int accumulate) {
+  const int64_t total = rows * cols;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / cols, c = i - r * cols;
+    const float* p = part + r * ld_part + c;
+    float acc = p[0];
+    for (int sp = 1; sp < splits; ++sp) acc += p[sp * stride];
+    out[r * ld_out + c] = accumulate ? out[r * ld_out + c] + acc : acc;
+  }
+}
+
+void launch_sum_splits(const float* part, int splits, int64_t stride, int64_t ld_part, float* out,
+                       int64_t ld_out, int64_t rows, int64_t cols, int accumulate, hipStream_t s) {
+  const int64_t total = rows * cols;
+  if (total <= 0) return;
+  const int blocks = (int)(ceil_div(total, 256) < 16384 ? ceil_div(total, 256) : 16384);
+  hipLaunchKernelGGL(k_sum_splits, dim3(blocks), dim3(256), 0, s, part, splits, stride, ld_part,
+                     out, ld_out, rows, cols, accumulate);
+}
+
 void launch_adamw(const AdamArgs& a, hipStream_t s) {
   const int64_t n4 = a.n >> 2;
   int64_t blocks = ceil_div(n4 > 0 ? n4 : 1, 256);

@@ -324,6 +324,7 @@ struct EpiStore {
   const int32_t* out_rows;  // output row = out_rows[m] (NULL: m)
   int64_t m_limit;       // rows >= m_limit are not stored (static bound)
   int64_t n_limit;       // columns >= n_limit are not stored
+  int64_t split_stride;  // with a split K, split y writes acc_buf + y * split_stride
 
   template <int NI>
   struct Pre {};
@@ -340,7 +341,7 @@ struct EpiStore {
     const int64_t n0 = (int64_t)f.tn * kTile + f.cbase + (f.lane & 31);
     const bool full = (int64_t)f.tm * kTile + kTile <= mlim &&
                       (int64_t)f.tn * kTile + kTile <= n_limit;
-    float* pacc = acc_buf ? acc_buf + m0 * ld_acc + n0 : nullptr;
+    float* pacc = acc_buf ? acc_buf + blockIdx.y * split_stride + m0 * ld_acc + n0 : nullptr;
     // Batches of RB rows x NI columns of this lane (16 or 32 values): each
     // batch is loaded, combined and stored before the next starts, so the
     // loads of a batch are in flight together and its registers die right
@@ -463,7 +464,17 @@ __global__ void __launch_bounds__(64 * kWaves, 1) k_gemm_bf16(GemmArgs g, Epi ep
   const int n_valid = g.n_dev ? min(*g.n_dev, g.N) : g.N;
   int tm, tn;
   if (!gemm_tile(g, m_valid, n_valid, tm, tn)) return;
-  const int K = g.k_dev ? (int)round_up(*g.k_dev, kBK) : g.K;
+  // this workgroup's part of K: blocks [kb0, kb0 + K/32) of an even split
+  // over the grid's y dimension (a part past the end does no K steps)
+  int K = g.k_dev ? (int)round_up(*g.k_dev, kBK) : g.K;
+  int64_t kb0 = 0;
+  if (g.splits > 1) {
+    const int per = (int)ceil_div(K / kBK, g.splits);
+    const int first = (int)blockIdx.y * per;
+    const int cnt = K / kBK - first < per ? K / kBK - first : per;
+    kb0 = cnt > 0 ? first : 0;
+    K = cnt > 0 ? cnt * kBK : 0;
+  }
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -486,8 +497,10 @@ __global__ void __launch_bounds__(64 * kWaves, 1) k_gemm_bf16(GemmArgs g, Epi ep
   const int qrow = 16 * w + (lane >> 2);
   const int qch = (lane & 3) ^ ((qrow >> 2) & 3);  // the same for q + 128j
   // load l of step kt (l < kJ: A part l, else B part l - kJ) into stage bytes la
-  const __amdgpu_buffer_rsrc_t ra = tile_rsrc(g.A + ((int64_t)tm * g.a_kt + g.a_kb0) * kTileElems);
-  const __amdgpu_buffer_rsrc_t rb = tile_rsrc(g.B + ((int64_t)tn * g.b_kt + g.b_kb0) * kTileElems);
+  const __amdgpu_buffer_rsrc_t ra =
+      tile_rsrc(g.A + ((int64_t)tm * g.a_kt + g.a_kb0 + kb0) * kTileElems);
+  const __amdgpu_buffer_rsrc_t rb =
+      tile_rsrc(g.B + ((int64_t)tn * g.b_kt + g.b_kb0 + kb0) * kTileElems);
   const uint32_t lofs = (uint32_t)(qrow * 32 + qch * 8) * 2;
   auto load = [&](int kt, char* la, auto l) {
     const uint32_t so = (uint32_t)kt * (kTileElems * 2);
@@ -599,7 +612,17 @@ __global__ void __launch_bounds__(64 * kW4Waves, 1) k_gemm_w4(GemmArgs g, Epi ep
   const int n_valid = g.n_dev ? min(*g.n_dev, g.N) : g.N;
   int tm, tn;
   if (!gemm_tile(g, m_valid, n_valid, tm, tn)) return;
-  const int K = g.k_dev ? (int)round_up(*g.k_dev, kBK) : g.K;
+  // this workgroup's part of K: blocks [kb0, kb0 + K/32) of an even split
+  // over the grid's y dimension (a part past the end does no K steps)
+  int K = g.k_dev ? (int)round_up(*g.k_dev, kBK) : g.K;
+  int64_t kb0 = 0;
+  if (g.splits > 1) {
+    const int per = (int)ceil_div(K / kBK, g.splits);
+    const int first = (int)blockIdx.y * per;
+    const int cnt = K / kBK - first < per ? K / kBK - first : per;
+    kb0 = cnt > 0 ? first : 0;
+    K = cnt > 0 ? cnt * kBK : 0;
+  }
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -618,8 +641,10 @@ __global__ void __launch_bounds__(64 * kW4Waves, 1) k_gemm_w4(GemmArgs g, Epi ep
 
   const int qrow = 16 * w + (lane >> 2);
   const int qch = (lane & 3) ^ ((qrow >> 2) & 3);
-  const __amdgpu_buffer_rsrc_t ra = tile_rsrc(g.A + ((int64_t)tm * g.a_kt + g.a_kb0) * kTileElems);
-  const __amdgpu_buffer_rsrc_t rb = tile_rsrc(g.B + ((int64_t)tn * g.b_kt + g.b_kb0) * kTileElems);
+  const __amdgpu_buffer_rsrc_t ra =
+      tile_rsrc(g.A + ((int64_t)tm * g.a_kt + g.a_kb0 + kb0) * kTileElems);
+  const __amdgpu_buffer_rsrc_t rb =
+      tile_rsrc(g.B + ((int64_t)tn * g.b_kt + g.b_kb0 + kb0) * kTileElems);
   const uint32_t lofs = (uint32_t)(qrow * 32 + qch * 8) * 2;
   // load l of step kt (l < kW4J: A part l, else B part l - kW4J) into stage bytes la
   auto load = [&](int kt, char* la, auto l) {
@@ -711,10 +736,11 @@ constexpr bool four_waves() {
 template <class Epi>
 static void launch_gemm(const GemmArgs& g, const Epi& e, hipStream_t s) {
   int grid = gemm_grid(g.tiles_m, g.tiles_n);
+  const dim3 blocks(grid, g.splits > 1 ? g.splits : 1);
   if constexpr (four_waves<Epi>())
-    hipLaunchKernelGGL((k_gemm_w4<Epi>), dim3(grid), dim3(64 * kW4Waves), 0, s, g, e);
+    hipLaunchKernelGGL((k_gemm_w4<Epi>), blocks, dim3(64 * kW4Waves), 0, s, g, e);
   else
-    hipLaunchKernelGGL((k_gemm_bf16<Epi>), dim3(grid), dim3(64 * kWaves), 0, s, g, e);
+    hipLaunchKernelGGL((k_gemm_bf16<Epi>), blocks, dim3(64 * kWaves), 0, s, g, e);
 }
 
 void launch_gemm_lse(const GemmArgs& g, const int32_t* y_p, float* zy, float2* ms, int64_t ldms,
@@ -731,8 +757,8 @@ void launch_gemm_dz(const GemmArgs& g, const int32_t* y_p, const float* lse_p, c
 }
 
 void launch_gemm_store(const GemmArgs& g, const StoreArgs& a, bool grad_weight, hipStream_t s) {
-  EpiStore e{a.acc_buf, a.ld_acc, a.read_acc, a.out, a.ld_out, a.out_bf16, a.add_out,
-             a.out_rows, a.m_limit, a.n_limit};
+  EpiStore e{a.acc_buf, a.ld_acc,   a.read_acc, a.out,     a.ld_out,      a.out_bf16,
+             a.add_out, a.out_rows, a.m_limit,  a.n_limit, a.split_stride};
   if (grad_weight)
     launch_gemm<EpiGradWeight>(g, EpiGradWeight{e}, s);
   else

@@ -20,13 +20,13 @@ namespace {
 enum Kind {
   K_PACK, K_ADV, K_GEMM_LSE, K_LSE_FIN, K_TOKEN, K_TRANSPOSE, K_GEMM_DZ, K_GEMM_DH, K_GEMM_DW,
   K_F32_SCORE, K_F32_DH, K_F32_DW, K_ZERO_ROWS, K_GATHER_DOT, K_TILE, K_ADAMW,
-  K_RULE_REWARD, K_NUM_KINDS
+  K_RULE_REWARD, K_SUM_SPLITS, K_NUM_KINDS
 };
 const char* kKindNames[K_NUM_KINDS] = {
     "pack_valid",  "group_advantages", "gemm_logits_lse", "lse_finalize",   "token_objective",
     "transpose",   "gemm_recompute_dz", "gemm_grad_hidden", "gemm_grad_weight", "f32_score",
     "f32_grad_hidden", "f32_grad_weight", "zero_masked_rows", "gather_dot", "tile", "adamw",
-    "rule_reward"};
+    "rule_reward", "sum_splits"};
 
 struct Prof {
   std::mutex mu;
@@ -109,7 +109,7 @@ struct Layout {
   size_t lse = 0, zy = 0, logp = 0, g = 0, ms = 0, lpart = 0;
   int64_t Hk = 0;  // H rounded up to the tiled block width
   // tiled buffers and their tile-row strides in blocks
-  size_t WK = 0, hK = 0, hT = 0, WT = 0, dz = 0, dzT = 0, dhacc = 0;
+  size_t WK = 0, hK = 0, hT = 0, WT = 0, dz = 0, dzT = 0, dhacc = 0, dwpart = 0;
   int64_t sK = 0, sTok = 0, sVoc = 0, sChunk = 0;
   size_t total = 0;
 };
@@ -121,6 +121,25 @@ struct Layout {
 #define GRPO_TILE_SKEW 1
 #endif
 int64_t tile_stride(int64_t K) { return ceil_div(K, kBK) + GRPO_TILE_SKEW; }
+
+// K splits for a product of `tiles` output tiles: none when the tiles fill
+// the 256 CUs, else the count up to kMaxSplits that best fills whole rounds
+// of 256 workgroups (the smallest among equals).
+constexpr int kMaxSplits = 8;
+int dw_splits(int64_t tiles) {
+  if (tiles <= 0 || tiles >= 256) return 1;
+  int best = 1;
+  double best_fill = 0;
+  for (int sp = 1; sp <= kMaxSplits; ++sp) {
+    const int64_t wg = sp * tiles;
+    const double fill = (double)wg / (double)(256 * ceil_div(wg, 256));
+    if (fill > best_fill + 1e-9) {
+      best = sp;
+      best_fill = fill;
+    }
+  }
+  return best;
+}
 
 size_t take(size_t& cur, size_t bytes) {
   size_t at = cur;
@@ -178,6 +197,9 @@ Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_
       L.dzT = take(c, 2 * L.Vc * L.sTok * kBK);
       // fp32 dh accumulator with every row and column of every tile present
       if (L.nchunks > kDhGroup) L.dhacc = take(c, 4 * L.Npad * Hpad);
+      // dW partials of a split K (chunks too narrow to fill the GPU)
+      if (dw_splits(L.Vc / kTile * (Hpad / kTile)) > 1)
+        L.dwpart = take(c, 4 * kMaxSplits * L.Vc * Hpad);
     }
   }
   L.total = c;
@@ -225,6 +247,7 @@ GemmArgs gemm_args(const void* A, int64_t a_kt, int64_t M, const void* B, int64_
   g.k_dev = k_dev;
   g.tiles_m = (int)ceil_div(M, kTile);
   g.tiles_n = (int)ceil_div(N, kTile);
+  g.splits = 1;
   return g;
 }
 
@@ -363,17 +386,35 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
       GemmArgs gw = gemm_args(dzT, kt_tok, Mc, hT, kt_tok, H, nullptr, nullptr, 0,
                               &hdr->num_valid);
       StoreArgs sa{};
-      sa.acc_buf = nullptr;
-      sa.ld_acc = 0;
-      sa.read_acc = 0;
-      sa.out = grad_weight + v0 * H;
-      sa.ld_out = H;
       sa.out_bf16 = 0;
-      sa.add_out = accumulate_grad_weight != 0;
       sa.out_rows = nullptr;
       sa.m_limit = Mc;
       sa.n_limit = H;
-      TRY(timed(K_GEMM_DW, s, [&] { launch_gemm_store(gw, sa, true, s); }));
+      const int splits = L.dwpart ? dw_splits((int64_t)gw.tiles_m * gw.tiles_n) : 1;
+      if (splits > 1) {
+        // split K: fp32 partials per split (every row/column of every tile),
+        // then their sum into dW in split order
+        const int64_t Hpad = round_up(H, kTile);
+        gw.splits = splits;
+        sa.acc_buf = at<float>(ws, L.dwpart);
+        sa.ld_acc = Hpad;
+        sa.split_stride = L.Vc * Hpad;
+        sa.read_acc = 0;
+        sa.out = nullptr;
+        TRY(timed(K_GEMM_DW, s, [&] { launch_gemm_store(gw, sa, true, s); }));
+        TRY(timed(K_SUM_SPLITS, s, [&] {
+          launch_sum_splits(at<float>(ws, L.dwpart), splits, L.Vc * Hpad, Hpad,
+                            grad_weight + v0 * H, H, Mc, H, accumulate_grad_weight != 0, s);
+        }));
+      } else {
+        sa.acc_buf = nullptr;
+        sa.ld_acc = 0;
+        sa.read_acc = 0;
+        sa.out = grad_weight + v0 * H;
+        sa.ld_out = H;
+        sa.add_out = accumulate_grad_weight != 0;
+        TRY(timed(K_GEMM_DW, s, [&] { launch_gemm_store(gw, sa, true, s); }));
+      }
     }
     if (grad_hidden && (j == kDhGroup - 1 || last)) {
       // dh[t, :] (+)= sum_{v in group} dz[t, v] W[v, :]

@@ -19,6 +19,7 @@ struct GemmArgs {
   int K;                  // contraction length, a multiple of 32 (when k_dev is NULL)
   const int32_t* k_dev;   // optional device K, rounded up to 32 (operands zero-padded)
   int tiles_m, tiles_n;   // 256x256 tiles covering the static M x N
+  int splits;             // K split over this many workgroups per tile (grid y), 1 = none
 };
 
 struct StoreArgs {
@@ -32,6 +33,7 @@ struct StoreArgs {
   const int32_t* out_rows;
   int64_t m_limit;
   int64_t n_limit;
+  int64_t split_stride;  // with a split K: elements between the splits' acc_buf partials
 };
 
 int gemm_grid(int tiles_m, int tiles_n);
@@ -103,6 +105,10 @@ struct AdamArgs {
   float inv_sqrt_bc2;  // 1 / sqrt(1 - beta2^t)
 };
 void launch_adamw(const AdamArgs& a, hipStream_t s);
+// out[r, c] (+)= the sum over s < splits of part[s * stride + r * ld_part + c], summed in
+// split order before it is added
+void launch_sum_splits(const float* part, int splits, int64_t stride, int64_t ld_part, float* out,
+                       int64_t ld_out, int64_t rows, int64_t cols, int accumulate, hipStream_t s);
 
 // ------------------------------------------------------------ rule reward
 struct RewardArgs {
