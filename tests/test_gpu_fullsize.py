@@ -11,6 +11,8 @@ configuration bench.py times. GPU only.
 * the SFT cross-entropy workload (one 16384-token sequence, prompt prefix
   unsupervised): sampled rows' logp and dL/dh rows, the loss from the
   per-token log-probs, and the dL/dW identities.
+* the ragged workload at full size (1,048,576 padded rows): sampled rows,
+  masked rows, the dL/dW identities.
 """
 import math
 
@@ -239,3 +241,61 @@ def test_sft_full_size_sampled_rows_and_identities():
     bb = float((out["grad_hidden"].double() * hf).sum())
     assert abs(a - bb) <= 5e-3 * max(abs(a), abs(bb)), (a, bb)
 
+
+
+@pytest.mark.timeout(600)
+def test_ragged_full_size_sampled_rows_and_identities():
+    """The ragged workload at full size (16 x 8 rollouts of 256..8192 tokens
+    padded to 8192, 1,048,576 rows): the batch's narrow vocabulary chunks take
+    the column-split tile mapping and the split-K dL/dW product."""
+    w = workloads.WORKLOADS["ragged_bf16"]
+    W_bits = workloads.make_weight(w)
+    h_bits = workloads.make_hidden(w)
+    b = workloads.make_batch(w)
+    N, V, B = w.num_tokens, w.vocab, w.num_seqs
+    m = b["mask"]
+    rows = workloads.sample_rows(m, 16, seed=3)
+    Wd = oracle.decode(W_bits, "bf16")
+    hs = oracle.decode(h_bits[rows], "bf16")
+    o_lse, o_logp, _ = oracle.score_rows(hs, Wd, b["tokens"][rows])
+    base = np.full(N, -math.log(V))
+    base[rows] = o_logp
+    old = (base + b["old_noise"]).astype(np.float32)
+    ref = (base + b["ref_noise"]).astype(np.float32)
+    adv = oracle.advantages(b["rewards"], w.group).astype(np.float32)
+    hd, Wdv = to_dev(h_bits, "bf16"), to_dev(W_bits, "bf16")
+    del h_bits
+    mask_d = dev(m)
+    out = grpo.loss_fwd_bwd(hd, Wdv, dev(b["tokens"]), mask_d, dev(b["cu_seqlens"]), dev(old),
+                            dev(ref), dev(adv), w.clip_eps, w.beta, check=True)
+    torch.cuda.synchronize()
+    c, seq = _seq_weights(b, B)
+    o_ell, o_g, _ = oracle.token_objective(o_logp, old[rows], ref[rows], adv[seq[rows]],
+                                           c[seq[rows]], None, w.clip_eps, w.beta)
+    assert rel_err(host64(out["logp"])[rows], o_logp) <= TOL
+    g = host64(out["dlogp"])[rows]
+    assert np.max(np.abs(g - o_g)) <= TOL * np.max(np.abs(o_g))
+    o_dh = oracle.grad_hidden_rows(hs, Wd, b["tokens"][rows], o_lse, o_g)
+    dh = host64(out["grad_hidden"][torch.from_numpy(rows).cuda()])
+    for i in range(len(rows)):
+        if np.linalg.norm(o_dh[i]) > 0:  # rows of all-equal groups have g = 0
+            assert norm_rel(dh[i], o_dh[i]) <= GRAD_TOL, (i, norm_rel(dh[i], o_dh[i]))
+    del Wd
+    mb = mask_d.bool()
+    assert out["logp"][~mb].abs().max().item() == 0.0
+    assert out["grad_hidden"][~mb].float().abs().max().item() == 0.0
+    # dL/dW identities, as for the fwd+bwd workload (sums over rows in slices)
+    gw = out["grad_weight"]
+    gt = out["dlogp"].double()
+    colsum = gw.double().sum(0)
+    bound = torch.zeros_like(colsum)
+    bb = 0.0
+    for r0 in range(0, N, 1 << 16):
+        hc = hd[r0:r0 + (1 << 16)].double()
+        bound += (hc.abs() * gt[r0:r0 + (1 << 16)].abs()[:, None]).sum(0)
+        bb += float((out["grad_hidden"][r0:r0 + (1 << 16)].double() * hc).sum())
+    bound = 2.0 ** -7 * bound + 1e-6
+    assert torch.all(colsum.abs() <= bound), float((colsum.abs() / bound).max())
+    a = float((gw.double() * Wdv.double()).sum())
+    assert abs(a - bb) <= 5e-3 * max(abs(a), abs(bb)), (a, bb)
+    assert torch.isfinite(gw).all()
