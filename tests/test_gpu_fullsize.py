@@ -12,7 +12,8 @@ configuration bench.py times. GPU only.
   unsupervised): sampled rows' logp and dL/dh rows, the loss from the
   per-token log-probs, and the dL/dW identities.
 * the ragged workload at full size (1,048,576 padded rows): sampled rows,
-  masked rows, the dL/dW identities.
+  masked rows, the dL/dW identities; the double-scoring workload at full size
+  (N = 262144): both scorings and the loss terms of sampled rows.
 """
 import math
 
@@ -299,3 +300,45 @@ def test_ragged_full_size_sampled_rows_and_identities():
     a = float((gw.double() * Wdv.double()).sum())
     assert abs(a - bb) <= 5e-3 * max(abs(a), abs(bb)), (a, bb)
     assert torch.isfinite(gw).all()
+
+
+@pytest.mark.timeout(600)
+def test_double_scoring_full_size_sampled_rows():
+    """The two-model sequence at full size (16 x 8 x 2048 tokens, N = 262144):
+    policy and reference scoring, then the loss on the policy reusing its
+    log-sum-exp; sampled rows against the oracle and the on-policy ratio."""
+    w = workloads.WORKLOADS["double_bf16"]
+    Wp, Wr = workloads.make_weight(w, "policy"), workloads.make_weight(w, "reference")
+    h_bits, b = workloads.make_hidden(w), workloads.make_batch(w)
+    rows = workloads.sample_rows(b["mask"], 12, seed=4)
+    hs = oracle.decode(h_bits[rows], "bf16")
+    hd = to_dev(h_bits, "bf16")
+    del h_bits
+    Wpd, Wrd = to_dev(Wp, "bf16"), to_dev(Wr, "bf16")
+    y = dev(b["tokens"])
+    lp_pol, lse_pol = grpo.logprob_fwd(hd, Wpd, y)
+    lp_ref, _ = grpo.logprob_fwd(hd, Wrd, y)
+    Wpo = oracle.decode(Wp, "bf16")
+    o_lse_p, o_lp_p, _ = oracle.score_rows(hs, Wpo, b["tokens"][rows])
+    _, o_lp_r, _ = oracle.score_rows(hs, oracle.decode(Wr, "bf16"), b["tokens"][rows])
+    assert rel_err(host64(lp_pol)[rows], o_lp_p) <= TOL
+    assert rel_err(host64(lp_ref)[rows], o_lp_r) <= TOL
+    adv = oracle.advantages(b["rewards"], w.group).astype(np.float32)
+    out = grpo.loss_fwd_bwd(hd, Wpd, y, None, dev(b["cu_seqlens"]), lp_pol, lp_ref, dev(adv),
+                            w.clip_eps, w.beta, lse_in=lse_pol, check=True)
+    torch.cuda.synchronize()
+    # on policy: old = the policy's own log-prob, so rho = 1 up to the
+    # difference between the gathered z_y of the two calls (the reused-lse
+    # path takes z_y from a dot product, the scoring call from its GEMM)
+    rho = torch.exp(out["logp"].double() - lp_pol.double())
+    assert float((rho - 1).abs().max()) <= 1e-3
+    c, seq = _seq_weights(b, w.num_seqs)
+    o_ell, o_g, _ = oracle.token_objective(o_lp_p, o_lp_p, o_lp_r, adv[seq[rows]],
+                                           c[seq[rows]], None, w.clip_eps, w.beta)
+    g = host64(out["dlogp"])[rows]
+    assert np.max(np.abs(g - o_g)) <= TOL * np.max(np.abs(o_g))
+    o_dh = oracle.grad_hidden_rows(hs, Wpo, b["tokens"][rows], o_lse_p, o_g)
+    dh = host64(out["grad_hidden"][torch.from_numpy(rows).cuda()])
+    for i in range(len(rows)):
+        assert norm_rel(dh[i], o_dh[i]) <= GRAD_TOL, (i, norm_rel(dh[i], o_dh[i]))
+    assert torch.isfinite(out["grad_weight"]).all()
