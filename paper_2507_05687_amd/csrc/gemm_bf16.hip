@@ -526,8 +526,9 @@ __global__ void __launch_bounds__(64 * kWaves, 1) k_gemm_bf16(GemmArgs g, Epi ep
   static_for<2>([&](auto t) { rd_ch[t] = ((2 * t + (lane >> 5)) ^ ((fr >> 2) & 3)) << 4; });
   bf16x8 fa[2][4], fb[2][NI];
   // fragment r (A blocks first, then B blocks) of sub-step t of step kt
-  auto fread = [&](auto slot, int kt, int t, auto r) {
-    const char* base = smem + (kt % kStages) * kStage;
+  // fragment r (A blocks first, then B blocks) of sub-step t from LDS stage st
+  auto fread = [&](auto slot, auto st, int t, auto r) {
+    const char* base = smem + st.value * kStage;
     if constexpr (r.value < 4)
       fa[slot.value][r.value] = *(const bf16x8*)(base + rd_a + r.value * 32 * 64 + rd_ch[t]);
     else
@@ -535,9 +536,9 @@ __global__ void __launch_bounds__(64 * kWaves, 1) k_gemm_bf16(GemmArgs g, Epi ep
           *(const bf16x8*)(base + rd_b + (r.value - 4) * 32 * 64 + rd_ch[t]);
   };
   constexpr int kReads = 4 + NI;  // fragment reads per sub-step
-  auto fread_half = [&](auto slot, int kt, int t, auto h) {
+  auto fread_half = [&](auto slot, auto st, int t, auto h) {
     static_for<kReads>([&](auto r) {
-      if constexpr ((r.value < kReads / 2) == (h.value == 0)) fread(slot, kt, t, r);
+      if constexpr ((r.value < kReads / 2) == (h.value == 0)) fread(slot, st, t, r);
     });
   };
   auto mfma = [&](auto slot, auto m) {
@@ -556,40 +557,47 @@ __global__ void __launch_bounds__(64 * kWaves, 1) k_gemm_bf16(GemmArgs g, Epi ep
   static_for<kStages>([&](auto st) { load_step(min((int)st.value, last), st.value); });
   __builtin_amdgcn_s_waitcnt(wait_vm((kStages - 1) * kPerStep));  // step 0 has landed
   __builtin_amdgcn_s_barrier();
-  fread_half(I0{}, 0, 0, I0{});
-  fread_half(I0{}, 0, 0, I1{});
+  fread_half(I0{}, I0{}, 0, I0{});
+  fread_half(I0{}, I0{}, 0, I1{});
 
   // The instruction order is fixed by scheduling fences. Each sub-step's
   // MFMAs run on fragments read one sub-step earlier; the next sub-step's
   // reads go out right after its first two MFMAs. Step kt: sub-step 0 (with
   // the B half of step kt+4's loads), wait for step kt+1, barrier, sub-step
   // 1 (with the A half of step kt+5's loads and the reads of step kt+1).
-  // Past the end the last step is loaded again, into free stages only.
-  int nkt = 0;
-  char* nl = smem;
-  for (int kt = 0; kt < nk; ++kt) {
+  // Past the end the last step is loaded again, into free stages only. The
+  // loop is unrolled over the ring, so every LDS stage is a constant.
+  auto step = [&](int kt, auto st) {
+    constexpr int S = st.value;
+    using Nxt = std::integral_constant<int, (S + 1) % kStages>;
+    const int nkt_b = min(kt + kStages - 1, last);  // into the stage of step kt-1
     static_for<kMfmas>([&](auto m) {
       mfma(I0{}, m);
-      if constexpr (m.value < 2) fread_half(I1{}, kt, 1, std::integral_constant<int, m.value>{});
+      if constexpr (m.value < 2) fread_half(I1{}, st, 1, std::integral_constant<int, m.value>{});
       if constexpr (m.value % kSpread == kSpread - 1) {
-        if (kt > 0) load(nkt, nl, std::integral_constant<int, kJ + m.value / kSpread>{});
+        if (kt > 0)
+          load(nkt_b, smem + ((S + kStages - 1) % kStages) * kStage + w * 1024,
+               std::integral_constant<int, kJ + m.value / kSpread>{});
       }
       __builtin_amdgcn_sched_barrier(0);
     });
     __builtin_amdgcn_s_waitcnt(wait_vm(3 * kPerStep));  // step kt+1 has landed
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    nkt = min(kt + kStages, last);
-    nl = smem + (kt % kStages) * kStage + w * 1024;
+    const int nkt_a = min(kt + kStages, last);  // into the stage of step kt
     static_for<kMfmas>([&](auto m) {
       if constexpr (m.value % kSpread == kSpread - 1)
-        load(nkt, nl, std::integral_constant<int, m.value / kSpread>{});
+        load(nkt_a, smem + S * kStage + w * 1024, std::integral_constant<int, m.value / kSpread>{});
       mfma(I1{}, m);
       if constexpr (m.value == 1 || m.value == 2)
-        fread_half(I0{}, kt + 1, 0, std::integral_constant<int, m.value - 1>{});
+        fread_half(I0{}, Nxt{}, 0, std::integral_constant<int, m.value - 1>{});
       __builtin_amdgcn_sched_barrier(0);
     });
-  }
+  };
+  for (int kt0 = 0; kt0 < nk; kt0 += kStages)
+    static_for<kStages>([&](auto st) {
+      if (kt0 + st.value < nk) step(kt0 + st.value, st);
+    });
   __syncthreads();  // every load has landed before LDS is reused
 
   epi(acc, f, m_valid, n_valid, smem, pre);
