@@ -677,9 +677,10 @@ __global__ void __launch_bounds__(64 * kW4Waves, 1) k_gemm_w4(GemmArgs g, Epi ep
   static_for<2>([&](auto t) { rd_ch[t] = ((2 * t + (lane >> 5)) ^ ((fr >> 2) & 3)) << 4; });
   // fragments of one step: q = t*8 + r, r < 4 A block r, else B block r-4
   bf16x8 fs[2][16];
-  auto fread = [&](auto slot, int kt, auto q) {
+  // fragment q of a step from LDS stage st
+  auto fread = [&](auto slot, auto st, auto q) {
     constexpr int t = q.value / 8, r = q.value % 8;
-    const char* base = smem + (kt % kStages) * kStage;
+    const char* base = smem + st.value * kStage;
     if constexpr (r < 4)
       fs[slot.value][q.value] = *(const bf16x8*)(base + rd_a + r * 32 * 64 + rd_ch[t]);
     else
@@ -703,19 +704,21 @@ __global__ void __launch_bounds__(64 * kW4Waves, 1) k_gemm_w4(GemmArgs g, Epi ep
   static_for<kStages>([&](auto st) { load_step(min((int)st.value, last), st.value); });
   __builtin_amdgcn_s_waitcnt(wait_vm((kStages - 1) * kPerStep));  // step 0 has landed
   __builtin_amdgcn_s_barrier();
-  static_for<16>([&](auto q) { fread(I0{}, 0, q); });
+  static_for<16>([&](auto q) { fread(I0{}, I0{}, q); });
   __builtin_amdgcn_s_waitcnt(wait_vm((kStages - 2) * kPerStep));  // step 1 has landed
   __builtin_amdgcn_s_barrier();  // and every wave holds step 0: its stage is free
 
-  // step kt from register set `cur`; reads step kt+1 into the other set;
-  // loads step kt+5 into the stage of step kt (free since the last barrier)
-  auto step = [&](int kt, auto cur) {
+  // step kt (in LDS stage st) from register set `cur`; reads step kt+1 into
+  // the other set; loads step kt+5 into the stage of step kt (free since the
+  // last barrier)
+  auto step = [&](int kt, auto cur, auto st) {
     using Nxt = std::integral_constant<int, cur.value ^ 1>;
+    using StNxt = std::integral_constant<int, (st.value + 1) % kStages>;
     const int nkt = min(kt + kStages, last);
-    char* nl = smem + (kt % kStages) * kStage + w * 1024;
+    char* nl = smem + st.value * kStage + w * 1024;
     static_for<kMfmas>([&](auto m) {
       mfma(cur, m);
-      if constexpr (m.value < 16) fread(Nxt{}, kt + 1, m);
+      if constexpr (m.value < 16) fread(Nxt{}, StNxt{}, m);
       if constexpr (m.value % kSpread == kSpread - 1)
         load(nkt, nl, std::integral_constant<int, m.value / kSpread>{});
       __builtin_amdgcn_sched_barrier(0);
@@ -725,12 +728,13 @@ __global__ void __launch_bounds__(64 * kW4Waves, 1) k_gemm_w4(GemmArgs g, Epi ep
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
   };
-  int kt = 0;
-  for (; kt + 1 < nk; kt += 2) {
-    step(kt, I0{});
-    step(kt + 1, I1{});
-  }
-  if (kt < nk) step(kt, I0{});
+  // unrolled over both register sets and the ring: every stage is a constant
+  for (int kt0 = 0; kt0 < nk; kt0 += 2 * kStages)
+    static_for<2 * kStages>([&](auto u) {
+      if (kt0 + u.value < nk)
+        step(kt0 + u.value, std::integral_constant<int, u.value % 2>{},
+             std::integral_constant<int, u.value % kStages>{});
+    });
   __syncthreads();  // every load has landed before LDS is reused
 
   epi(acc, f, m_valid, n_valid, smem, pre);
