@@ -303,7 +303,7 @@ struct EpiDz {
             constexpr int r = q * 4 + e;
             constexpr int o = mi * 32 + q * 8 + e;
             const float p = __builtin_amdgcn_exp2f(fmaf(acc[mi][ni][r], kLog2e, -l2));
-            const float dv = g * ((o == y ? 1.f : 0.f) - p);
+            const float dv = g * (0.f - p);  // the sampled id's entry is redone below
             d[e] = (Full::value || o < vlim) ? dv : 0.f;
           });
           const uint32_t w0 = bf16_pack2(d[0], d[1]), w1 = bf16_pack2(d[2], d[3]);
@@ -311,6 +311,21 @@ struct EpiDz {
               make_uint2(w0, w1);
         });
       });
+      // dz at the sampled id: g * (1 - p), written over its staged entry by
+      // the one lane that holds it (row offsets o < 128 with o & 4 == 0)
+      if ((unsigned)y < 128u && (y & 4) == 0) {
+        static_for<4>([&](auto mi) {
+          static_for<16>([&](auto r) {
+            constexpr int q = r / 4, e = r % 4;
+            constexpr int o = mi * 32 + q * 8 + e;
+            if (o == y) {
+              const float p = __builtin_amdgcn_exp2f(fmaf(acc[mi][ni][r.value], kLog2e, -l2));
+              *(uint16_t*)(stage + mi * (NI * 2048) + tl * 64 + (stage_chunk(tl, q) << 4) +
+                           hi * 2 + e * 2) = bf16_bits(g * (1.f - p));
+            }
+          });
+        });
+      }
     });
   }
 };
