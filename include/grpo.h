@@ -175,6 +175,8 @@ grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weig
  *   grad_weight [V, H] fp32: overwritten, or added to when
  *               accumulate_grad_weight != 0.
  * workspace >= grpo_workspace_bytes(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, num_seqs).
+ * Sizes as grpo_logprob_fwd, and for bf16 N <= 2^22 (4,194,304 rows per call;
+ * larger batches are split by the caller, accumulating grad_weight).
  */
 grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight,
                               const int64_t* tokens, const uint8_t* mask,
@@ -204,7 +206,7 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
  *   grad_hidden, grad_hidden_dt, grad_weight, accumulate_grad_weight
  *               as grpo_loss_fwd_bwd (either gradient may be NULL).
  * workspace >= grpo_workspace_bytes(GRPO_OP_SFT_FWD_BWD, dt, N, H, V, 1).
- * Errors as grpo_loss_fwd_bwd (a token id outside [0, V) sets the flag that
+ * Sizes and errors as grpo_loss_fwd_bwd (a token id outside [0, V) sets the flag that
  * grpo_check_error reports).
  */
 grpo_status sft_ce_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight,

@@ -222,6 +222,14 @@ grpo_status check_sizes(grpo_dtype dt, int64_t N, int64_t H, int64_t V) {
   return GRPO_OK;
 }
 
+// The bf16 backward: dL/dW contracts over the tokens, and the MFMA loop
+// addresses its K steps (16 KiB each) with a 32-bit offset.
+constexpr int64_t kMaxBwdTokens = 1ll << 22;
+grpo_status check_bwd_sizes(grpo_dtype dt, int64_t N, int64_t H, int64_t V) {
+  TRY(check_sizes(dt, N, H, V));
+  return dt == GRPO_BF16 && N > kMaxBwdTokens ? GRPO_ERR_SHAPE : GRPO_OK;
+}
+
 grpo_status check_ws(void* ws, size_t bytes, const Layout& L) {
   if (ws == nullptr) return GRPO_ERR_WORKSPACE;
   if (!aligned(ws, kAlign)) return GRPO_ERR_WORKSPACE;
@@ -471,6 +479,7 @@ size_t grpo_workspace_bytes(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int
   if (op != GRPO_OP_LOGPROB_FWD && op != GRPO_OP_LOSS_FWD_BWD && op != GRPO_OP_SFT_FWD_BWD)
     return 0;
   if (check_sizes(dt, N, H, V) != GRPO_OK || num_seqs < 1) return 0;
+  if (op != GRPO_OP_LOGPROB_FWD && check_bwd_sizes(dt, N, H, V) != GRPO_OK) return 0;
   if (op == GRPO_OP_SFT_FWD_BWD) return layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, 1).total;
   return layout(op, dt, N, H, V, num_seqs).total;
 }
@@ -535,7 +544,7 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
                               void* grad_hidden, grpo_dtype grad_hidden_dt, float* grad_weight,
                               int32_t accumulate_grad_weight, void* workspace,
                               size_t workspace_bytes, hipStream_t stream) {
-  TRY(check_sizes(dt, N, H, V));
+  TRY(check_bwd_sizes(dt, N, H, V));
   if (!hidden || !weight || !tokens || !cu_seqlens || !old_logp || !adv || !loss)
     return GRPO_ERR_NULL;
   if (num_seqs < 1 || num_seqs > N) return GRPO_ERR_SHAPE;
@@ -626,7 +635,7 @@ grpo_status sft_ce_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight
                            grpo_dtype grad_hidden_dt, float* grad_weight,
                            int32_t accumulate_grad_weight, void* workspace,
                            size_t workspace_bytes, hipStream_t stream) {
-  TRY(check_sizes(dt, N, H, V));
+  TRY(check_bwd_sizes(dt, N, H, V));
   if (!hidden || !weight || !tokens || !loss) return GRPO_ERR_NULL;
   if (grad_hidden && grad_hidden_dt != GRPO_F32 && grad_hidden_dt != GRPO_BF16)
     return GRPO_ERR_DTYPE;

@@ -68,6 +68,12 @@ def test_workspace_bytes(lib):
     assert ws(2, 1, 100, 60, 1000, 1) == 0
     # full-size loss workspace stays well inside one MI355X's 288 GB
     assert ws(1, 1, 131072, 4096, 155136, 64) < 32 << 30
+    # the bf16 backward takes at most 2^22 rows per call (the scoring alone more)
+    assert ws(1, 1, 1 << 22, 64, 1000, 1) > 0 and ws(2, 1, 1 << 22, 64, 1000, 1) > 0
+    assert ws(1, 1, (1 << 22) + 1, 64, 1000, 1) == 0
+    assert ws(2, 1, (1 << 22) + 1, 64, 1000, 1) == 0
+    assert ws(0, 1, (1 << 22) + 1, 64, 1000, 1) > 0
+    assert ws(1, 0, (1 << 22) + 1, 64, 1000, 1) > 0
 
 
 NULL = None
@@ -88,6 +94,7 @@ def test_loss_argument_errors(lib):
     assert _loss(lib, loss=NULL) == 1
     assert _loss(lib, beta=0.1, ref=NULL) == 1
     assert _loss(lib, N=0) == 2
+    assert _loss(lib, N=(1 << 22) + 1) == 2
     assert _loss(lib, H=60) == 2
     assert _loss(lib, B=0) == 2
     assert _loss(lib, B=9) == 2
@@ -136,6 +143,7 @@ def test_sft_argument_errors(lib):
     assert _sft(lib, tokens=NULL) == 1
     assert _sft(lib, loss=NULL) == 1
     assert _sft(lib, N=0) == 2
+    assert _sft(lib, N=(1 << 22) + 1) == 2
     assert _sft(lib, H=60) == 2
     assert _sft(lib, dt=4) == 3
     assert _sft(lib, gh=P, gh_dt=7) == 3
