@@ -136,8 +136,9 @@ grpo_status grpo_pack_valid(const uint8_t* mask, const int64_t* cu_seqlens, int6
  *   logp, lse [N] fp32 outputs (0 on masked rows). Either may be NULL.
  *   workspace >= grpo_workspace_bytes(GRPO_OP_LOGPROB_FWD, dt, N, H, V, 1),
  *             256-byte aligned.
- * Requires N, H, V >= 1, N < 2^31, V < 2^31; bf16 also needs H % 8 == 0 and
- * 16-byte aligned hidden/weight.
+ * Requires N, H, V >= 1, N < 2^31, V < 2^31, H < 2^20; bf16 also needs
+ * H % 8 == 0, (ceil(V/256) + 32) * ceil(N/256) < 2^31 and 16-byte aligned
+ * hidden/weight; fp32 needs H <= 8192. fp32 arrays are 4-byte aligned.
  */
 grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weight,
                              const int64_t* tokens, const uint8_t* mask, int64_t N, int64_t H,

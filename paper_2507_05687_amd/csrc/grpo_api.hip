@@ -219,6 +219,9 @@ grpo_status check_sizes(grpo_dtype dt, int64_t N, int64_t H, int64_t V) {
   if (N >= (1ll << 31) - kTile || V >= (1ll << 31) - kTile || H >= (1ll << 20)) return GRPO_ERR_SHAPE;
   if (dt == GRPO_BF16 && H % 8 != 0) return GRPO_ERR_SHAPE;
   if (dt == GRPO_F32 && H > 8192) return GRPO_ERR_SHAPE;  // two LDS rows of H floats
+  // the scoring product's grid (whole bands of 32 tile-rows) counts in 32 bits
+  if (dt == GRPO_BF16 && (ceil_div(V, kTile) + 32) * ceil_div(N, kTile) >= (1ll << 31))
+    return GRPO_ERR_SHAPE;
   return GRPO_OK;
 }
 
@@ -561,6 +564,9 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
     return GRPO_ERR_ALIGN;
   if ((grad_hidden && !aligned(grad_hidden, 4)) || (grad_weight && !aligned(grad_weight, 4)))
     return GRPO_ERR_ALIGN;
+  for (const void* p : {(const void*)ref_logp, (const void*)lse_in, (const void*)logp_out,
+                        (const void*)lse_out, (const void*)token_loss, (const void*)dlogp})
+    if (p && !aligned(p, 4)) return GRPO_ERR_ALIGN;
   Layout L = layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, num_seqs);
   TRY(check_ws(workspace, workspace_bytes, L));
   TRY(check_device());

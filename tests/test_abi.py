@@ -107,6 +107,8 @@ def test_loss_argument_errors(lib):
     assert _loss(lib, beta=float("nan")) == 4
     assert _loss(lib, agg=3) == 4
     assert _loss(lib, hidden=ctypes.c_void_p(0x1008)) == 5
+    for k in ("ref", "lse_in", "logp", "lse", "tl", "dlogp", "gw"):
+        assert _loss(lib, **{k: ctypes.c_void_p(0x1002)}) == 5, k
     assert _loss(lib) == 6                          # no workspace
     assert _loss(lib, ws=ctypes.c_void_p(0x1010), ws_bytes=1 << 40) == 6  # misaligned
     assert _loss(lib, ws=P, ws_bytes=16) == 6       # too small
@@ -124,6 +126,9 @@ def test_other_entry_point_errors(lib):
     assert fwd(1, P, P, P, NULL, 8, 64, 0, P, P, P, 1 << 30, NULL) == 2
     assert fwd(2, P, P, P, NULL, 8, 64, 100, P, P, P, 1 << 30, NULL) == 3
     assert fwd(1, P, P, P, NULL, 8, 64, 100, P, P, P, 8, NULL) == 6
+    # bf16 scoring grid beyond 32 bits; fp32 H beyond its LDS rows
+    assert fwd(1, P, P, P, NULL, 1 << 22, 8, (1 << 31) - 512, P, P, P, 1 << 30, NULL) == 2
+    assert fwd(0, P, P, P, NULL, 8, 8200, 100, P, P, P, 1 << 30, NULL) == 2
     pk = lib.grpo_pack_valid
     assert pk(NULL, NULL, 2, 8, P, P, P, P, 1 << 30, NULL) == 1
     assert pk(NULL, P, 0, 8, P, P, P, P, 1 << 30, NULL) == 2
