@@ -89,7 +89,7 @@ grpo_status check_device() {
 // --------------------------------------------------------- workspace
 constexpr size_t kAlign = 256;
 #ifndef GRPO_DZ_BUDGET_GIB
-#define GRPO_DZ_BUDGET_GIB 12
+#define GRPO_DZ_BUDGET_GIB 48
 #endif
 #ifndef GRPO_VC_MAX
 #define GRPO_VC_MAX 8192
@@ -122,18 +122,19 @@ struct Layout {
 #endif
 int64_t tile_stride(int64_t K) { return ceil_div(K, kBK) + GRPO_TILE_SKEW; }
 
-// K splits for a product of `tiles` output tiles: none when the tiles fill
-// the 256 CUs, else the count up to kMaxSplits that best fills whole rounds
-// of 256 workgroups (the smallest among equals).
+// K splits for a product of `tiles` output tiles: the count up to kMaxSplits
+// that best fills whole rounds of 256 workgroups (one per CU), taking more
+// splits only for at least 2% more fill (each adds a pass over fp32
+// partials). 512 tiles stay whole; 336 (a 5376-row chunk at H = 4096) take 3.
 constexpr int kMaxSplits = 8;
 int dw_splits(int64_t tiles) {
-  if (tiles <= 0 || tiles >= 256) return 1;
+  if (tiles <= 0) return 1;
   int best = 1;
   double best_fill = 0;
   for (int sp = 1; sp <= kMaxSplits; ++sp) {
     const int64_t wg = sp * tiles;
     const double fill = (double)wg / (double)(256 * ceil_div(wg, 256));
-    if (fill > best_fill + 1e-9) {
+    if (fill > best_fill + (sp == 1 ? 0.0 : 0.02)) {
       best = sp;
       best_fill = fill;
     }

@@ -37,6 +37,21 @@ PROFILED = {
         args=[], kinds=GEMM_KINDS, source=os.path.join(CSRC, "gemm_bf16.hip"),
         desc="N=131072, H=4096, V=155136, bf16",
         note="the warm-up step and the setup scoring call are included: 5 scoring launches"),
+    "fwd_bf16": dict(
+        args=["--workload", "fwd_bf16"], kinds=GEMM_KINDS,
+        source=os.path.join(CSRC, "gemm_bf16.hip"),
+        desc="log-prob scoring only, N=32768, H=4096, V=155136, bf16",
+        note="the warm-up step and the setup scoring call are included: 5 scoring launches"),
+    "ragged_bf16": dict(
+        args=["--workload", "ragged_bf16"], kinds=GEMM_KINDS,
+        source=os.path.join(CSRC, "gemm_bf16.hip"),
+        desc="16 prompts x G = 8, lengths U{256..8192} padded to 8192, H=4096, V=155136, bf16",
+        note="the warm-up step and the setup scoring call are included: 5 scoring launches"),
+    "double_bf16": dict(
+        args=["--workload", "double_bf16"], kinds=GEMM_KINDS,
+        source=os.path.join(CSRC, "gemm_bf16.hip"),
+        desc="policy and reference scoring then loss fwd+bwd, N=262144, H=4096, V=155136, bf16",
+        note="the warm-up step and the setup scoring call are included: 9 scoring launches"),
     "sft_bf16": dict(
         args=["--workload", "sft_bf16"], kinds=GEMM_KINDS,
         source=os.path.join(CSRC, "gemm_bf16.hip"),

@@ -163,6 +163,8 @@ SMALL = {
     "multi_chunk": dict(prompts=2, group=4, seq_len=40, hidden=128, vocab=40000),
     # smallest shapes
     "tiny": dict(prompts=1, group=2, seq_len=3, hidden=8, vocab=5),
+    # dL/dW of 21 x 16 = 336 tiles: K split in 3 to fill whole rounds of 256 CUs
+    "split_rounds": dict(prompts=2, group=4, seq_len=40, hidden=4096, vocab=5376),
 }
 
 
