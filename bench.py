@@ -51,7 +51,8 @@ def _gemm_flops(kind: str, w, n_valid: int, vc_sizes: list[int]) -> float:
 
 def _traffic_from_profiles(kernel: str, workload: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary of this
-    workload, if it was taken on the current source of its kernels; else None."""
+    workload, if it was taken on the current source of its kernels and of the
+    host code that sizes their launches; else None."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
@@ -59,9 +60,13 @@ def _traffic_from_profiles(kernel: str, workload: str):
         import hashlib
 
         rec = json.load(open(path))
-        src = open(os.path.join(ROOT, *rec["source"].split("/")), "rb").read()
-        if rec.get("source_sha256") != hashlib.sha256(src).hexdigest():
+        shas = rec.get("sources_sha256") or {}
+        if not shas:
             return None
+        for rel, sha in shas.items():
+            src = open(os.path.join(ROOT, *rel.split("/")), "rb").read()
+            if sha != hashlib.sha256(src).hexdigest():
+                return None
         if rec.get("workload") != workload:
             return None
         return rec.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")

@@ -10,8 +10,8 @@ WRITE_SIZE (one counter pass each) over one benchmark step and over a plain
 must move / what the counter reports), and the workload's main kernels'
 readings, scaled by that factor, give their HBM bytes per launch. Raw
 rocprofv3 output stays in --raw; the text summaries and traffic_W.json (with
-the SHA-256 of the kernels' source, so that a stale record is never used) go
-to --out.
+the SHA-256 of the kernels' source and of the host code that sizes their
+launches, so that a stale record is never used) go to --out.
 """
 from __future__ import annotations
 
@@ -69,6 +69,8 @@ PROFILED = {
         note="the warm-up step is included"),
 }
 COPY_BYTES = 1 << 30
+# the host code that chooses chunk sizes, splits and grids of every launch
+HOST_SOURCE = os.path.join(CSRC, "grpo_api.hip")
 
 
 def _run(cmd: list[str], log: str, limit: int):
@@ -99,6 +101,15 @@ def source_sha(rel: str) -> str:
     return hashlib.sha256(open(os.path.join(ROOT, rel), "rb").read()).hexdigest()
 
 
+def sources_sha(cfg: dict) -> dict:
+    """SHA-256 of the workload's kernel source and of the host launch code."""
+    return {rel.replace(os.sep, "/"): source_sha(rel) for rel in (cfg["source"], HOST_SOURCE)}
+
+
+def sha_lines(cfg: dict) -> list[str]:
+    return [f"# source sha256 ({os.path.basename(k)}): {v}" for k, v in sources_sha(cfg).items()]
+
+
 def trace(wl: str, raw: str, out: str, run: bool = True):
     cfg = PROFILED[wl]
     d = os.path.join(raw, f"trace_{wl}")
@@ -112,7 +123,7 @@ def trace(wl: str, raw: str, out: str, run: bool = True):
              "# command: " + " ".join(["rocprofv3", "--kernel-trace", "--stats", "-d", "<raw>",
                                       "-o", "bench", "--", "python", *bench]),
              f"# ({cfg['note']})",
-             f"# source sha256 ({os.path.basename(cfg['source'])}): {source_sha(cfg['source'])}",
+             *sha_lines(cfg),
              f"{'calls':>6} {'total_ms':>10} {'avg_ms':>9} {'pct':>6}  kernel"]
     for name, calls, tot, avg, pct in rows:
         if pct < 0.01:
@@ -141,16 +152,14 @@ def counters(wl: str, raw: str, out: str):
     kib = COPY_BYTES / 1024
     f_scale = kib / (sum(copy_f) / len(copy_f))
     w_scale = kib / (sum(copy_w) / len(copy_w))
-    sha = source_sha(cfg["source"])
     cmd = f"python -m paper_2507_05687_amd.profiling counters --workload {wl}"
-    rec = {"workload": wl, "source": cfg["source"].replace(os.sep, "/"), "source_sha256": sha,
-           "fetch_scale": f_scale, "write_scale": w_scale, "command": cmd, "kernels": {}}
+    rec = {"workload": wl, "sources_sha256": sources_sha(cfg), "fetch_scale": f_scale, "write_scale": w_scale, "command": cmd, "kernels": {}}
     lines = [f"# HBM traffic per launch, workload {wl}, from rocprofv3 --pmc FETCH_SIZE and "
              f"--pmc WRITE_SIZE (one pass each) over `python {' '.join(bench)}`",
              "# calibration: `python bench.py --copy-calibration` (1 GiB device copy): "
              f"FETCH_SIZE x{f_scale:.4f}, WRITE_SIZE x{w_scale:.4f} to reach the bytes it moves",
              f"# command: {cmd}",
-             f"# source sha256 ({os.path.basename(cfg['source'])}): {sha}",
+             *sha_lines(cfg),
              f"{'kind':22s} {'launches':>8} {'fetch_GB':>10} {'write_GB':>10} {'total_GB':>10}"]
     for kind, sym in cfg["kinds"].items():
         f = [v for k, v in res["FETCH_SIZE"][0].items() if sym in k]
