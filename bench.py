@@ -49,11 +49,11 @@ def _gemm_flops(kind: str, w, n_valid: int, vc_sizes: list[int]) -> float:
     return 0.0
 
 
-def _traffic_from_profiles(kernel: str, workload: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary of this
-    workload, if it was taken on the current source of its kernels and of the
-    host code that sizes their launches; else None."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+def _profile_record(prefix: str, workload: str):
+    """The committed rocprofv3 summary profiles/<prefix>_<workload>.json, if it
+    was taken on the current source of its kernels and of the host code that
+    sizes their launches; else None."""
+    path = os.path.join(ROOT, "profiles", f"{prefix}_{workload}.json")
     if not os.path.exists(path):
         return None
     try:
@@ -61,17 +61,29 @@ def _traffic_from_profiles(kernel: str, workload: str):
 
         rec = json.load(open(path))
         shas = rec.get("sources_sha256") or {}
-        if not shas:
+        if not shas or rec.get("workload") != workload:
             return None
         for rel, sha in shas.items():
             src = open(os.path.join(ROOT, *rel.split("/")), "rb").read()
             if sha != hashlib.sha256(src).hexdigest():
                 return None
-        if rec.get("workload") != workload:
-            return None
-        return rec.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")
+        return rec
     except Exception:
         return None
+
+
+def _traffic_from_profiles(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the counter summary, or None."""
+    rec = _profile_record("traffic", workload)
+    return rec and rec.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")
+
+
+def _mfma_from_profiles(kernel: str, workload: str):
+    """(MFMA-busy fraction, executed bf16 flops per launch) of `kernel` from the
+    MFMA counter summary, or (None, None)."""
+    rec = _profile_record("mfma", workload)
+    k = (rec or {}).get("kernels", {}).get(kernel, {})
+    return k.get("mfma_busy"), k.get("mfma_flops_per_launch")
 
 
 def cpu_baseline(w, W_bits, h_bits, batch, adv, old, ref, sample_tokens: int):
@@ -395,10 +407,17 @@ def main():
     flops = _gemm_flops(kind, w, n_valid, []) * args.steps
     achieved = flops / (kms / 1e3) / 1e12 if flops else None
     traffic = _traffic_from_profiles(kind, w.name)
+    busy, exe_flops = _mfma_from_profiles(kind, w.name)
     roofline = {"kernel": kind, "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": (achieved / PEAK_BF16_TFLOPS) if achieved else None,
                 "traffic": traffic, "launches_per_step": launches / args.steps,
-                "avg_launch_ms": kms / launches}
+                "avg_launch_ms": kms / launches,
+                # rocprofv3 counters of the same kernel (profiles/mfma_<workload>.json):
+                # bf16 MFMA flops it executes per launch over this run's launch time, and
+                # the fraction of SIMD cycles its MFMA units were busy
+                "executed_frac_counters": (exe_flops / (kms / launches / 1e3) /
+                                           (PEAK_BF16_TFLOPS * 1e12)) if exe_flops else None,
+                "mfma_busy_counters": busy}
     per_tok = {"fwd_bf16": 2, "fwdbwd_bf16": 6, "ragged_bf16": 6, "double_bf16": 8,
                "sft_bf16": 6}[args.workload]
     executed = {"fwd_bf16": 2, "fwdbwd_bf16": 8, "ragged_bf16": 8, "double_bf16": 10,

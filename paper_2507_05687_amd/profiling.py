@@ -2,13 +2,19 @@
 
     python -m paper_2507_05687_amd.profiling trace    [--workload W] [--raw DIR] [--out DIR]
     python -m paper_2507_05687_amd.profiling counters [--workload W] [--raw DIR] [--out DIR]
+    python -m paper_2507_05687_amd.profiling mfma     [--workload W] [--raw DIR] [--out DIR]
 
 `trace` runs ``rocprofv3 --kernel-trace --stats`` over ``bench.py --workload W``
 and writes a per-kernel duration table. `counters` takes FETCH_SIZE and
 WRITE_SIZE (one counter pass each) over one benchmark step and over a plain
 1 GiB device copy; the copy's readings calibrate the counters (bytes the copy
 must move / what the counter reports), and the workload's main kernels'
-readings, scaled by that factor, give their HBM bytes per launch. Raw
+readings, scaled by that factor, give their HBM bytes per launch. `mfma`
+takes GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES and SQ_INSTS_VALU_MFMA_MOPS_BF16
+in one pass over one step: per GEMM launch the bf16 MFMA flops executed (512
+per MOP), the fraction of SIMD cycles with the MFMA unit busy, the clock, and
+the executed flops over the launch's duration in the trace run (no counters)
+against the bf16 peak. Raw
 rocprofv3 output stays in --raw; the text summaries and traffic_W.json (with
 the SHA-256 of the kernels' source and of the host code that sizes their
 launches, so that a stale record is never used) go to --out.
@@ -69,6 +75,9 @@ PROFILED = {
         note="the warm-up step is included"),
 }
 COPY_BYTES = 1 << 30
+PEAK_BF16 = 2.5e15  # MI355X dense bf16 MFMA, flop/s
+SIMDS = 256 * 4
+XCDS = 8
 # the host code that chooses chunk sizes, splits and grids of every launch
 HOST_SOURCE = os.path.join(CSRC, "grpo_api.hip")
 
@@ -178,9 +187,73 @@ def counters(wl: str, raw: str, out: str):
     print("\n".join(lines))
 
 
+def _trace_avg_ms(raw: str, wl: str, sym: str):
+    """Average duration (ms) of the kernels matching sym in the trace run, if present."""
+    d = os.path.join(raw, f"trace_{wl}")
+    if not glob.glob(os.path.join(d, "*_results.db")):
+        return None
+    n = t = 0.0
+    for name, calls, tot in _db(d).execute("select name, total_calls, total_duration "
+                                           "from top_kernels"):
+        if sym in name:
+            n += calls
+            t += tot
+    return t / n / 1e3 if n else None  # top_kernels reports microseconds
+
+
+def mfma(wl: str, raw: str, out: str):
+    cfg = PROFILED[wl]
+    bench = ["bench.py", *cfg["args"], "--steps", "1", "--warmup", "0", "--cpu-sample", "0"]
+    names = ["GRBM_GUI_ACTIVE", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16"]
+    d = os.path.join(raw, f"pmc_{wl}_mfma")
+    _run(["rocprofv3", "--pmc", *names, "-d", d, "-o", "bench", "--", sys.executable, *bench],
+         os.path.join(raw, f"pmc_{wl}_mfma.log"), 600)
+    c = _db(d)
+    cols = [r[1] for r in c.execute("pragma table_info(counters_collection)")]
+    ki, ni, vi = cols.index("kernel_name"), cols.index("counter_name"), cols.index("value")
+    di, si, ei = cols.index("dispatch_id"), cols.index("start"), cols.index("end")
+    per = collections.defaultdict(dict)  # (kernel, dispatch) -> counter -> value
+    dur = {}
+    for r in c.execute("select * from counters_collection"):
+        per[(r[ki], r[di])][r[ni]] = float(r[vi])
+        dur[(r[ki], r[di])] = (r[ei] - r[si]) / 1e9
+    cmd = f"python -m paper_2507_05687_amd.profiling mfma --workload {wl}"
+    rec = {"workload": wl, "sources_sha256": sources_sha(cfg), "command": cmd, "kernels": {}}
+    lines = [f"# MFMA counters per launch, workload {wl}, from one rocprofv3 --pmc "
+             f"{' '.join(names)} pass over `python {' '.join(bench)}`",
+             "# flops = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16; busy = SQ_VALU_MFMA_BUSY_CYCLES / "
+             f"(GRBM_GUI_ACTIVE / {XCDS} x {SIMDS} SIMDs); clock = GRBM_GUI_ACTIVE / {XCDS} / "
+             "duration (counters on); frac = flops / trace duration / 2.5 PFLOP/s",
+             f"# command: {cmd}",
+             *sha_lines(cfg),
+             f"{'kind':22s} {'launches':>8} {'TFLOP/launch':>12} {'busy':>6} {'GHz':>5} "
+             f"{'trace_ms':>9} {'frac':>6}"]
+    for kind, sym in cfg["kinds"].items():
+        keys = [k for k in per if sym in k[0]]
+        if not keys:
+            continue
+        avg = {n: sum(per[k].get(n, 0.0) for k in keys) / len(keys) for n in names}
+        gui = avg["GRBM_GUI_ACTIVE"] / XCDS
+        flops = avg["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
+        busy = avg["SQ_VALU_MFMA_BUSY_CYCLES"] / (gui * SIMDS) if gui else None
+        ghz = gui / (sum(dur[k] for k in keys) / len(keys)) / 1e9
+        tms = _trace_avg_ms(raw, wl, sym)
+        frac = flops / (tms / 1e3) / PEAK_BF16 if tms else None
+        rec["kernels"][kind] = {"symbol": sym, "launches": len(keys),
+                                "mfma_flops_per_launch": flops, "mfma_busy": busy,
+                                "clock_ghz_counters_on": ghz, "trace_avg_ms": tms,
+                                "executed_frac_of_peak": frac}
+        lines.append(f"{kind:22s} {len(keys):8d} {flops / 1e12:12.2f} {busy:6.3f} {ghz:5.2f} "
+                     f"{tms if tms else float('nan'):9.3f} "
+                     f"{frac if frac else float('nan'):6.3f}")
+    json.dump(rec, open(os.path.join(out, f"mfma_{wl}.json"), "w"), indent=1)
+    open(os.path.join(out, f"mfma_{wl}.txt"), "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("what", choices=["trace", "counters", "all"])
+    ap.add_argument("what", choices=["trace", "counters", "mfma", "all"])
     ap.add_argument("--workload", default="fwdbwd_bf16", choices=sorted(PROFILED))
     ap.add_argument("--raw", default=os.path.join(tempfile.gettempdir(), "grpo_prof_raw"))
     ap.add_argument("--out", default=os.path.join(ROOT, "profiles"))
@@ -194,6 +267,8 @@ def main():
         trace(a.workload, a.raw, a.out, run=not a.summarize_only)
     if a.what in ("counters", "all"):
         counters(a.workload, a.raw, a.out)
+    if a.what in ("mfma", "all") and any(k.startswith("gemm") for k in PROFILED[a.workload]["kinds"]):
+        mfma(a.workload, a.raw, a.out)
 
 
 if __name__ == "__main__":
