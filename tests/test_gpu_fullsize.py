@@ -1,6 +1,8 @@
 """Parity at the benchmark's full sizes (H=4096, V=155136), in the launch
 configuration bench.py times. GPU only.
 
+* scoring workload (4 prompts x G=8 x 1024 tokens, N=32768): sampled rows'
+  logp and lse against the oracle, a bound on every row.
 * fwd+bwd workload (8 prompts x G=8 x 2048 tokens, N=131072): per-token
   outputs (logp, lse, ell, dL/dlogp, dL/dh rows) of a seeded sample of rows
   against the oracle, which scores each sampled row over the whole
@@ -110,6 +112,32 @@ def test_fwdbwd_full_size_sampled_rows_and_identities():
     bb = float((out["grad_hidden"].double() * hf).sum())
     assert abs(a - bb) <= 5e-3 * max(abs(a), abs(bb)), (a, bb)
     assert torch.isfinite(gw).all() and torch.isfinite(out["grad_hidden"].float()).all()
+
+
+def test_fwd_full_size_sampled_rows_and_bounds():
+    # log-prob scoring alone (4 prompts x G = 8 x 1024 tokens, N = 32768),
+    # through grpo_logprob_fwd without a mask, as bench.py's fwd workload
+    w = workloads.WORKLOADS["fwd_bf16"]
+    W_bits = workloads.make_weight(w)
+    h_bits = workloads.make_hidden(w)
+    b = workloads.make_batch(w)
+    V = w.vocab
+    rows = workloads.sample_rows(b["mask"], 24, seed=2)
+    Wd = oracle.decode(W_bits, "bf16")
+    hs = oracle.decode(h_bits[rows], "bf16")
+    o_lse, o_logp, _ = oracle.score_rows(hs, Wd, b["tokens"][rows])
+    del Wd
+    hd, Wdv = to_dev(h_bits, "bf16"), to_dev(W_bits, "bf16")
+    logp, lse = grpo.logprob_fwd(hd, Wdv, dev(b["tokens"]), None, check=True)
+    torch.cuda.synchronize()
+    assert rel_err(host64(logp)[rows], o_logp) <= TOL
+    assert rel_err(host64(lse)[rows], o_lse) <= TOL
+    # every row: a log-probability (< 0 with V = 155136 comparable logits),
+    # and Jensen's bound log sum_v e^z_v >= ln V + mean_v z_v = ln V + <h, mean_v W_v>
+    lp, ls = host64(logp), host64(lse)
+    assert np.all(np.isfinite(lp)) and np.all(np.isfinite(ls)) and np.all(lp < 0)
+    zbar = (hd.double() @ Wdv.double().mean(0)).cpu().numpy()
+    assert np.all(ls >= math.log(V) + zbar - 1e-3 * np.abs(ls))
 
 
 def test_reduced_tokens_full_vocab_grad_weight_rows():
