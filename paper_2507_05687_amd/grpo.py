@@ -8,6 +8,7 @@ calls raise.
 from __future__ import annotations
 
 import ctypes
+import functools
 import os
 
 import torch
@@ -105,6 +106,9 @@ def _need(t, name, dtype=None, device=None):
         raise ValueError(f"{name} is required")
     if not t.is_cuda:
         raise ValueError(f"{name} must be a device tensor")
+    if t.device.index != torch.cuda.current_device():
+        raise ValueError(f"{name} is on {t.device}, the call's other tensors on "
+                         f"cuda:{torch.cuda.current_device()}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if dtype is not None and t.dtype != dtype:
@@ -112,7 +116,23 @@ def _need(t, name, dtype=None, device=None):
     return t
 
 
+def _on_tensor_device(fn):
+    """Runs an entry point with its first device tensor's GPU current, so that
+    the library launches on that GPU's current stream."""
+    @functools.wraps(fn)
+    def wrapped(*args, **kw):
+        t = next((a for a in (*args, *kw.values()) if isinstance(a, torch.Tensor) and a.is_cuda),
+                 None)
+        if t is None:
+            return fn(*args, **kw)
+        with torch.cuda.device(t.device):
+            return fn(*args, **kw)
+    return wrapped
+
+
 # ------------------------------------------------------------ workspace
+# One buffer per (device, stream): calls on different streams may overlap and
+# must not share scratch; calls on one stream run in order.
 _ws_cache: dict = {}
 
 
@@ -121,9 +141,12 @@ def workspace_bytes(op: int, dt: int, N: int, H: int, V: int, num_seqs: int = 1)
 
 
 def workspace(nbytes: int, device=None) -> torch.Tensor:
-    """A 256-byte-aligned device byte buffer of at least nbytes (cached per device)."""
-    device = torch.device(device or torch.cuda.current_device())
-    key = device.index
+    """A 256-byte-aligned device byte buffer of at least nbytes, cached per
+    device and current stream (allocated on, and used only by, that stream, so
+    that torch's allocator reuses a replaced buffer only after the work queued
+    on it)."""
+    device = torch.device(device if device is not None else torch.cuda.current_device())
+    key = (device.index, torch.cuda.current_stream(device).cuda_stream)
     buf = _ws_cache.get(key)
     if buf is None or buf.numel() < nbytes + 256:
         _ws_cache.pop(key, None)
@@ -138,6 +161,7 @@ def free_workspace():
 
 
 # ------------------------------------------------------------ entry points
+@_on_tensor_device
 def group_advantages(rewards: torch.Tensor, group_size: int, std_eps: float = 1e-6,
                      unbiased: bool = True, out: torch.Tensor | None = None) -> torch.Tensor:
     """Eq. 2: per-prompt group-normalised advantages (rewards [P*G] fp32, prompt-major)."""
@@ -152,6 +176,7 @@ def group_advantages(rewards: torch.Tensor, group_size: int, std_eps: float = 1e
     return out
 
 
+@_on_tensor_device
 def pack_valid(mask: torch.Tensor | None, cu_seqlens: torch.Tensor):
     """(rows int32 [num_valid], counts int32 [B], num_valid int) of the valid rows."""
     _need(cu_seqlens, "cu_seqlens", torch.int64)
@@ -170,6 +195,7 @@ def pack_valid(mask: torch.Tensor | None, cu_seqlens: torch.Tensor):
     return rows[:n], counts, n
 
 
+@_on_tensor_device
 def logprob_fwd(hidden: torch.Tensor, weight: torch.Tensor, tokens: torch.Tensor,
                 mask: torch.Tensor | None = None, check: bool = False):
     """Per-token log-prob and log-sum-exp over the vocabulary: (logp, lse), fp32 [N]."""
@@ -191,6 +217,7 @@ def logprob_fwd(hidden: torch.Tensor, weight: torch.Tensor, tokens: torch.Tensor
     return logp, lse
 
 
+@_on_tensor_device
 def loss_fwd_bwd(hidden, weight, tokens, mask, cu_seqlens, old_logp, ref_logp, adv,
                  clip_eps: float = 0.2, beta: float = 0.0, agg: int = AGG_SEQ_MEAN,
                  lse_in=None, grad_hidden: bool = True, grad_weight: bool = True,
@@ -245,6 +272,7 @@ def loss_fwd_bwd(hidden, weight, tokens, mask, cu_seqlens, old_logp, ref_logp, a
     return out
 
 
+@_on_tensor_device
 def sft_ce_fwd_bwd(hidden, weight, tokens, mask=None, grad_hidden: bool = True,
                    grad_weight: bool = True, grad_hidden_dtype=None,
                    grad_weight_out: torch.Tensor | None = None,
@@ -285,6 +313,7 @@ def sft_ce_fwd_bwd(hidden, weight, tokens, mask=None, grad_hidden: bool = True,
     return out
 
 
+@_on_tensor_device
 def adamw_step(weight, exp_avg, exp_avg_sq, grad, step: int, lr: float = 1e-6,
                beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
                weight_decay: float = 0.01, weight_bf16: torch.Tensor | None = None):
@@ -305,6 +334,7 @@ def adamw_step(weight, exp_avg, exp_avg_sq, grad, step: int, lr: float = 1e-6,
     _check(st, "adamw_step")
 
 
+@_on_tensor_device
 def triton_rule_reward(text, offsets, test_passed, require_launch: bool = False,
                        weighted: bool = False, rule_weight: float = 0.0,
                        exec_weight: float = 0.0):
@@ -328,6 +358,7 @@ def triton_rule_reward(text, offsets, test_passed, require_launch: bool = False,
     return flags, reward
 
 
+@_on_tensor_device
 def check_error(ws: torch.Tensor):
     st = load().grpo_check_error(_ptr(ws), _stream())
     _check(st, "device")

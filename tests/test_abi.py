@@ -218,3 +218,17 @@ def test_profile_interface_without_launches(lib):
     assert lib.grpo_profile_query(0, ctypes.byref(c), ctypes.byref(t)) == 0
     assert c.value == 0 and t.value == 0.0
     assert lib.grpo_profile_query(n, ctypes.byref(c), ctypes.byref(t)) == 4
+
+
+def test_binding_rejects_host_tensors():
+    # argument marshalling checks run before any library call
+    import torch
+
+    from paper_2507_05687_amd import grpo
+
+    x = torch.zeros(8)
+    with pytest.raises(ValueError, match="device tensor"):
+        grpo.group_advantages(x, 4)
+    bf = torch.zeros(4, 8, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="device tensor"):
+        grpo.logprob_fwd(bf, bf, torch.zeros(4, dtype=torch.int64))

@@ -254,6 +254,26 @@ def test_deterministic_bits():
         assert torch.equal(a[k], c[k]), k
 
 
+def test_side_stream_and_workspace_per_stream():
+    # the binding launches on the caller's current stream, with a workspace of
+    # that stream's own; a side stream gives the same bits as the default one
+    kw = dict(SMALL["ragged_tiles"], dtype="bf16", rms_norm_hidden=True, seed=18)
+    w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    a = _run_loss(w, W, h, b, adv, old, ref)
+    ws_default = grpo.workspace(1024)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        c = _run_loss(w, W, h, b, adv, old, ref)
+        ws_side = grpo.workspace(1024)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    assert ws_side.data_ptr() != ws_default.data_ptr()
+    assert grpo.workspace(512).data_ptr() == ws_default.data_ptr()
+    for k in ("loss", "logp", "lse", "dlogp", "grad_hidden", "grad_weight"):
+        assert torch.equal(a[k], c[k]), k
+
+
 def test_lse_in_reuse():
     kw = dict(SMALL["ragged_tiles"], dtype="bf16", rms_norm_hidden=True, seed=17)
     w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
