@@ -314,7 +314,9 @@ def main():
     W_bits = workloads.make_weight(w, "policy")
     h_bits = workloads.make_hidden(w)
     batch = workloads.make_batch(w)
-    log(f"inputs generated in {time.time() - t0:.1f}s")
+    # the GPU run and the CPU-baseline leg both read these arrays
+    inputs_sha256 = workloads.batch_digest(W_bits, h_bits, batch)
+    log(f"inputs generated in {time.time() - t0:.1f}s, sha256 {inputs_sha256}")
     W = _to_dev_bf16(W_bits, torch)
     Wref = _to_dev_bf16(workloads.make_weight(w, "reference"), torch) if w.double_scoring else None
     h = _to_dev_bf16(h_bits, torch)
@@ -451,6 +453,7 @@ def main():
         "mfma_frac_executed": exe_frac,
         "roofline": roofline,
         "kernels_ms_per_step": {k: v[1] / args.steps for k, v in sorted(prof.items())},
+        "inputs_sha256": inputs_sha256,
     }
     if args.cpu_sample > 0:
         adv_h = adv.cpu().numpy().astype(np.float64)

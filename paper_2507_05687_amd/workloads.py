@@ -23,6 +23,7 @@ data, which these seeded synthetic tensors stand in for):
 from __future__ import annotations
 
 import dataclasses
+import hashlib
 import math
 from concurrent.futures import ThreadPoolExecutor
 
@@ -190,6 +191,23 @@ def make_batch(w: Workload) -> dict:
     ref_noise = (g.standard_normal(N) * w.noise_sigma).astype(np.float32)
     return dict(tokens=tokens, mask=mask, cu_seqlens=cu, lengths=lengths, rewards=rewards,
                 old_noise=old_noise, ref_noise=ref_noise)
+
+
+def input_digest(*arrays: np.ndarray) -> str:
+    """SHA-256 over the dtype, shape and bytes of each array, in order: logged
+    so that two consumers of a workload's inputs can be shown to read the same
+    bytes."""
+    d = hashlib.sha256()
+    for a in arrays:
+        a = np.ascontiguousarray(a)
+        d.update(f"{a.dtype.str}{a.shape}".encode())
+        d.update(memoryview(a).cast("B"))
+    return d.hexdigest()
+
+
+def batch_digest(W: np.ndarray, h: np.ndarray, batch: dict) -> str:
+    """input_digest of a workload's weight, hidden states and batch arrays."""
+    return input_digest(W, h, *(batch[k] for k in sorted(batch)))
 
 
 def sample_rows(mask: np.ndarray, count: int, seed: int = 0) -> np.ndarray:
