@@ -33,7 +33,11 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "grpo_oracle.c")
-_LIB = os.path.join(_HERE, "libgrpo_oracle.so")
+# The test that checks the pins themselves runs them against copies of the
+# library with a planted mistake, named by this variable; it is never built
+# over. Nothing else sets it.
+_OVERRIDE = os.environ.get("GRPO_ORACLE_LIB")
+_LIB = _OVERRIDE or os.path.join(_HERE, "libgrpo_oracle.so")
 _lib = None
 
 _D = np.ctypeslib.ndpointer(dtype=np.float64, flags="C_CONTIGUOUS")
@@ -46,6 +50,8 @@ _vp = ctypes.c_void_p
 
 def build(force: bool = True) -> str:
     """Compile the oracle with gcc (no fast-math: sums keep their order)."""
+    if _OVERRIDE:
+        return _LIB
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp"
         subprocess.run(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c99",
@@ -57,7 +63,8 @@ def build(force: bool = True) -> str:
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        if not _OVERRIDE and (not os.path.exists(_LIB) or
+                              os.path.getmtime(_LIB) < os.path.getmtime(_SRC)):
             build(force=True)
         lib = ctypes.CDLL(_LIB)
         lib.oracle_group_advantages.argtypes = [_D, _i64, _i64, _dbl, ctypes.c_int, _D]
