@@ -73,11 +73,16 @@ def _compare_loss(w, W, h, b, adv, old, ref, out, tol, grad_tol, agg=0):
     # token loss and dL/dlogp, absolute scale-aware
     tl = host64(out["token_loss"])
     assert np.max(np.abs(tl - o["ell"])) <= tol * max(1.0, np.max(np.abs(o["ell"])))
-    g = host64(out["dlogp"])
-    assert np.max(np.abs(g - o["g"])) <= tol * np.max(np.abs(o["g"])) + 1e-12
-    # clip flags bit-exact away from the clip boundary
+    # dL/dlogp jumps at the clip bounds (the clipped branch has zero slope), so a
+    # token whose ratio is within rounding of a bound may take either branch: it
+    # is compared, like the clip flag, only away from the bounds (the count of
+    # such tokens grows with N: about 60 of 4M within 1e-5 of 1.2 at sigma 0.1)
     rho = np.exp(o["logp"] - old)
     far = (np.abs(rho - (1 - w.clip_eps)) > 1e-3) & (np.abs(rho - (1 + w.clip_eps)) > 1e-3) & m
+    g = host64(out["dlogp"])
+    keep = far | ~m
+    assert np.max(np.abs(g - o["g"])[keep]) <= tol * np.max(np.abs(o["g"])) + 1e-12
+    # clip flags bit-exact away from the clip boundary
     flag = out["clip_flag"].cpu().numpy()
     assert np.array_equal(flag[far], o["clipped"][far])
     assert np.all(flag[~m] == 0)
@@ -173,6 +178,19 @@ def test_bf16_loss_parity(case):
     kw = dict(SMALL[case], dtype="bf16", rms_norm_hidden=True, beta=0.01, noise_sigma=0.1,
               seed=11)
     w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    out = _run_loss(w, W, h, b, adv, old, ref)
+    _compare_loss(w, W, h, b, adv, old, ref, out, BF16_TOL, BF16_GRAD_TOL)
+
+
+@pytest.mark.timeout(900)
+def test_bf16_backward_at_its_row_limit():
+    # 2^22 rows, the most the bf16 backward takes per call: packing and
+    # scoring over 16384 token tiles, dz products in column mode, dL/dW with
+    # its K (the tokens) split 8 ways, every output against the full oracle
+    kw = dict(prompts=2048, group=8, seq_len=256, hidden=32, vocab=512, dtype="bf16",
+              rms_norm_hidden=True, beta=0.01, noise_sigma=0.1, seed=21)
+    w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    assert w.num_tokens == 1 << 22
     out = _run_loss(w, W, h, b, adv, old, ref)
     _compare_loss(w, W, h, b, adv, old, ref, out, BF16_TOL, BF16_GRAD_TOL)
 
