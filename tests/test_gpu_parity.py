@@ -195,6 +195,18 @@ def test_bf16_backward_at_its_row_limit():
     _compare_loss(w, W, h, b, adv, old, ref, out, BF16_TOL, BF16_GRAD_TOL)
 
 
+@pytest.mark.timeout(900)
+def test_bf16_vocabulary_of_4m_entries():
+    # V = 2^22 with few tokens: 512 vocabulary chunks in the backward pass,
+    # 32768 (max, sum-exp) partials per token to merge, a split dL/dW product
+    # per chunk; every output against the full oracle
+    kw = dict(prompts=2, group=4, seq_len=64, hidden=16, vocab=1 << 22, dtype="bf16",
+              rms_norm_hidden=True, beta=0.01, noise_sigma=0.1, seed=22)
+    w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    out = _run_loss(w, W, h, b, adv, old, ref)
+    _compare_loss(w, W, h, b, adv, old, ref, out, BF16_TOL, BF16_GRAD_TOL)
+
+
 def test_bf16_token_mean_aggregation():
     kw = dict(SMALL["ragged_tiles"], dtype="bf16", rms_norm_hidden=True, beta=0.01, seed=12)
     w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
