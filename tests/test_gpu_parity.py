@@ -170,6 +170,8 @@ SMALL = {
     "tiny": dict(prompts=1, group=2, seq_len=3, hidden=8, vocab=5),
     # dL/dW of 21 x 16 = 336 tiles: K split in 3 to fill whole rounds of 256 CUs
     "split_rounds": dict(prompts=2, group=4, seq_len=40, hidden=4096, vocab=5376),
+    # a wide hidden state: 2048 K steps per scoring tile, 256 gradient tile-columns
+    "wide_hidden": dict(prompts=2, group=4, seq_len=32, hidden=65536, vocab=300),
 }
 
 
