@@ -144,6 +144,15 @@ def test_tiny_fp32_config():
     _compare_loss(w, W, h, b, adv, old, ref, out, F32_TOL, F32_TOL)
 
 
+def test_fp32_at_its_hidden_limit():
+    """fp32 with H = 8192 (two LDS rows of H floats, 64 KiB), a ragged mask and
+    a vocabulary tail, against the oracle at 1e-5."""
+    w, W, h, b, adv, old, ref = _problem("tiny_fp32", hidden=8192, vocab=777, seq_len=12,
+                                         ragged=True, min_len=1, seed=24)
+    out = _run_loss(w, W, h, b, adv, old, ref)
+    _compare_loss(w, W, h, b, adv, old, ref, out, F32_TOL, F32_TOL)
+
+
 def test_tiny_fp32_pipeline_from_rewards():
     """Rewards -> group_advantages -> loss, all on the device, vs the oracle chain."""
     w, W, h, b, _, old, ref = _problem("tiny_fp32", seed=5)
