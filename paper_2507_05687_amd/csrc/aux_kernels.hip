@@ -105,12 +105,13 @@ __device__ inline bool row_valid(const uint8_t* mask, const int64_t* tokens, int
 }
 
 // Row range of rollout b, checked against 0 = cu[0] <= ... <= cu[B] = N.
-// cu == NULL stands for a single rollout covering every row.
-__device__ inline bool seq_range(const int64_t* cu, int64_t b, int64_t B, int64_t N, int64_t& lo,
-                                 int64_t& hi, WsHeader* hdr) {
+// cu == NULL stands for a single rollout covering every row, cut into
+// segments of `seg` rows (one workgroup each); b is then a segment.
+__device__ inline bool seq_range(const int64_t* cu, int64_t seg, int64_t b, int64_t B, int64_t N,
+                                 int64_t& lo, int64_t& hi, WsHeader* hdr) {
   if (cu == nullptr) {
-    lo = 0;
-    hi = N;
+    lo = b * seg;
+    hi = lo + seg < N ? lo + seg : N;
     return true;
   }
   lo = cu[b];
@@ -131,12 +132,12 @@ __global__ void k_fill_i32(int32_t* p, int64_t n, int32_t v) {
 // counts[b] = number of valid rows of rollout b.
 __global__ void __launch_bounds__(256) k_pack_count(const uint8_t* __restrict__ mask,
                                                     const int64_t* __restrict__ tokens, int64_t V,
-                                                    const int64_t* __restrict__ cu, int64_t B,
-                                                    int64_t N, int32_t* __restrict__ counts,
-                                                    WsHeader* hdr) {
+                                                    const int64_t* __restrict__ cu, int64_t seg,
+                                                    int64_t B, int64_t N,
+                                                    int32_t* __restrict__ counts, WsHeader* hdr) {
   int64_t b = blockIdx.x;
   int64_t lo, hi;
-  seq_range(cu, b, B, N, lo, hi, hdr);
+  seq_range(cu, seg, b, B, N, lo, hi, hdr);
   int c = 0;
   for (int64_t r = lo + threadIdx.x; r < hi; r += 256) c += row_valid(mask, tokens, V, r, hdr);
   __shared__ int redi[256];
@@ -184,13 +185,14 @@ __global__ void __launch_bounds__(256) k_pack_scan(const int32_t* __restrict__ c
 // rows_p[j] = row, seq_p[j] = b, y_p[j] = token id, pidx[row] = j (or -1).
 __global__ void __launch_bounds__(256) k_pack_scatter(
     const uint8_t* __restrict__ mask, const int64_t* __restrict__ tokens, int64_t V,
-    const int64_t* __restrict__ cu, int64_t B, int64_t N, const int32_t* __restrict__ base,
+    const int64_t* __restrict__ cu, int64_t seg, int64_t B, int64_t N,
+    const int32_t* __restrict__ base,
     int32_t* __restrict__ rows_p, int32_t* __restrict__ seq_p, int32_t* __restrict__ y_p,
     int32_t* __restrict__ pidx, WsHeader* hdr) {
   __shared__ int32_t wcount[4];
   int64_t b = blockIdx.x;
   int64_t lo, hi;
-  seq_range(cu, b, B, N, lo, hi, hdr);
+  seq_range(cu, seg, b, B, N, lo, hi, hdr);
   int32_t next = base[b];
   int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   for (int64_t r0 = lo; r0 < hi; r0 += 256) {
@@ -233,11 +235,11 @@ void launch_pack(const PackArgs& a, hipStream_t s) {
                        a.N, -1);
   }
   hipLaunchKernelGGL(k_pack_count, dim3((unsigned)a.B), dim3(256), 0, s, a.mask, a.tokens, a.V,
-                     a.cu, a.B, a.N, a.counts, a.hdr);
+                     a.cu, a.seg, a.B, a.N, a.counts, a.hdr);
   hipLaunchKernelGGL(k_pack_scan, dim3(1), dim3(256), 0, s, a.counts, a.B, a.base, a.hdr,
                      a.num_valid_out);
   hipLaunchKernelGGL(k_pack_scatter, dim3((unsigned)a.B), dim3(256), 0, s, a.mask, a.tokens,
-                     a.V, a.cu, a.B, a.N, a.base, a.rows_p, a.seq_p, a.y_p, a.pidx, a.hdr);
+                     a.V, a.cu, a.seg, a.B, a.N, a.base, a.rows_p, a.seq_p, a.y_p, a.pidx, a.hdr);
 }
 
 // ------------------------------------------------------ lse combine

@@ -88,6 +88,7 @@ grpo_status check_device() {
 
 // --------------------------------------------------------- workspace
 constexpr size_t kAlign = 256;
+constexpr int64_t kPackSeg = 4096;  // rows per packing workgroup without cu_seqlens
 #ifndef GRPO_DZ_BUDGET_GIB
 #define GRPO_DZ_BUDGET_GIB 48
 #endif
@@ -172,8 +173,10 @@ Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_
   L.seq = take(c, 4 * L.Npad);
   L.y = take(c, 4 * L.Npad);
   L.pidx = take(c, 4 * N);
-  L.counts = take(c, 4 * B);
-  L.base = take(c, 4 * (B + 1));
+  // per rollout, or per packing segment when every row forms one rollout
+  const int64_t units = B > ceil_div(N, kPackSeg) ? B : ceil_div(N, kPackSeg);
+  L.counts = take(c, 4 * units);
+  L.base = take(c, 4 * (units + 1));
   L.lse = take(c, 4 * L.Npad);
   L.zy = take(c, 4 * L.Npad);
   L.logp = take(c, 4 * L.Npad);
@@ -272,7 +275,10 @@ grpo_status run_pack(const Layout& L, void* ws, const uint8_t* mask, const int64
   a.tokens = tokens;
   a.V = V;
   a.cu = cu;
-  a.B = B;
+  // without cu_seqlens every row belongs to one rollout; it is packed in
+  // segments, one workgroup each (the per-row rollout index is then unused)
+  a.seg = kPackSeg;
+  a.B = cu ? B : ceil_div(N, kPackSeg);
   a.N = N;
   a.counts = counts_out ? counts_out : at<int32_t>(ws, L.counts);
   a.base = at<int32_t>(ws, L.base);

@@ -50,6 +50,7 @@ struct PackArgs {
   const int64_t* tokens;  // optional: ids are range-checked against V
   int64_t V;
   const int64_t* cu;
+  int64_t seg;       // cu == NULL: rows are packed in segments of seg rows, B = their count
   int64_t B, N;
   int32_t* counts;   // [B]
   int32_t* base;     // [B+1]
