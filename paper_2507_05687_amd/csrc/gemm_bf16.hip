@@ -712,7 +712,6 @@ __global__ void __launch_bounds__(64 * kW4Waves, 1) k_gemm_w4(GemmArgs g, Epi ep
   constexpr int kMfmas = 32;           // MFMAs per wave per step
   constexpr int kSpread = kMfmas / kPerStep;
   using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
 
   const int nk = K / kBK;
   const int last = nk > 0 ? nk - 1 : 0;
