@@ -244,20 +244,44 @@ void launch_pack(const PackArgs& a, hipStream_t s) {
 
 // ------------------------------------------------------ lse combine
 // lse of packed token j from the per-vocabulary-tile partials, then
-// logp = z_y - lse.
-__global__ void __launch_bounds__(256) k_lse_finalize(const float2* __restrict__ ms, int64_t ldms,
-                                                      int tiles, const float* __restrict__ zy,
-                                                      const WsHeader* __restrict__ hdr,
-                                                      float* __restrict__ lse_p,
-                                                      float* __restrict__ logp_p) {
-  int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+// logp = z_y - lse. One token per lane (the partials of consecutive tokens are
+// contiguous); the partials are merged in kChains interleaved chains, partial
+// t going to chain t % kChains, so that that many loads are in flight, and the
+// chains are then merged pairwise in a fixed order.
+constexpr int kChains = 8;
+__global__ void __launch_bounds__(64) k_lse_finalize(const float2* __restrict__ ms, int64_t ldms,
+                                                     int tiles, const float* __restrict__ zy,
+                                                     const WsHeader* __restrict__ hdr,
+                                                     float* __restrict__ lse_p,
+                                                     float* __restrict__ logp_p) {
+  int64_t j = (int64_t)blockIdx.x * 64 + threadIdx.x;
   if (j >= hdr->num_valid) return;
-  float m = -INFINITY, s = 0.f;
-  for (int t = 0; t < tiles; ++t) {
-    float2 p = ms[(int64_t)t * ldms + j];
-    lse_merge(m, s, p.x, p.y);
+  float m[kChains], s[kChains];
+#pragma unroll
+  for (int c = 0; c < kChains; ++c) {
+    m[c] = -INFINITY;
+    s[c] = 0.f;
   }
-  float l = m + __logf(s);
+  int t = 0;
+  for (; t + kChains <= tiles; t += kChains) {
+    float2 p[kChains];
+#pragma unroll
+    for (int c = 0; c < kChains; ++c) p[c] = ms[(int64_t)(t + c) * ldms + j];
+#pragma unroll
+    for (int c = 0; c < kChains; ++c) lse_merge(m[c], s[c], p[c].x, p[c].y);
+  }
+#pragma unroll
+  for (int c = 0; c < kChains - 1; ++c) {
+    if (t + c < tiles) {
+      const float2 p = ms[(int64_t)(t + c) * ldms + j];
+      lse_merge(m[c], s[c], p.x, p.y);
+    }
+  }
+#pragma unroll
+  for (int w = 1; w < kChains; w *= 2)
+#pragma unroll
+    for (int c = 0; c + w < kChains; c += 2 * w) lse_merge(m[c], s[c], m[c + w], s[c + w]);
+  float l = m[0] + __logf(s[0]);
   lse_p[j] = l;
   logp_p[j] = zy[j] - l;
 }
@@ -265,7 +289,7 @@ __global__ void __launch_bounds__(256) k_lse_finalize(const float2* __restrict__
 void launch_lse_finalize(const float2* ms, int64_t ldms, int tiles, const float* zy,
                          const WsHeader* hdr, float* lse_p, float* logp_p, int64_t Nmax,
                          hipStream_t s) {
-  hipLaunchKernelGGL(k_lse_finalize, dim3((unsigned)ceil_div(Nmax, 256)), dim3(256), 0, s, ms,
+  hipLaunchKernelGGL(k_lse_finalize, dim3((unsigned)ceil_div(Nmax, 64)), dim3(64), 0, s, ms,
                      ldms, tiles, zy, hdr, lse_p, logp_p);
 }
 
