@@ -145,7 +145,11 @@ __device__ __forceinline__ bool decorator_at(const T& X, int64_t p) {
   return true;
 }
 
-// name [ns, ns + nl) of the function decorated by the decorator at p
+// name [ns, ns + nl) of the function decorated by the decorator at p.
+// Also false when the follow-up reaches a later @triton.jit line whose own
+// follow-up starts where this one continues: that decorator decorates the
+// same function and reports it, so a stack of n decorators costs O(n) lines
+// instead of O(n^2).
 template <class T>
 __device__ __forceinline__ bool decorated_name(const T& X, int64_t p, int64_t& ns, int64_t& nl) {
   int64_t i = finish_line(X, p + kDecoLen);
@@ -162,6 +166,7 @@ __device__ __forceinline__ bool decorated_name(const T& X, int64_t p, int64_t& n
       int64_t k = j + 1;
       while (k < X.n && X[k] != '(' && X[k] != '\n') ++k;
       i = (k < X.n && X[k] == '(') ? finish_line(X, k) : line_end(X, k) + 1;
+      if (i >= 0 && decorator_at(X, j) && finish_line(X, j + kDecoLen) == i) return false;
       continue;
     }
     if (!(j + 3 < X.n && X[j] == 'd' && X[j + 1] == 'e' && X[j + 2] == 'f' && is_blank(X[j + 3])))
@@ -360,7 +365,8 @@ __device__ int64_t wave_finish_line(const LdsText& X, int64_t i) {
   return wave_line_end(X, i) + 1;
 }
 
-// decorated_name with the long scans shared by the wave
+// decorated_name with the long scans shared by the wave (used for at most
+// kRrList decorators per completion, so it follows stacks to their end)
 __device__ bool wave_decorated_name(const LdsText& X, int64_t p, int64_t& ns, int64_t& nl) {
   int64_t i = wave_finish_line(X, p + kDecoLen);
   while (i >= 0) {

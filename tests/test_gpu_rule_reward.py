@@ -82,6 +82,29 @@ def test_edges():
     assert np.array_equal(f, [0, 0]) and np.array_equal(r, [0.0, 0.0])
 
 
+def test_deep_decorator_stacks():
+    # repetition loops of decorators (each resolved up to the next one of the
+    # same function), with the lines where that shortcut must not apply: text
+    # after the decorator, a parenthesis inside its comment, arguments over
+    # several lines, other decorators in between, no function at the end
+    n = 1500
+    kernel = b"def k(x):\n    pass\nk[1](0)\n"
+    stacks = [
+        b"@triton.jit\n" * n + kernel,
+        b"@triton.jit\n" * n,
+        b"@triton.jit\n" * n + b"x = 1\n" + kernel,
+        b"@triton.jit\n" * (n // 2) + b"@triton.jit x\n" + b"@triton.jit\n" * (n // 2) + kernel,
+        b"@triton.jit x\n" * n + kernel,
+        b"@triton.jit  # f(x)\n" * n + kernel,
+        b"@triton.jit  # f(x\n" * n + kernel,
+        b"@triton.jit(\n  a=(1, 2),\n)\n" * (n // 3) + kernel,
+        (b"@triton.jit\n@triton.autotune(configs=[])\n" * (n // 2)) + kernel,
+        b"\t@triton.jit()\n\n# c\n" * (n // 2) + kernel,
+        b"@triton.jit\n" * n + b"def 9k(x):\n",
+    ]
+    _check(stacks, np.array([1, 0] * 5 + [1], np.uint8))
+
+
 def test_decreasing_offsets_count_as_empty():
     data = np.frombuffer(b"@triton.jit\ndef k(x):\n    pass\n", np.uint8).copy()
     offsets = np.array([0, len(data), 5], np.int64)
