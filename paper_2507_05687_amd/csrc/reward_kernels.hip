@@ -240,8 +240,14 @@ __device__ __forceinline__ bool is_triton_block(const T& X, int require_launch, 
     }
     return false;
   }
-  // too many to list: wave 0 takes the decorators in text order
+  // too many to list: wave 0 takes the decorators in text order; a name equal
+  // to one of the last kRecent names it found unlaunched is not searched again
+  // (a completion that repeats one definition costs one search, not one per copy)
   if (tid < 64) {
+    constexpr int kRecent = 4;
+    int64_t rs[kRecent], rl[kRecent];
+    static_for<kRecent>([&](auto q) { rs[q.value] = rl[q.value] = -1; });
+    int next = 0;
     bool found = false;
     for (int64_t base = 0; base < X.n && !found; base += 64) {
       const int64_t p = base + tid;
@@ -251,6 +257,22 @@ __device__ __forceinline__ bool is_triton_block(const T& X, int require_launch, 
         m &= m - 1;
         int64_t ns = 0, nl = 0;
         if (!decorated_name(X, pp, ns, nl)) continue;
+        bool seen = false;
+        static_for<kRecent>([&](auto q) {
+          if (!seen && rl[q.value] == nl) {
+            bool eq = true;
+            for (int64_t k = 0; k < nl && eq; ++k) eq = X[rs[q.value] + k] == X[ns + k];
+            seen = eq;
+          }
+        });
+        if (seen) continue;
+        static_for<kRecent>([&](auto q) {
+          if (q.value == next) {
+            rs[q.value] = ns;
+            rl[q.value] = nl;
+          }
+        });
+        next = (next + 1) % kRecent;
         for (int64_t b2 = 0; b2 < X.n; b2 += 64) {
           if (__ballot(b2 + tid < X.n && launch_at(X, b2 + tid, ns, nl)) != 0) {
             found = true;

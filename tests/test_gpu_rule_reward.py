@@ -105,6 +105,19 @@ def test_deep_decorator_stacks():
     _check(stacks, np.array([1, 0] * 5 + [1], np.uint8))
 
 
+def test_repeated_definitions():
+    # more decorated functions than the name list holds: one definition
+    # repeated (searched once), a few alternating, and distinct names with the
+    # only launch at the end or of an earlier name
+    one = b"@triton.jit\ndef add(x):\n    pass\n"
+    alt = b"".join(b"@triton.jit\ndef f%d(x):\n    pass\n" % (i % 3) for i in range(300))
+    distinct = b"".join(b"@triton.jit\ndef g%d(x):\n    pass\n" % i for i in range(150))
+    texts = [one * 400, one * 400 + b"add[(1,)](0)\n", one * 200 + b"adder[1](0)\n" + one * 200,
+             alt, alt + b"f2[g](1)\n", alt + b"f3[g](1)\n",
+             distinct + b"g149[1](0)\n", distinct + b"g0[1](0)\n", distinct + b"g150[1](0)\n"]
+    _check(texts, np.ones(len(texts), np.uint8))
+
+
 def test_decreasing_offsets_count_as_empty():
     data = np.frombuffer(b"@triton.jit\ndef k(x):\n    pass\n", np.uint8).copy()
     offsets = np.array([0, len(data), 5], np.int64)
