@@ -135,9 +135,7 @@ def trace(wl: str, raw: str, out: str, run: bool = True):
              *sha_lines(cfg),
              f"{'calls':>6} {'total_ms':>10} {'avg_ms':>9} {'pct':>6}  kernel"]
     for name, calls, tot, avg, pct in rows:
-        if pct < 0.01:
-            continue
-        # top_kernels reports microseconds
+        # every kernel, the small streaming ones included; top_kernels reports microseconds
         lines.append(f"{calls:6d} {tot / 1e3:10.3f} {avg / 1e3:9.4f} {pct:6.2f}  {name[:110]}")
     path = os.path.join(out, f"kernels_{wl}.txt")
     open(path, "w").write("\n".join(lines) + "\n")
