@@ -17,7 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libgrpo.so")
 BUILD_DIR = os.path.join(PKG, "_build")
-SOURCES = ["grpo_api.hip", "aux_kernels.hip", "gemm_bf16.hip", "reward_kernels.hip"]
+SOURCES = ["grpo_api.hip", "aux_kernels.hip", "gemm_bf16.hip", "reward_kernels.hip", "onehot.hip"]
 
 # Packed fp32 VALU forms are turned off for all device code.
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall",

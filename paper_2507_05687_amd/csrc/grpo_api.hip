@@ -20,13 +20,13 @@ namespace {
 enum Kind {
   K_PACK, K_ADV, K_GEMM_LSE, K_LSE_FIN, K_TOKEN, K_TRANSPOSE, K_GEMM_DZ, K_GEMM_DH, K_GEMM_DW,
   K_F32_SCORE, K_F32_DH, K_F32_DW, K_ZERO_ROWS, K_GATHER_DOT, K_TILE, K_ADAMW,
-  K_RULE_REWARD, K_SUM_SPLITS, K_NUM_KINDS
+  K_RULE_REWARD, K_SUM_SPLITS, K_ONEHOT, K_NUM_KINDS
 };
 const char* kKindNames[K_NUM_KINDS] = {
     "pack_valid",  "group_advantages", "gemm_logits_lse", "lse_finalize",   "token_objective",
     "transpose",   "gemm_recompute_dz", "gemm_grad_hidden", "gemm_grad_weight", "f32_score",
     "f32_grad_hidden", "f32_grad_weight", "zero_masked_rows", "gather_dot", "tile", "adamw",
-    "rule_reward", "sum_splits"};
+    "rule_reward", "sum_splits", "onehot_grad_weight"};
 
 struct Prof {
   std::mutex mu;
@@ -111,6 +111,7 @@ struct Layout {
   int64_t Hk = 0;  // H rounded up to the tiled block width
   // tiled buffers and their tile-row strides in blocks
   size_t WK = 0, hK = 0, hT = 0, WT = 0, dz = 0, dzT = 0, dhacc = 0, dwpart = 0;
+  size_t okeys[2] = {0, 0}, ovals[2] = {0, 0}, ocounts = 0;  // sort of the sampled ids
   int64_t sK = 0, sTok = 0, sVoc = 0, sChunk = 0;
   size_t total = 0;
 };
@@ -204,6 +205,12 @@ Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_
       // dW partials of a split K (chunks too narrow to fill the GPU)
       if (dw_splits(L.Vc / kTile * (Hpad / kTile)) > 1)
         L.dwpart = take(c, 4 * kMaxSplits * L.Vc * Hpad);
+      // the stable sort of the packed ids for the sampled-id term of dL/dW
+      for (int b = 0; b < 2; ++b) {
+        L.okeys[b] = take(c, 4 * L.Npad);
+        L.ovals[b] = take(c, 4 * L.Npad);
+      }
+      L.ocounts = take(c, 4 * onehot_count_entries(L.Npad));
     }
   }
   L.total = c;
@@ -396,8 +403,8 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
                             nullptr);
     uint16_t* dz_c = dz + j * (L.Vc / kBK) * kTileElems;
     TRY(timed(K_GEMM_DZ, s, [&] {
-      launch_gemm_dz(gz, y_p, lse_p, g_p, dz_c, kt_chunk, grad_weight ? dzT : nullptr, kt_tok, V,
-                     v0, s);
+      launch_gemm_dz(gz, lse_p, g_p, dz_c, kt_chunk, grad_weight ? dzT : nullptr, kt_tok, V, v0,
+                     s);
     }));
     if (grad_weight) {
       // dW[v, :] = sum_t dz[t, v] h[t, :] over the valid tokens
@@ -446,6 +453,12 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
       sa.out = last ? grad_hidden : nullptr;
       sa.ld_out = H;
       sa.out_bf16 = grad_hidden_dt == GRPO_BF16;
+      if (last) {  // the sampled id's term g_t W[y_t], in fp32 before the final rounding
+        sa.oh_g = g_p;
+        sa.oh_y = y_p;
+        sa.oh_w = (const uint16_t*)weight;
+        sa.oh_ld = H;
+      }
       sa.add_out = 0;
       sa.out_rows = rows_p;
       sa.m_limit = L.Npad;
@@ -454,7 +467,25 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
     }
     if (last) break;
   }
-  if (grad_hidden && mask) {
+  if (grad_weight) {  // the sampled id's term sum_{t: y_t = v} g_t h_t of dW[v], in fp32
+    OnehotArgs oa;
+    oa.y_p = y_p;
+    oa.rows_p = rows_p;
+    oa.g_p = g_p;
+    oa.hdr = hdr;
+    oa.hidden = (const uint16_t*)hidden;
+    oa.H = H;
+    oa.V = V;
+    oa.n = L.Npad;
+    for (int b = 0; b < 2; ++b) {
+      oa.keys[b] = at<int32_t>(ws, L.okeys[b]);
+      oa.vals[b] = at<int32_t>(ws, L.ovals[b]);
+    }
+    oa.counts = at<int32_t>(ws, L.ocounts);
+    oa.dW = grad_weight;
+    TRY(timed(K_ONEHOT, s, [&] { launch_onehot_dw(oa, s); }));
+  }
+  if (grad_hidden) {  // rows that packing dropped (masked, bad id or bad cu_seqlens) get dh = 0
     TRY(timed(K_ZERO_ROWS, s, [&] {
       launch_zero_masked_rows(pidx, N, H, grad_hidden, grad_hidden_dt == GRPO_BF16, s);
     }));

@@ -34,14 +34,22 @@ struct StoreArgs {
   int64_t m_limit;
   int64_t n_limit;
   int64_t split_stride;  // with a split K: elements between the splits' acc_buf partials
+  // optional term added to every stored row m: oh_g[m] * row oh_y[m] of the bf16
+  // matrix oh_w (row stride oh_ld); used only on the product that writes `out`
+  const float* oh_g;
+  const int32_t* oh_y;
+  const uint16_t* oh_w;
+  int64_t oh_ld;
 };
 
 int gemm_grid(int tiles_m, int tiles_n);
 void launch_gemm_lse(const GemmArgs& g, const int32_t* y_p, float* zy, float2* ms, int64_t ldms,
                      int64_t V, hipStream_t s);
-void launch_gemm_dz(const GemmArgs& g, const int32_t* y_p, const float* lse_p, const float* g_p,
-                    uint16_t* dz, int64_t dz_kt, uint16_t* dzT, int64_t dzT_kt, int64_t V,
-                    int64_t v0, hipStream_t s);
+// dz = -g * exp(z - lse) for a vocabulary chunk starting at row v0 (the
+// sampled id's +g is left to the gradient products' callers)
+void launch_gemm_dz(const GemmArgs& g, const float* lse_p, const float* g_p, uint16_t* dz,
+                    int64_t dz_kt, uint16_t* dzT, int64_t dzT_kt, int64_t V, int64_t v0,
+                    hipStream_t s);
 void launch_gemm_store(const GemmArgs& g, const StoreArgs& a, bool grad_weight, hipStream_t s);
 
 // ------------------------------------------------------------- packing
@@ -91,6 +99,26 @@ struct TokenArgs {
 };
 int64_t token_objective_blocks(int64_t N);
 void launch_token_objective(const TokenArgs& a, hipStream_t s);
+
+// ------------------------------------------------ sampled-id term of dL/dW
+// dW[y_t] += g_t h_t for every valid packed token t, summed per id in packed
+// order (ids grouped by a stable radix sort). keys/vals: two int32 buffers of
+// n each; counts: onehot_count_entries(n) int32.
+struct OnehotArgs {
+  const int32_t* y_p;     // packed token -> id
+  const int32_t* rows_p;  // packed token -> row of hidden
+  const float* g_p;       // packed token -> dL/dlogp
+  const WsHeader* hdr;    // num_valid
+  const uint16_t* hidden; // bf16 [rows][H], H % 8 == 0, 16-byte aligned
+  int64_t H, V;
+  int64_t n;              // packed rows covered (>= num_valid)
+  int32_t* keys[2];
+  int32_t* vals[2];
+  int32_t* counts;
+  float* dW;              // [V][H]
+};
+int64_t onehot_count_entries(int64_t n);
+void launch_onehot_dw(const OnehotArgs& a, hipStream_t s);
 
 // ------------------------------------------------------------ AdamW
 struct AdamArgs {

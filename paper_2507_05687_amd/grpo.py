@@ -116,6 +116,24 @@ def _need(t, name, dtype=None, device=None):
     return t
 
 
+def _extent(t, name, *shape):
+    """Raises ValueError unless t (if given) has exactly the given shape; the C ABI
+    receives bare pointers and cannot check extents itself."""
+    if t is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t
+
+
+def _matrices(hidden, weight):
+    """(N, H, V) of hidden [N, H] and weight [V, H]."""
+    if hidden.dim() != 2 or weight.dim() != 2:
+        raise ValueError("hidden and weight must be 2-D ([N, H] and [V, H])")
+    N, H = hidden.shape
+    V = weight.shape[0]
+    _extent(weight, "weight", V, H)
+    return N, H, V
+
+
 def _on_tensor_device(fn):
     """Runs an entry point with its first device tensor's GPU current, so that
     the library launches on that GPU's current stream."""
@@ -170,6 +188,8 @@ def group_advantages(rewards: torch.Tensor, group_size: int, std_eps: float = 1e
     if n % group_size:
         raise ValueError("rewards length must be a multiple of group_size")
     out = torch.empty_like(rewards) if out is None else _need(out, "out", torch.float32)
+    if out.numel() != n:
+        raise ValueError(f"out has {out.numel()} elements, rewards {n}")
     st = load().group_advantages(_ptr(rewards), n // group_size, group_size, std_eps,
                                  int(unbiased), _ptr(out), _stream())
     _check(st, "group_advantages")
@@ -188,6 +208,8 @@ def pack_valid(mask: torch.Tensor | None, cu_seqlens: torch.Tensor):
     nv = torch.empty(1, dtype=torch.int32, device=dev)
     ws = workspace(workspace_bytes(OP_LOGPROB_FWD, F32, N, 1, 1, B), dev)
     m = None if mask is None else _need(mask, "mask").view(torch.uint8)
+    if B < 1:
+        raise ValueError("cu_seqlens needs at least two entries")
     st = load().grpo_pack_valid(_ptr(m), _ptr(cu_seqlens), B, N, _ptr(rows), _ptr(counts),
                                 _ptr(nv), _ptr(ws), ws.numel(), _stream())
     _check(st, "grpo_pack_valid")
@@ -202,8 +224,10 @@ def logprob_fwd(hidden: torch.Tensor, weight: torch.Tensor, tokens: torch.Tensor
     _need(hidden, "hidden")
     _need(weight, "weight", hidden.dtype)
     _need(tokens, "tokens", torch.int64)
-    N, H = hidden.shape
-    V = weight.shape[0]
+    N, H, V = _matrices(hidden, weight)
+    _extent(tokens.view(-1), "tokens", N)
+    if mask is not None and mask.numel() != N:
+        raise ValueError(f"mask has {mask.numel()} elements, expected {N}")
     dt = _dt(hidden)
     logp = torch.empty(N, dtype=torch.float32, device=hidden.device)
     lse = torch.empty(N, dtype=torch.float32, device=hidden.device)
@@ -237,9 +261,16 @@ def loss_fwd_bwd(hidden, weight, tokens, mask, cu_seqlens, old_logp, ref_logp, a
         _need(ref_logp, "ref_logp", torch.float32)
     if lse_in is not None:
         _need(lse_in, "lse_in", torch.float32)
-    N, H = hidden.shape
-    V = weight.shape[0]
+    N, H, V = _matrices(hidden, weight)
     B = cu_seqlens.numel() - 1
+    if B < 1:
+        raise ValueError("cu_seqlens needs at least two entries")
+    for t, name in ((tokens, "tokens"), (old_logp, "old_logp"), (ref_logp, "ref_logp"),
+                    (lse_in, "lse_in"), (mask, "mask")):
+        if t is not None and t.numel() != N:
+            raise ValueError(f"{name} has {t.numel()} elements, expected N = {N}")
+    if adv.numel() != B:
+        raise ValueError(f"adv has {adv.numel()} elements, expected one per rollout ({B})")
     dt = _dt(hidden)
     dev = hidden.device
     f32 = dict(dtype=torch.float32, device=dev)
@@ -253,7 +284,8 @@ def loss_fwd_bwd(hidden, weight, tokens, mask, cu_seqlens, old_logp, ref_logp, a
         out["grad_hidden"] = torch.empty(N, H, dtype=gh_dt, device=dev)
     if grad_weight:
         if grad_weight_out is not None:
-            out["grad_weight"] = _need(grad_weight_out, "grad_weight_out", torch.float32)
+            out["grad_weight"] = _extent(_need(grad_weight_out, "grad_weight_out",
+                                               torch.float32), "grad_weight_out", V, H)
         else:
             out["grad_weight"] = torch.empty(V, H, **f32)
     ws = workspace(workspace_bytes(OP_LOSS_FWD_BWD, dt, N, H, V, B), dev)
@@ -283,8 +315,10 @@ def sft_ce_fwd_bwd(hidden, weight, tokens, mask=None, grad_hidden: bool = True,
     _need(hidden, "hidden")
     _need(weight, "weight", hidden.dtype)
     _need(tokens, "tokens", torch.int64)
-    N, H = hidden.shape
-    V = weight.shape[0]
+    N, H, V = _matrices(hidden, weight)
+    for t, name in ((tokens, "tokens"), (mask, "mask")):
+        if t is not None and t.numel() != N:
+            raise ValueError(f"{name} has {t.numel()} elements, expected N = {N}")
     dt = _dt(hidden)
     dev = hidden.device
     f32 = dict(dtype=torch.float32, device=dev)
@@ -296,7 +330,8 @@ def sft_ce_fwd_bwd(hidden, weight, tokens, mask=None, grad_hidden: bool = True,
         out["grad_hidden"] = torch.empty(N, H, dtype=gh_dt, device=dev)
     if grad_weight:
         if grad_weight_out is not None:
-            out["grad_weight"] = _need(grad_weight_out, "grad_weight_out", torch.float32)
+            out["grad_weight"] = _extent(_need(grad_weight_out, "grad_weight_out",
+                                               torch.float32), "grad_weight_out", V, H)
         else:
             out["grad_weight"] = torch.empty(V, H, **f32)
     ws = workspace(workspace_bytes(OP_SFT_FWD_BWD, dt, N, H, V, 1), dev)

@@ -25,12 +25,15 @@ import torch
 
 import oracle
 from paper_2507_05687_amd import grpo, workloads
-from tests.gpu_util import dev, host64, norm_rel, rel_err, to_dev
+from tests.gpu_util import (BF16_OUT, dev, grad_tolerances, host64, norm_rel, rel_err,
+                            rounding_bounds, row_tolerances, to_dev)
 
 pytestmark = pytest.mark.gpu
 
 TOL = 2e-3
-GRAD_TOL = 5e-3
+# dL/dW and dL/dh: within the bound that bf16 rounding of the -g p entries of
+# dz implies (tests.gpu_util), plus 2^-9 for the bf16 dL/dh output; at these
+# shapes (V = 155136, logit std 1.3) the bound is about 1e-4
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -87,8 +90,9 @@ def test_fwdbwd_full_size_sampled_rows_and_identities():
     assert np.max(np.abs(g - o_g)) <= TOL * np.max(np.abs(o_g))
     o_dh = oracle.grad_hidden_rows(hs, Wd, b["tokens"][rows], o_lse, o_g)
     dh = host64(out["grad_hidden"][torch.from_numpy(rows).cuda()])
+    tols = row_tolerances(rounding_bounds(hs, Wd, o_g, vrows=[])[0], o_dh) + BF16_OUT
     for i in range(len(rows)):
-        assert norm_rel(dh[i], o_dh[i]) <= GRAD_TOL, (i, norm_rel(dh[i], o_dh[i]))
+        assert norm_rel(dh[i], o_dh[i]) <= tols[i], (i, norm_rel(dh[i], o_dh[i]), tols[i])
     del Wd
 
     # the loss is the weighted sum of the per-token terms it also returns
@@ -97,20 +101,30 @@ def test_fwdbwd_full_size_sampled_rows_and_identities():
     scale = float((out["token_loss"].double().abs() * c_t).sum())
     assert abs(out["loss"].item() - want) <= 1e-5 * scale
 
-    # identities of dL/dW that hold at any size:
-    #  sum_v dL/dW_v = sum_t h_t * g_t * (1 - sum_v p_tv) = 0, up to the bf16
-    #  rounding of dz: |.| <= 2^-7 * sum_t |h_t| |g_t| (each dz row sums to 0
-    #  and its absolute sum is at most 2|g_t|)
+    _grad_weight_identities(out, hd, Wdv)
+
+
+def _grad_weight_identities(out, hd, Wdv, dlogp=None):
+    """Identities of dL/dW that hold at any size:
+    * sum_v dL/dW_v = sum_t h_t g_t (1 - sum_v p_tv) = 0, up to the bf16
+      rounding of the -g p entries of dz (the +g of the sampled id is exact):
+      |.| <= 2^-9 sum_t |h_t| |g_t|, checked at 2^-8;
+    * <dW, W> = <dh, h> = sum_{t,v} dz_tv z_tv (the same dz on both sides),
+      up to fp32 accumulation and the bf16 rounding of a bf16 dL/dh: this
+      sum nearly cancels (on policy it is close to 0), so it is checked
+      against 2^-8 sum |dh| |h| (the rounding bound, doubled) and 1e-4 of
+      its own size."""
     gw = out["grad_weight"]
-    gt = out["dlogp"].double()
+    gt = (out["dlogp"] if dlogp is None else dlogp).double()
     hf = hd.double()
     colsum = gw.double().sum(0)
-    bound = 2.0 ** -7 * (hf.abs() * gt.abs()[:, None]).sum(0) + 1e-6
+    bound = 2.0 ** -8 * (hf.abs() * gt.abs()[:, None]).sum(0) + 1e-7
     assert torch.all(colsum.abs() <= bound), float((colsum.abs() / bound).max())
-    #  <dW, W> = <dh, h> = sum_{t,v} dz_tv z_tv
     a = float((gw.double() * Wdv.double()).sum())
-    bb = float((out["grad_hidden"].double() * hf).sum())
-    assert abs(a - bb) <= 5e-3 * max(abs(a), abs(bb)), (a, bb)
+    dhf = out["grad_hidden"].double()
+    bb = float((dhf * hf).sum())
+    scale = float((dhf.abs() * hf.abs()).sum())
+    assert abs(a - bb) <= 2.0 ** -8 * scale + 1e-4 * max(abs(a), abs(bb)), (a, bb, scale)
     assert torch.isfinite(gw).all() and torch.isfinite(out["grad_hidden"].float()).all()
 
 
@@ -165,9 +179,12 @@ def test_reduced_tokens_full_vocab_grad_weight_rows():
                                       [0, w.vocab - 1]]))
     o_dW = oracle.grad_weight_rows(hd64, Wd, b["tokens"], o_lse, o_g, vrows)
     dW = host64(out["grad_weight"][torch.from_numpy(vrows).cuda()])
-    assert norm_rel(dW, o_dW) <= GRAD_TOL, norm_rel(dW, o_dW)
+    m = b["mask"].astype(bool)
+    _, dW_b = rounding_bounds(hd64, Wd, np.where(m, o_g, 0.0), vrows=vrows)
+    tols = row_tolerances(dW_b, o_dW)
+    assert norm_rel(dW, o_dW) <= tols.max(), norm_rel(dW, o_dW)
     for i in range(len(vrows)):
-        assert norm_rel(dW[i], o_dW[i]) <= 4 * GRAD_TOL, (vrows[i], norm_rel(dW[i], o_dW[i]))
+        assert norm_rel(dW[i], o_dW[i]) <= tols[i], (vrows[i], norm_rel(dW[i], o_dW[i]), tols[i])
 
 
 def test_ragged_equal_groups_zero_gradient():
@@ -191,8 +208,10 @@ def test_ragged_equal_groups_zero_gradient():
     assert torch.all(out["grad_hidden"][:len(eq_rows)] == 0)
     o = oracle.grpo_loss(hd64, Wd, b["tokens"], b["mask"], b["cu_seqlens"], old.astype(np.float64),
                          old.astype(np.float64), adv.astype(np.float64), w.clip_eps, 0.0)
-    assert norm_rel(host64(out["grad_weight"]), o["dW"]) <= GRAD_TOL
-    assert norm_rel(host64(out["grad_hidden"]), o["dh"]) <= GRAD_TOL
+    tol_dh, tol_dW = grad_tolerances(hd64, Wd, np.where(b["mask"].astype(bool), o["g"], 0.0),
+                                     o["dh"], o["dW"])
+    assert norm_rel(host64(out["grad_weight"]), o["dW"]) <= tol_dW
+    assert norm_rel(host64(out["grad_hidden"]), o["dh"]) <= tol_dh + BF16_OUT
 
 
 def test_double_scoring_sequence():
@@ -224,8 +243,9 @@ def test_double_scoring_sequence():
     c, seq = _seq_weights(b, w.num_seqs)
     abs_sum = float(np.sum(c[seq] * np.abs(o["ell"])))
     assert abs(out["loss"].item() - o["loss"]) <= TOL * max(abs(o["loss"]), abs_sum)
-    assert norm_rel(host64(out["grad_weight"]), o["dW"]) <= GRAD_TOL
-    assert norm_rel(host64(out["grad_hidden"]), o["dh"]) <= GRAD_TOL
+    tol_dh, tol_dW = grad_tolerances(h64, oracle.decode(Wp, "bf16"), o["g"], o["dh"], o["dW"])
+    assert norm_rel(host64(out["grad_weight"]), o["dW"]) <= tol_dW
+    assert norm_rel(host64(out["grad_hidden"]), o["dh"]) <= tol_dh + BF16_OUT
     # on policy: rho = exp(logp - old) is 1 up to the difference between the
     # device's and the oracle's log-prob
     rho = np.exp(host64(out["logp"]) - old)
@@ -247,11 +267,12 @@ def test_sft_full_size_sampled_rows_and_identities():
     out = grpo.sft_ce_fwd_bwd(hd, Wdv, dev(b["tokens"]), mask, check=True)
     torch.cuda.synchronize()
     assert rel_err(host64(out["logp"])[rows], o_logp) <= TOL
-    o_dh = oracle.grad_hidden_rows(hs, Wd, b["tokens"][rows], o_lse,
-                                   np.full(len(rows), -1.0 / n_valid))
+    g_rows = np.full(len(rows), -1.0 / n_valid)
+    o_dh = oracle.grad_hidden_rows(hs, Wd, b["tokens"][rows], o_lse, g_rows)
     dh = host64(out["grad_hidden"][torch.from_numpy(rows).cuda()])
+    tols = row_tolerances(rounding_bounds(hs, Wd, g_rows, vrows=[])[0], o_dh) + BF16_OUT
     for i in range(len(rows)):
-        assert norm_rel(dh[i], o_dh[i]) <= GRAD_TOL, (i, norm_rel(dh[i], o_dh[i]))
+        assert norm_rel(dh[i], o_dh[i]) <= tols[i], (i, norm_rel(dh[i], o_dh[i]), tols[i])
     del Wd
     # masked rows: zero log-prob and gradient
     m = mask.bool()
@@ -261,14 +282,7 @@ def test_sft_full_size_sampled_rows_and_identities():
     want = -float(out["logp"].double().sum()) / n_valid
     assert abs(out["loss"].item() - want) <= 1e-5 * abs(want)
     # dL/dW identities (as for the GRPO loss, with g_t = -1/n on valid rows)
-    gw = out["grad_weight"]
-    hf = hd.double()
-    colsum = gw.double().sum(0)
-    bound = 2.0 ** -7 * (hf.abs() * m.double()[:, None]).sum(0) / n_valid + 1e-6
-    assert torch.all(colsum.abs() <= bound), float((colsum.abs() / bound).max())
-    a = float((gw.double() * Wdv.double()).sum())
-    bb = float((out["grad_hidden"].double() * hf).sum())
-    assert abs(a - bb) <= 5e-3 * max(abs(a), abs(bb)), (a, bb)
+    _grad_weight_identities(out, hd, Wdv, dlogp=-m.double() / n_valid)
 
 
 
@@ -306,9 +320,10 @@ def test_ragged_full_size_sampled_rows_and_identities():
     assert np.max(np.abs(g - o_g)) <= TOL * np.max(np.abs(o_g))
     o_dh = oracle.grad_hidden_rows(hs, Wd, b["tokens"][rows], o_lse, o_g)
     dh = host64(out["grad_hidden"][torch.from_numpy(rows).cuda()])
+    tols = row_tolerances(rounding_bounds(hs, Wd, o_g, vrows=[])[0], o_dh) + BF16_OUT
     for i in range(len(rows)):
         if np.linalg.norm(o_dh[i]) > 0:  # rows of all-equal groups have g = 0
-            assert norm_rel(dh[i], o_dh[i]) <= GRAD_TOL, (i, norm_rel(dh[i], o_dh[i]))
+            assert norm_rel(dh[i], o_dh[i]) <= tols[i], (i, norm_rel(dh[i], o_dh[i]), tols[i])
     del Wd
     mb = mask_d.bool()
     assert out["logp"][~mb].abs().max().item() == 0.0
@@ -318,15 +333,17 @@ def test_ragged_full_size_sampled_rows_and_identities():
     gt = out["dlogp"].double()
     colsum = gw.double().sum(0)
     bound = torch.zeros_like(colsum)
-    bb = 0.0
+    bb = scale = 0.0
     for r0 in range(0, N, 1 << 16):
         hc = hd[r0:r0 + (1 << 16)].double()
+        dhc = out["grad_hidden"][r0:r0 + (1 << 16)].double()
         bound += (hc.abs() * gt[r0:r0 + (1 << 16)].abs()[:, None]).sum(0)
-        bb += float((out["grad_hidden"][r0:r0 + (1 << 16)].double() * hc).sum())
-    bound = 2.0 ** -7 * bound + 1e-6
+        bb += float((dhc * hc).sum())
+        scale += float((dhc.abs() * hc.abs()).sum())
+    bound = 2.0 ** -8 * bound + 1e-7
     assert torch.all(colsum.abs() <= bound), float((colsum.abs() / bound).max())
     a = float((gw.double() * Wdv.double()).sum())
-    assert abs(a - bb) <= 5e-3 * max(abs(a), abs(bb)), (a, bb)
+    assert abs(a - bb) <= 2.0 ** -8 * scale + 1e-4 * max(abs(a), abs(bb)), (a, bb, scale)
     assert torch.isfinite(gw).all()
 
 
@@ -367,6 +384,9 @@ def test_double_scoring_full_size_sampled_rows():
     assert np.max(np.abs(g - o_g)) <= TOL * np.max(np.abs(o_g))
     o_dh = oracle.grad_hidden_rows(hs, Wpo, b["tokens"][rows], o_lse_p, o_g)
     dh = host64(out["grad_hidden"][torch.from_numpy(rows).cuda()])
+    tols = row_tolerances(rounding_bounds(hs, Wpo, o_g, vrows=[])[0], o_dh) + BF16_OUT
     for i in range(len(rows)):
-        assert norm_rel(dh[i], o_dh[i]) <= GRAD_TOL, (i, norm_rel(dh[i], o_dh[i]))
-    assert torch.isfinite(out["grad_weight"]).all()
+        assert norm_rel(dh[i], o_dh[i]) <= tols[i], (i, norm_rel(dh[i], o_dh[i]), tols[i])
+    del Wpo
+    # dL/dW identities, as for the fwd+bwd workload
+    _grad_weight_identities(out, hd, Wpd)
