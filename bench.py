@@ -31,8 +31,24 @@ if ROOT not in sys.path:
 
 METRIC = "rollout tokens/sec for fused log-prob + GRPO loss fwd+bwd; % bf16 MFMA peak"
 METRIC_SFT = "supervised tokens/sec for fused LM-head cross-entropy fwd+bwd (SFT stage); % bf16 MFMA peak"
-PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA, the published figure (roofline peak)
+# the same peak from the unit counts: 256 CUs x 4096 bf16 flop/clock x 2.4 GHz; the
+# step's MFMA fractions are taken against this, the larger of the two
+PEAK_BF16_UNITS_TFLOPS = 256 * 4096 * 2.4e9 / 1e12
 PEAK_HBM_GBS = 8000.0
+
+
+def host_cpu() -> dict:
+    """Model name and online core count of the host that ran the CPU leg."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"cpu_model": model, "nproc": os.cpu_count()}
 
 
 def _to_dev_bf16(bits, torch):
@@ -117,7 +133,7 @@ def cpu_baseline(w, W_bits, h_bits, batch, adv, old, ref, sample_tokens: int):
     return {"value": len(rows) / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{len(rows)} valid tokens of {w.name} at H={w.hidden}, V={w.vocab}: "
                       f"scoring, loss terms, dL/dh rows and their dL/dW over all V rows "
-                      f"({dt:.1f} s)"}
+                      f"({dt:.1f} s)", **host_cpu()}
 
 
 def bench_adamw(args):
@@ -191,7 +207,8 @@ def bench_adamw(args):
         dt = time.perf_counter() - t0
         res["cpu_baseline"] = {"value": reps * k / dt, "unit": "params/s", "cores": 1,
                                "kind": "oracle",
-                               "sample": f"{reps} oracle steps on {k} parameters ({dt:.1f} s)"}
+                               "sample": f"{reps} oracle steps on {k} parameters ({dt:.1f} s)",
+                               **host_cpu()}
     else:
         res["cpu_baseline"] = None
     print(json.dumps(res), flush=True)
@@ -261,7 +278,7 @@ def bench_rule_reward(args):
         res["cpu_baseline"] = {"value": reps * len(texts) / dt, "unit": "completions/s",
                                "cores": 1, "kind": "oracle",
                                "sample": f"{reps} passes of the oracle over the same {len(texts)} "
-                                         f"completions ({dt:.1f} s)"}
+                                         f"completions ({dt:.1f} s)", **host_cpu()}
     else:
         res["cpu_baseline"] = None
     print(json.dumps(res), flush=True)
@@ -270,7 +287,7 @@ def bench_rule_reward(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="fwdbwd_bf16",
                     choices=["fwdbwd_bf16", "fwd_bf16", "ragged_bf16", "double_bf16",
@@ -389,18 +406,20 @@ def main():
 
     grpo.profile_reset()
     grpo.profile_enable(True)
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+    # one event per step boundary, on the stream the library launches on
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    e0.record()
-    for _ in range(args.steps):
+    ev[0].record()
+    for i in range(args.steps):
         step()
-    e1.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
     grpo.profile_enable(False)
-    total_ms = e0.elapsed_time(e1)
+    total_ms = ev[0].elapsed_time(ev[-1])
+    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
     prof = grpo.profile_read()
     ms_per_step = total_ms / args.steps
+    ms_median = float(np.median(step_ms))
     tokens_per_s = n_valid / (ms_per_step / 1e3)
     log(json.dumps(prof))
 
@@ -425,8 +444,8 @@ def main():
     executed = {"fwd_bf16": 2, "fwdbwd_bf16": 8, "ragged_bf16": 8, "double_bf16": 10,
                 "sft_bf16": 8}[args.workload]
     step_s = ms_per_step / 1e3
-    alg_frac = per_tok * n_valid * V * H / step_s / (PEAK_BF16_TFLOPS * 1e12)
-    exe_frac = executed * n_valid * V * H / step_s / (PEAK_BF16_TFLOPS * 1e12)
+    alg_frac = per_tok * n_valid * V * H / step_s / (PEAK_BF16_UNITS_TFLOPS * 1e12)
+    exe_frac = executed * n_valid * V * H / step_s / (PEAK_BF16_UNITS_TFLOPS * 1e12)
 
     res = {
         "metric": METRIC_SFT if sft else METRIC,
@@ -449,6 +468,10 @@ def main():
                    {"workload": w.name, "prompts": w.prompts, "group": w.group,
                     "seq_len": w.seq_len, "valid_tokens": n_valid, "hidden": H, "vocab": V,
                     "clip_eps": w.clip_eps, "beta": w.beta}),
+        "ms_per_step_median": ms_median,
+        "value_median": n_valid / (ms_median / 1e3),
+        "step_ms": step_ms,
+        "mfma_peak_tflops": PEAK_BF16_UNITS_TFLOPS,
         "mfma_frac_algorithmic": alg_frac,
         "mfma_frac_executed": exe_frac,
         "roofline": roofline,

@@ -60,6 +60,11 @@ typedef enum grpo_status {
   GRPO_ERR_SEQLENS = 10     /* (device) cu_seqlens not monotone from 0 to N */
 } grpo_status;
 
+/* GRPO_BF16 is the production path (MFMA contractions). GRPO_F32 is an
+ * exact-arithmetic parity path for small problems (e.g. H = 64, V = 1000):
+ * plain fp32 FMA loops, no matrix cores, H <= 8192, and dL/dweight re-reads
+ * every valid hidden row once per vocabulary row (O(V * N * H) loads), so
+ * its cost grows far faster than the bf16 path's. */
 typedef enum grpo_dtype {
   GRPO_F32 = 0, /* IEEE binary32 */
   GRPO_BF16 = 1 /* bfloat16; fp32 accumulation, round-to-nearest-even stores */
@@ -94,7 +99,8 @@ typedef enum grpo_op {
  *   rewards  [num_prompts * group_size] fp32, prompt-major (the G rollouts
  *            of one prompt contiguous). Device.
  *   adv      [num_prompts * group_size] fp32 output, same order. Device.
- * Requires num_prompts >= 1, group_size >= 2, std_eps >= 0 (and finite).
+ * Requires 1 <= num_prompts <= 4 * (2^24 - 1) (one wave per prompt; the
+ * grid stays below 2^32 threads), group_size >= 2, std_eps >= 0 (and finite).
  * Computed in fp32 with a fixed reduction order (bitwise reproducible).
  */
 grpo_status group_advantages(const float* rewards, int64_t num_prompts, int32_t group_size,
@@ -156,7 +162,11 @@ grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weig
  *   loss  = sum_b c_b * sum_{valid t in b} ell_t     (c_b from `agg`, see grpo_agg)
  * and the exact gradients dL/dhidden, dL/dweight through the log-softmax.
  * A tie rho*A == clip(rho)*A takes the unclipped branch; the clipped branch
- * has zero slope.
+ * has zero slope. With bf16 the logits gradient g_t (1[v = y_t] - p_tv) enters
+ * the matrix-core products as -g_t p_tv rounded to bf16, and the sampled id's
+ * g_t is applied in fp32 (to dL/dhidden_t as g_t * weight_{y_t}, to
+ * dL/dweight_{y_t} as a fixed-order sum of g_t * hidden_t), so the gradients'
+ * error is that of the bf16 rounding of the small -g p terms.
  *
  *   dt, hidden, weight, tokens, mask, N, H, V   as grpo_logprob_fwd.
  *   cu_seqlens [num_seqs + 1] int64. Device.
@@ -255,19 +265,21 @@ grpo_status adamw_step(float* weight, float* exp_avg, float* exp_avg_sq, const f
  * run, "]", blanks, "(". Strings and comments are not otherwise parsed.
  *   text        the completions' bytes, concatenated; 16-byte aligned.
  *               Device.
+ *   text_bytes  bytes readable at text (>= 0); nothing beyond is read.
  *   offsets     [num_completions + 1] int64: completion b is
- *               text[offsets[b], offsets[b+1]); a decreasing pair counts as
- *               an empty completion. Device.
+ *               text[offsets[b], offsets[b+1]); a decreasing pair, or one
+ *               with an offset outside [0, text_bytes], counts as an empty
+ *               completion. Device.
  *   test_passed [num_completions] u8, nonzero = the execution harness's
  *               tests passed (that harness is outside this library). Device.
  *   is_triton   [num_completions] u8 output (0/1). Device.
  *   reward      [num_completions] fp32 output, the input of
  *               group_advantages. Device.
- * Requires require_launch, weighted in {0, 1}, finite weights. Enqueued on
- * `stream`, no workspace; num_completions = 0 does nothing (no pointer is
- * read).
+ * Requires require_launch, weighted in {0, 1}, finite weights, text_bytes
+ * >= 0. Enqueued on `stream`, no workspace; num_completions = 0 does nothing
+ * (no pointer is read).
  */
-grpo_status triton_rule_reward(const uint8_t* text, const int64_t* offsets,
+grpo_status triton_rule_reward(const uint8_t* text, int64_t text_bytes, const int64_t* offsets,
                                int64_t num_completions, const uint8_t* test_passed,
                                int32_t require_launch, int32_t weighted, float rule_weight,
                                float exec_weight, uint8_t* is_triton, float* reward,

@@ -406,17 +406,6 @@ void launch_token_objective(const TokenArgs& a, hipStream_t s) {
 }
 
 // Zero the g of packed slots beyond the valid count (so padding contributes 0).
-__global__ void k_zero_tail(float* __restrict__ g_p, int64_t Npad, const WsHeader* hdr) {
-  int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (j < Npad && j >= hdr->num_valid) g_p[j] = 0.f;
-}
-void launch_zero_tail(float* g_p, int64_t Npad, const WsHeader* hdr, hipStream_t s) {
-  hipLaunchKernelGGL(k_zero_tail, dim3((unsigned)ceil_div(Npad, 256)), dim3(256), 0, s, g_p, Npad,
-                     hdr);
-}
-
-// z at the sampled id when the log-sum-exp is supplied by the caller: one
-// wave per packed token, fp32 accumulation of bf16 products.
 __global__ void __launch_bounds__(256) k_gather_dot_bf16(const uint16_t* __restrict__ hidden,
                                                          const uint16_t* __restrict__ W, int64_t H,
                                                          const int32_t* __restrict__ rows_p,

@@ -41,7 +41,26 @@ Prof& prof() {
   return p;
 }
 
-// Runs `launch` bracketed by events when timing is on.
+// Folds finished event pairs into the per-kind totals (waits for them).
+// Caller holds p.mu.
+grpo_status fold_records(Prof& p) {
+  for (auto& r : p.recs) {
+    if (hipEventSynchronize(r.b) != hipSuccess) return GRPO_ERR_HIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return GRPO_ERR_HIP;
+    p.launches[r.kind] += 1;
+    p.ms[r.kind] += ms;
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  p.recs.clear();
+  return GRPO_OK;
+}
+constexpr size_t kMaxPendingRecords = 4096;  // event pairs held before they are folded
+
+// Runs `launch` bracketed by events when timing is on. A launch failure is
+// told apart from an error the calling thread had already left pending: the
+// last-error state is only peeked at, and consumed only when it is ours.
 template <class F>
 grpo_status timed(int kind, hipStream_t s, F&& launch) {
   Prof& p = prof();
@@ -55,12 +74,17 @@ grpo_status timed(int kind, hipStream_t s, F&& launch) {
     if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return GRPO_ERR_HIP;
     if (hipEventRecord(a, s) != hipSuccess) return GRPO_ERR_HIP;
   }
+  const hipError_t before = hipPeekAtLastError();
   launch();
-  if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+  if (before == hipSuccess && hipPeekAtLastError() != hipSuccess) {
+    (void)hipGetLastError();
+    return GRPO_ERR_HIP;
+  }
   if (on) {
     if (hipEventRecord(b, s) != hipSuccess) return GRPO_ERR_HIP;
     std::lock_guard<std::mutex> g(p.mu);
     p.recs.push_back({kind, a, b});
+    if (p.recs.size() >= kMaxPendingRecords) return fold_records(p);
   }
   return GRPO_OK;
 }
@@ -89,6 +113,7 @@ grpo_status check_device() {
 // --------------------------------------------------------- workspace
 constexpr size_t kAlign = 256;
 constexpr int64_t kPackSeg = 4096;  // rows per packing workgroup without cu_seqlens
+constexpr int64_t kMaxAdvPrompts = 4 * ((1ll << 24) - 1);  // group_advantages' grid limit
 #ifndef GRPO_DZ_BUDGET_GIB
 #define GRPO_DZ_BUDGET_GIB 48
 #endif
@@ -529,7 +554,10 @@ grpo_status group_advantages(const float* rewards, int64_t num_prompts, int32_t 
                              float std_eps, int32_t unbiased_std, float* adv,
                              hipStream_t stream) {
   if (!rewards || !adv) return GRPO_ERR_NULL;
-  if (num_prompts < 1 || group_size < 2 || num_prompts > (1ll << 40) / group_size)
+  // one wave per prompt, four per 256-thread workgroup: the grid's thread
+  // count stays below 2^32
+  if (num_prompts < 1 || group_size < 2 || num_prompts > (1ll << 40) / group_size ||
+      num_prompts > kMaxAdvPrompts)
     return GRPO_ERR_SHAPE;
   if (!(std_eps >= 0.f) || isinf(std_eps)) return GRPO_ERR_PARAM;
   TRY(check_device());
@@ -752,12 +780,13 @@ grpo_status adamw_step(float* weight, float* exp_avg, float* exp_avg_sq, const f
   return timed(K_ADAMW, stream, [&] { launch_adamw(a, stream); });
 }
 
-grpo_status triton_rule_reward(const uint8_t* text, const int64_t* offsets,
+grpo_status triton_rule_reward(const uint8_t* text, int64_t text_bytes, const int64_t* offsets,
                                int64_t num_completions, const uint8_t* test_passed,
                                int32_t require_launch, int32_t weighted, float rule_weight,
                                float exec_weight, uint8_t* is_triton, float* reward,
                                hipStream_t stream) {
-  if (num_completions < 0 || num_completions > 0x7fffffff) return GRPO_ERR_SHAPE;
+  if (num_completions < 0 || num_completions > 0x7fffffff || text_bytes < 0)
+    return GRPO_ERR_SHAPE;
   if ((require_launch != 0 && require_launch != 1) || (weighted != 0 && weighted != 1) ||
       !isfinite(rule_weight) || !isfinite(exec_weight))
     return GRPO_ERR_PARAM;
@@ -767,6 +796,7 @@ grpo_status triton_rule_reward(const uint8_t* text, const int64_t* offsets,
   TRY(check_device());
   RewardArgs a;
   a.text = text;
+  a.text_bytes = text_bytes;
   a.offsets = offsets;
   a.test_passed = test_passed;
   a.require_launch = require_launch;
@@ -827,17 +857,7 @@ grpo_status grpo_profile_query(int32_t kind, int64_t* launches, double* total_ms
   if (!launches || !total_ms) return GRPO_ERR_NULL;
   Prof& p = prof();
   std::lock_guard<std::mutex> g(p.mu);
-  // fold finished records into the totals
-  for (auto& r : p.recs) {
-    if (hipEventSynchronize(r.b) != hipSuccess) return GRPO_ERR_HIP;
-    float ms = 0.f;
-    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return GRPO_ERR_HIP;
-    p.launches[r.kind] += 1;
-    p.ms[r.kind] += ms;
-    (void)hipEventDestroy(r.a);
-    (void)hipEventDestroy(r.b);
-  }
-  p.recs.clear();
+  TRY(fold_records(p));
   *launches = p.launches[kind];
   *total_ms = p.ms[kind];
   return GRPO_OK;

@@ -142,7 +142,8 @@ void launch_sum_splits(const float* part, int splits, int64_t stride, int64_t ld
 // ------------------------------------------------------------ rule reward
 struct RewardArgs {
   const uint8_t* text;         // completions, concatenated
-  const int64_t* offsets;      // [count + 1]
+  int64_t text_bytes;          // readable bytes at text
+  const int64_t* offsets;      // [count + 1]; pairs outside [0, text_bytes] are empty
   const uint8_t* test_passed;  // [count]
   int require_launch;          // is_Triton also needs a launch of the kernel
   int weighted;                // reward = w_rule*is_Triton + w_exec*passed (else the product)
@@ -166,7 +167,6 @@ void launch_rows_out(const int32_t* pidx, int64_t N, const float* logp_p, const 
 void launch_gather_dot_bf16(const uint16_t* hidden, const uint16_t* W, int64_t H,
                             const int32_t* rows_p, const int32_t* y_p, const WsHeader* hdr,
                             float* zy, int64_t Nmax, hipStream_t s);
-void launch_zero_tail(float* g_p, int64_t Npad, const WsHeader* hdr, hipStream_t s);
 // Tiled layout of rows of `in` (row i = in[rows ? rows[i] : i], K columns):
 // r_pad x round_up(K, 32), rows >= the valid count (hdr->num_valid, else
 // n_static) and columns >= K zero; tile-rows `stride` blocks apart.

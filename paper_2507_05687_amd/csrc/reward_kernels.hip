@@ -501,7 +501,9 @@ __global__ void __launch_bounds__(kRrThreads) k_rule_reward(RewardArgs a) {
   __shared__ RrShared sh;
   const int64_t b = blockIdx.x;
   const int tid = threadIdx.x;
-  const int64_t s0 = a.offsets[b], s1 = a.offsets[b + 1];
+  // a pair outside [0, text_bytes] is an empty completion, like a decreasing one
+  int64_t s0 = a.offsets[b], s1 = a.offsets[b + 1];
+  if (s0 < 0 || s1 < 0 || s0 > a.text_bytes || s1 > a.text_bytes) s0 = s1 = 0;
   const int64_t n = s1 > s0 ? s1 - s0 : 0;
   if (tid == 0) {
     sh.count = 0;

@@ -40,7 +40,8 @@ SIGNATURES = {
                               _vp, _i32, _vp, _sz, _vp]),
     "adamw_step": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _f32, _f32, _f32, _f32, _f32, _i64,
                           _vp]),
-    "triton_rule_reward": (_i32, [_vp, _vp, _i64, _vp, _i32, _i32, _f32, _f32, _vp, _vp, _vp]),
+    "triton_rule_reward": (_i32, [_vp, _i64, _vp, _i64, _vp, _i32, _i32, _f32, _f32, _vp, _vp,
+                               _vp]),
     "grpo_workspace_bytes": (_sz, [_i32, _i32, _i64, _i64, _i64, _i64]),
     "grpo_check_error": (_i32, [_vp, _vp]),
     "grpo_status_string": (ctypes.c_char_p, [_i32]),
@@ -384,9 +385,10 @@ def triton_rule_reward(text, offsets, test_passed, require_launch: bool = False,
         raise ValueError("offsets must have one entry more than test_passed")
     flags = torch.empty(b, dtype=torch.uint8, device=text.device)
     reward = torch.empty(b, dtype=torch.float32, device=text.device)
-    if text.numel() == 0:  # every completion is empty: any valid pointer will do
+    nbytes = text.numel()
+    if nbytes == 0:  # every completion is empty: any valid pointer will do
         text = torch.zeros(1, dtype=torch.uint8, device=offsets.device)
-    st = load().triton_rule_reward(_ptr(text), _ptr(offsets), b, _ptr(test_passed),
+    st = load().triton_rule_reward(_ptr(text), nbytes, _ptr(offsets), b, _ptr(test_passed),
                                    int(require_launch), int(weighted), rule_weight, exec_weight,
                                    _ptr(flags), _ptr(reward), _stream())
     _check(st, "triton_rule_reward")

@@ -120,6 +120,8 @@ def test_other_entry_point_errors(lib):
     assert adv(P, 2, 1, 1e-6, 1, P, NULL) == 2
     assert adv(P, 0, 4, 1e-6, 1, P, NULL) == 2
     assert adv(P, 2, 4, -1.0, 1, P, NULL) == 4
+    # one wave per prompt: the grid's thread count must stay below 2^32
+    assert adv(P, 4 * ((1 << 24) - 1) + 1, 2, 1e-6, 1, P, NULL) == 2
     fwd = lib.grpo_logprob_fwd
     assert fwd(1, NULL, P, P, NULL, 8, 64, 100, P, P, P, 1 << 30, NULL) == 1
     assert fwd(1, P, P, P, NULL, 8, 12, 100, P, P, P, 1 << 30, NULL) == 2
@@ -183,28 +185,29 @@ def test_adamw_argument_errors(lib):
 
 def test_rule_reward_argument_errors(lib):
     f = lib.triton_rule_reward
-    a = [P, P, 4, P, 0, 0, 0.0, 0.0, P, P, NULL]
+    a = [P, 64, P, 4, P, 0, 0, 0.0, 0.0, P, P, NULL]
 
     def call(i, x):
         b = list(a)
         b[i] = x
         return f(*b)
 
-    assert call(2, -1) == 2                  # count
-    assert call(2, 1 << 31) == 2
+    assert call(3, -1) == 2                  # count
+    assert call(3, 1 << 31) == 2
+    assert call(1, -1) == 2                  # text_bytes
     assert call(0, NULL) == 1
-    assert call(1, NULL) == 1
-    assert call(3, NULL) == 1
-    assert call(8, NULL) == 1
+    assert call(2, NULL) == 1
+    assert call(4, NULL) == 1
     assert call(9, NULL) == 1
-    assert call(4, 2) == 4                   # require_launch
-    assert call(5, -1) == 4                  # weighted
-    assert call(6, float("nan")) == 4
-    assert call(7, float("inf")) == 4
+    assert call(10, NULL) == 1
+    assert call(5, 2) == 4                   # require_launch
+    assert call(6, -1) == 4                  # weighted
+    assert call(7, float("nan")) == 4
+    assert call(8, float("inf")) == 4
     assert call(0, ctypes.c_void_p(0x1008)) == 5   # text not 16-byte aligned
-    assert call(1, ctypes.c_void_p(0x1004)) == 5
-    assert call(2, 0) == 0                   # nothing to do: no launch, no device needed
-    assert f(NULL, NULL, 0, NULL, 0, 0, 0.0, 0.0, NULL, NULL, NULL) == 0
+    assert call(2, ctypes.c_void_p(0x1004)) == 5
+    assert call(3, 0) == 0                   # nothing to do: no launch, no device needed
+    assert f(NULL, 0, NULL, 0, NULL, 0, 0, 0.0, 0.0, NULL, NULL, NULL) == 0
 
 
 def test_profile_interface_without_launches(lib):
@@ -232,3 +235,4 @@ def test_binding_rejects_host_tensors():
     bf = torch.zeros(4, 8, dtype=torch.bfloat16)
     with pytest.raises(ValueError, match="device tensor"):
         grpo.logprob_fwd(bf, bf, torch.zeros(4, dtype=torch.int64))
+

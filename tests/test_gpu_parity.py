@@ -377,6 +377,26 @@ def test_token_out_of_range_sets_flag():
     _run_loss(w, W, h, b, adv, old, ref)
 
 
+def test_bf16_token_out_of_range_without_mask_zeroes_its_row():
+    # a row whose id is outside [0, V) is dropped by packing even without a
+    # mask: its dL/dh row is exactly 0 (as its logp and loss terms) and the
+    # call reports the bad id
+    kw = dict(SMALL["k_tail"], dtype="bf16", rms_norm_hidden=True, seed=19)
+    w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    b["tokens"][5] = w.vocab
+    out = grpo.loss_fwd_bwd(to_dev(h, "bf16"), to_dev(W, "bf16"), dev(b["tokens"]), None,
+                            dev(b["cu_seqlens"]), dev(old), dev(ref), dev(adv), w.clip_eps,
+                            w.beta)
+    torch.cuda.synchronize()
+    assert torch.all(out["grad_hidden"][5] == 0)
+    assert out["logp"][5].item() == 0 and out["token_loss"][5].item() == 0
+    assert out["grad_hidden"][4].float().abs().sum().item() > 0
+    with pytest.raises(grpo.GrpoError) as e:
+        grpo.check_error(grpo.workspace(grpo.workspace_bytes(
+            grpo.OP_LOSS_FWD_BWD, grpo.BF16, w.num_tokens, w.hidden, w.vocab, w.num_seqs)))
+    assert e.value.status == 9
+
+
 def test_all_rows_masked():
     """No valid row at all: loss, per-token outputs and both gradients are 0
     (the weight-gradient contraction then has K = 0)."""

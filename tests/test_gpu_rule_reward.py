@@ -144,3 +144,24 @@ def test_reward_feeds_group_advantages():
     _, want_r = oracle.rule_rewards(texts, passed)
     want = oracle.advantages(want_r.astype(np.float64), 8)
     assert np.max(np.abs(adv - want)) <= 1e-5 * max(1.0, np.max(np.abs(want)))
+
+
+def test_offsets_outside_the_text_are_empty_completions():
+    # pairs reaching before the text or past text_bytes count as empty
+    # completions (no byte outside the buffer is read), as decreasing ones do
+    good = b"@triton.jit\ndef k(x):\n    pass\nk[(1,)](x)\n"
+    data, offsets = workloads.pack_completions([good, good])
+    n = len(data)
+    bad = np.array([0, len(good), -16, n + 64, 3, 1 << 40], dtype=np.int64)
+    offs = np.concatenate([offsets, bad])
+    # completions: good, good, [n, 0) decreasing, [0, len) good again,
+    # [len, -16) and [-16, n+64) and [n+64, 3) and [3, 2^40) outside the text
+    passed = np.ones(len(offs) - 1, np.uint8)
+    flags, reward = grpo.triton_rule_reward(torch.from_numpy(data).cuda(),
+                                            torch.from_numpy(offs).cuda(),
+                                            torch.from_numpy(passed).cuda(), require_launch=True,
+                                            weighted=True, rule_weight=0.25, exec_weight=0.5)
+    torch.cuda.synchronize()
+    f = flags.cpu().numpy()
+    assert list(f) == [1, 1, 0, 1, 0, 0, 0, 0]
+    assert np.allclose(reward.cpu().numpy(), np.where(f == 1, 0.75, 0.5))
