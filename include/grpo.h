@@ -127,6 +127,24 @@ grpo_status grpo_pack_valid(const uint8_t* mask, const int64_t* cu_seqlens, int6
                             void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * grpo_pack_valid_static -- grpo_pack_valid for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same outputs, with the scratch (error words,
+ * valid count, per-rollout offsets) in a static device array of the library
+ * instead of a caller workspace. No allocation of any kind.
+ *   mask, cu_seqlens, num_seqs, N, rows, counts, num_valid  as grpo_pack_valid.
+ *   error_out  [1] int32 output or NULL: GRPO_ERR_SEQLENS if cu_seqlens was
+ *              not monotone from 0 to N (those rollouts count as empty), else
+ *              0. Device.
+ * Limit: num_seqs <= 2^20 (GRPO_ERR_WORKSPACE above). Every call on one GPU
+ * shares that GPU's array: calls that overlap on a GPU (other streams or
+ * threads) race and must be ordered by the caller.
+ */
+grpo_status grpo_pack_valid_static(const uint8_t* mask, const int64_t* cu_seqlens,
+                                   int64_t num_seqs, int64_t N, int32_t* rows, int32_t* counts,
+                                   int32_t* num_valid, int32_t* error_out, hipStream_t stream);
+
+/*
  * grpo_logprob_fwd -- the policy probability inside the ratio of Eq. 1,
  * pi_theta(o_t | q, o_<t): for each valid row t,
  *   z_{t,v} = <hidden_t, weight_v>              (all v in [0, V))

@@ -228,6 +228,16 @@ __global__ void k_reset_flags(WsHeader* hdr) {
   hdr->err_seqlens = 0;
 }
 
+// status of the most recent call on the workspace header: GRPO_ERR_SEQLENS
+// (10), GRPO_ERR_TOKEN_RANGE (9) or 0
+__global__ void k_copy_status(const WsHeader* hdr, int32_t* out) {
+  *out = hdr->err_seqlens ? 10 : hdr->err_token ? 9 : 0;
+}
+
+void launch_copy_status(const WsHeader* hdr, int32_t* out, hipStream_t s) {
+  hipLaunchKernelGGL(k_copy_status, dim3(1), dim3(1), 0, s, hdr, out);
+}
+
 void launch_pack(const PackArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_reset_flags, dim3(1), dim3(1), 0, s, a.hdr);
   if (a.pidx) {

@@ -110,6 +110,33 @@ grpo_status check_device() {
   return checked[dev] == 1 ? GRPO_OK : GRPO_ERR_DEVICE;
 }
 
+// --------------------------------------------------------- static scratch
+// grpo_pack_valid_static's scratch: the workspace header (error words and the
+// valid count) and the per-rollout offsets, in a file-scope device array that
+// every GPU the library runs on holds until the process ends. Host code uses
+// the array only through the device address hipGetSymbolAddress returns for
+// the current device (kept per device); the array's name is not a device
+// address in host code.
+constexpr int64_t kStaticMaxSeqs = 1 << 20;  // rollouts per call
+constexpr size_t kStaticScratchBytes = 256 + 4 * ((size_t)kStaticMaxSeqs + 64);
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
+grpo_status static_scratch(char** out) {
+  static std::mutex mu;
+  static char* addr[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return GRPO_ERR_DEVICE;
+  std::lock_guard<std::mutex> g(mu);
+  if (addr[dev] == nullptr) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr)
+      return GRPO_ERR_HIP;
+    addr[dev] = (char*)ptr;
+  }
+  *out = addr[dev];
+  return GRPO_OK;
+}
+
 // --------------------------------------------------------- workspace
 constexpr size_t kAlign = 256;
 constexpr int64_t kPackSeg = 4096;  // rows per packing workgroup without cu_seqlens
@@ -576,6 +603,37 @@ grpo_status grpo_pack_valid(const uint8_t* mask, const int64_t* cu_seqlens, int6
   TRY(check_device());
   return run_pack(L, workspace, mask, nullptr, 1, cu_seqlens, num_seqs, N, rows, counts,
                   num_valid, stream);
+}
+
+grpo_status grpo_pack_valid_static(const uint8_t* mask, const int64_t* cu_seqlens,
+                                   int64_t num_seqs, int64_t N, int32_t* rows, int32_t* counts,
+                                   int32_t* num_valid, int32_t* error_out, hipStream_t stream) {
+  if (!cu_seqlens || !rows || !counts || !num_valid) return GRPO_ERR_NULL;
+  if (N < 1 || N >= (1ll << 31) - kTile || num_seqs < 1 || num_seqs > N) return GRPO_ERR_SHAPE;
+  if (num_seqs > kStaticMaxSeqs) return GRPO_ERR_WORKSPACE;  // beyond the static scratch
+  TRY(check_device());
+  char* sc = nullptr;
+  TRY(static_scratch(&sc));
+  PackArgs a;
+  a.mask = mask;
+  a.tokens = nullptr;
+  a.V = 1;
+  a.cu = cu_seqlens;
+  a.seg = kPackSeg;
+  a.B = num_seqs;
+  a.N = N;
+  a.counts = counts;
+  a.base = (int32_t*)(sc + 256);
+  a.rows_p = rows;
+  a.seq_p = nullptr;
+  a.y_p = nullptr;
+  a.pidx = nullptr;
+  a.num_valid_out = num_valid;
+  a.hdr = (WsHeader*)sc;
+  TRY(timed(K_PACK, stream, [&] { launch_pack(a, stream); }));
+  if (error_out)
+    return timed(K_PACK, stream, [&] { launch_copy_status(a.hdr, error_out, stream); });
+  return GRPO_OK;
 }
 
 grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weight,

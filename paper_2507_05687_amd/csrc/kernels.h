@@ -70,6 +70,8 @@ struct PackArgs {
   WsHeader* hdr;
 };
 void launch_pack(const PackArgs& a, hipStream_t s);
+// *out = the status code the header's error words stand for (0 if none)
+void launch_copy_status(const WsHeader* hdr, int32_t* out, hipStream_t s);
 
 // ------------------------------------------------ token objective (Eq. 1)
 // objective 0: the GRPO surrogate of Eq. 1; objective 1: the supervised

@@ -31,6 +31,7 @@ _vp, _i64, _i32, _f32, _sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, c
 SIGNATURES = {
     "group_advantages": (_i32, [_vp, _i64, _i32, _f32, _i32, _vp, _vp]),
     "grpo_pack_valid": (_i32, [_vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "grpo_pack_valid_static": (_i32, [_vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp]),
     "grpo_logprob_fwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp, _sz,
                                 _vp]),
     "grpo_loss_fwd_bwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _vp, _vp,

@@ -236,3 +236,12 @@ def test_binding_rejects_host_tensors():
     with pytest.raises(ValueError, match="device tensor"):
         grpo.logprob_fwd(bf, bf, torch.zeros(4, dtype=torch.int64))
 
+
+def test_static_pack_limits_without_a_device(lib):
+    f = lib.grpo_pack_valid_static
+    assert f(NULL, NULL, 4, 100, P, P, P, NULL, NULL) == 1
+    assert f(NULL, P, 4, 100, NULL, P, P, NULL, NULL) == 1
+    assert f(NULL, P, 0, 100, P, P, P, NULL, NULL) == 2
+    assert f(NULL, P, 101, 100, P, P, P, NULL, NULL) == 2
+    # more rollouts than the static scratch holds
+    assert f(NULL, P, (1 << 20) + 1, 1 << 21, P, P, P, NULL, NULL) == 6
