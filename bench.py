@@ -294,6 +294,9 @@ def main():
                              "sft_bf16", "adamw_lmhead", "rule_reward"])
     ap.add_argument("--cpu-sample", type=int, default=128,
                     help="valid tokens timed on the CPU oracle (0 skips the CPU baseline)")
+    ap.add_argument("--scratch-gb", type=float, default=32.0,
+                    help="workspace limit in GB (1e9 bytes): the logits-gradient budget is the "
+                         "largest whole GiB that keeps the workspace within it")
     ap.add_argument("--verbose", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
@@ -350,7 +353,8 @@ def main():
     if sft:
         old = ref = torch.zeros(N, dtype=torch.float32, device="cuda")
     else:
-        base, _ = grpo.logprob_fwd(h, W, tokens, use_mask)
+        base, _ = grpo.logprob_fwd(h, W, tokens, use_mask,
+                                   max_valid=n_valid if use_mask is not None else 0)
         old = base + torch.from_numpy(batch["old_noise"]).cuda()
         ref = base + torch.from_numpy(batch["ref_noise"]).cuda()
         del base
@@ -362,8 +366,21 @@ def main():
     lse_buf = torch.empty(N, **f32)
     old_buf = torch.empty(N, **f32)
     ref_buf = torch.empty(N, **f32)
-    ws_bytes = max(grpo.workspace_bytes(grpo.OP_LOSS_FWD_BWD, grpo.BF16, N, H, V, B),
-                   grpo.workspace_bytes(grpo.OP_LOGPROB_FWD, grpo.BF16, N, H, V, 1))
+    # the valid rows are known on the host (the mask is built there), so the
+    # workspace is sized for them; the logits-gradient budget is the largest
+    # whole GiB (at most the library default of 48) that keeps it within --scratch-gb
+    max_valid = n_valid if use_mask is not None else N
+    op_main = grpo.OP_SFT_FWD_BWD if sft else grpo.OP_LOSS_FWD_BWD
+
+    def ws_need(budget):
+        return max(grpo.workspace_bytes(op_main, grpo.BF16, N, H, V, B, max_valid, budget),
+                   grpo.workspace_bytes(grpo.OP_LOGPROB_FWD, grpo.BF16, N, H, V, 1, max_valid))
+    dz_budget = 48 << 30
+    while dz_budget > (1 << 30) and ws_need(dz_budget) > args.scratch_gb * 1e9:
+        dz_budget -= 1 << 30
+    ws_bytes = ws_need(dz_budget)
+    log(f"workspace {ws_bytes / 1e9:.2f} GB (logits-gradient budget {dz_budget >> 30} GiB, "
+        f"{max_valid} valid rows)")
     ws = grpo.workspace(ws_bytes)
     lib = grpo.load()
     P = grpo._ptr
@@ -373,29 +390,32 @@ def main():
     def step():
         if sft:  # the supervised stage: cross-entropy over the response tokens
             st = lib.sft_ce_fwd_bwd(grpo.BF16, P(h), P(W), P(tokens), mptr, N, H, V, P(loss),
-                                    None, P(gh), grpo.BF16, P(gw), 0, P(ws), ws.numel(), stream)
+                                    None, P(gh), grpo.BF16, P(gw), 0, P(ws), ws.numel(),
+                                    max_valid, dz_budget, stream)
             assert st == 0, st
             return
         st = lib.group_advantages(P(rewards), w.prompts, w.group, 1e-6, 1, P(adv), stream)
         assert st == 0, st
         if args.workload == "fwd_bf16":
             st = lib.grpo_logprob_fwd(grpo.BF16, P(h), P(W), P(tokens), mptr, N, H, V,
-                                      P(old_buf), P(lse_buf), P(ws), ws.numel(), stream)
+                                      P(old_buf), P(lse_buf), P(ws), ws.numel(), max_valid,
+                                      stream)
             assert st == 0, st
             return
         lse_in, o, r = None, old, ref
         if w.double_scoring:  # S8: score under the policy (old) and the reference
             st = lib.grpo_logprob_fwd(grpo.BF16, P(h), P(W), P(tokens), mptr, N, H, V,
-                                      P(old_buf), P(lse_buf), P(ws), ws.numel(), stream)
+                                      P(old_buf), P(lse_buf), P(ws), ws.numel(), max_valid,
+                                      stream)
             assert st == 0, st
             st = lib.grpo_logprob_fwd(grpo.BF16, P(h), P(Wref), P(tokens), mptr, N, H, V,
-                                      P(ref_buf), None, P(ws), ws.numel(), stream)
+                                      P(ref_buf), None, P(ws), ws.numel(), max_valid, stream)
             assert st == 0, st
             lse_in, o, r = lse_buf, old_buf, ref_buf
         st = lib.grpo_loss_fwd_bwd(grpo.BF16, P(h), P(W), P(tokens), mptr, P(cu), B, N, H, V,
                                    P(o), P(r), P(adv), w.clip_eps, w.beta, 0, P(lse_in), P(loss),
                                    None, None, None, None, None, P(gh), grpo.BF16, P(gw), 0,
-                                   P(ws), ws.numel(), stream)
+                                   P(ws), ws.numel(), max_valid, dz_budget, stream)
         assert st == 0, st
 
     for _ in range(args.warmup):
@@ -472,6 +492,8 @@ def main():
         "value_median": n_valid / (ms_median / 1e3),
         "step_ms": step_ms,
         "mfma_peak_tflops": PEAK_BF16_UNITS_TFLOPS,
+        "workspace_gb": ws_bytes / 1e9,
+        "dz_budget_gib": dz_budget >> 30,
         "mfma_frac_algorithmic": alg_frac,
         "mfma_frac_executed": exe_frac,
         "roofline": roofline,

@@ -33,6 +33,15 @@
  *    is nonzero (mask == NULL: every row). Outputs of masked rows are 0.
  *  - Calls on distinct streams are thread-safe. Calls that share a
  *    workspace must be ordered by the caller.
+ *  - Workspace size. max_valid (0 = N) bounds the number of valid rows a
+ *    call will see: the token-indexed scratch is sized for it (a ragged
+ *    batch with half its rows masked needs about half). A call whose mask
+ *    has more valid rows records GRPO_ERR_CAPACITY and treats no row as
+ *    valid (all outputs as for masked rows). dz_budget (0 = 48 GiB) bounds
+ *    the bytes of the logits-gradient chunks of the backward pass; a smaller
+ *    budget means narrower vocabulary chunks and more passes over the fp32
+ *    dL/dhidden accumulator, never a different result. Pass the same values
+ *    to grpo_workspace_bytes and to the call.
  */
 #ifndef GRPO_H_
 #define GRPO_H_
@@ -57,7 +66,8 @@ typedef enum grpo_status {
   GRPO_ERR_DEVICE = 7,      /* no usable gfx950 device */
   GRPO_ERR_HIP = 8,         /* a HIP runtime call failed */
   GRPO_ERR_TOKEN_RANGE = 9, /* (device) a token id was outside [0, V) */
-  GRPO_ERR_SEQLENS = 10     /* (device) cu_seqlens not monotone from 0 to N */
+  GRPO_ERR_SEQLENS = 10,    /* (device) cu_seqlens not monotone from 0 to N */
+  GRPO_ERR_CAPACITY = 11    /* (device) more valid rows than max_valid */
 } grpo_status;
 
 /* GRPO_BF16 is the production path (MFMA contractions). GRPO_F32 is an
@@ -158,8 +168,9 @@ grpo_status grpo_pack_valid_static(const uint8_t* mask, const int64_t* cu_seqlen
  *   hidden    [N, H] dt. Device.       weight [V, H] dt. Device.
  *   tokens    [N] int64 sampled ids.   mask   [N] uint8 or NULL.
  *   logp, lse [N] fp32 outputs (0 on masked rows). Either may be NULL.
- *   workspace >= grpo_workspace_bytes(GRPO_OP_LOGPROB_FWD, dt, N, H, V, 1),
- *             256-byte aligned.
+ *   workspace >= grpo_workspace_bytes(GRPO_OP_LOGPROB_FWD, dt, N, H, V, 1,
+ *             max_valid, 0), 256-byte aligned.
+ *   max_valid 0 (= N) or the most valid rows the mask will have, <= N.
  * Requires N, H, V >= 1, N < 2^31, V < 2^31, H < 2^20; bf16 also needs
  * H % 8 == 0, (ceil(V/256) + 32) * ceil(N/256) < 2^31 and 16-byte aligned
  * hidden/weight; fp32 needs H <= 8192. fp32 arrays are 4-byte aligned.
@@ -167,7 +178,7 @@ grpo_status grpo_pack_valid_static(const uint8_t* mask, const int64_t* cu_seqlen
 grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weight,
                              const int64_t* tokens, const uint8_t* mask, int64_t N, int64_t H,
                              int64_t V, float* logp, float* lse, void* workspace,
-                             size_t workspace_bytes, hipStream_t stream);
+                             size_t workspace_bytes, int64_t max_valid, hipStream_t stream);
 
 /*
  * grpo_loss_fwd_bwd -- loss = -J of Eq. 1 (AutoTriton Sec. 3.3) and its
@@ -203,7 +214,8 @@ grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weig
  *               dt == GRPO_BF16). Zero rows where masked.
  *   grad_weight [V, H] fp32: overwritten, or added to when
  *               accumulate_grad_weight != 0.
- * workspace >= grpo_workspace_bytes(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, num_seqs).
+ * workspace >= grpo_workspace_bytes(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, num_seqs,
+ * max_valid, dz_budget) (see the workspace-size convention above).
  * Sizes as grpo_logprob_fwd, and for bf16 N <= 2^22 (4,194,304 rows per call;
  * larger batches are split by the caller, accumulating grad_weight).
  */
@@ -216,7 +228,8 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
                               float* token_loss, float* dlogp, uint8_t* clip_flag,
                               void* grad_hidden, grpo_dtype grad_hidden_dt, float* grad_weight,
                               int32_t accumulate_grad_weight, void* workspace,
-                              size_t workspace_bytes, hipStream_t stream);
+                              size_t workspace_bytes, int64_t max_valid, size_t dz_budget,
+                              hipStream_t stream);
 
 /*
  * sft_ce_fwd_bwd -- the supervised fine-tuning stage that precedes GRPO
@@ -234,7 +247,8 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
  *   logp_out    [N] fp32 or NULL (0 on masked rows). Device.
  *   grad_hidden, grad_hidden_dt, grad_weight, accumulate_grad_weight
  *               as grpo_loss_fwd_bwd (either gradient may be NULL).
- * workspace >= grpo_workspace_bytes(GRPO_OP_SFT_FWD_BWD, dt, N, H, V, 1).
+ * workspace >= grpo_workspace_bytes(GRPO_OP_SFT_FWD_BWD, dt, N, H, V, 1, max_valid,
+ * dz_budget).
  * Sizes and errors as grpo_loss_fwd_bwd (a token id outside [0, V) sets the flag that
  * grpo_check_error reports).
  */
@@ -243,7 +257,8 @@ grpo_status sft_ce_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight
                            int64_t V, float* loss, float* logp_out, void* grad_hidden,
                            grpo_dtype grad_hidden_dt, float* grad_weight,
                            int32_t accumulate_grad_weight, void* workspace,
-                           size_t workspace_bytes, hipStream_t stream);
+                           size_t workspace_bytes, int64_t max_valid, size_t dz_budget,
+                           hipStream_t stream);
 
 /*
  * adamw_step -- the optimiser step applied to the LM head after its gradient
@@ -305,13 +320,15 @@ grpo_status triton_rule_reward(const uint8_t* text, int64_t text_bytes, const in
 
 /* Bytes of workspace an operation needs for these sizes (0 if the sizes are
  * invalid). For GRPO_OP_LOGPROB_FWD and GRPO_OP_SFT_FWD_BWD pass
- * num_seqs = 1. Host only. */
+ * num_seqs = 1; max_valid and dz_budget as described under "Workspace size"
+ * (dz_budget is ignored for GRPO_OP_LOGPROB_FWD). Host only. */
 size_t grpo_workspace_bytes(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V,
-                            int64_t num_seqs);
+                            int64_t num_seqs, int64_t max_valid, size_t dz_budget);
 
 /* Synchronises `stream`, then reads and clears the device error flags kept in
  * the workspace by the most recent call that used it. Returns GRPO_OK,
- * GRPO_ERR_TOKEN_RANGE or GRPO_ERR_SEQLENS (or GRPO_ERR_HIP if a copy fails). */
+ * GRPO_ERR_SEQLENS, GRPO_ERR_TOKEN_RANGE or GRPO_ERR_CAPACITY (or
+ * GRPO_ERR_HIP if a copy fails). */
 grpo_status grpo_check_error(void* workspace, hipStream_t stream);
 
 /* Static description of a status code. Never NULL. */

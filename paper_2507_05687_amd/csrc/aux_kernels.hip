@@ -1,6 +1,6 @@
 // Streaming and bookkeeping kernels of libgrpo: group advantages (Eq. 2),
 // valid-row packing (the |o_i| counts of Eq. 1), the per-token GRPO term
-// (Eq. 1), the log-sum-exp combine, transposes, and the plain fp32 path.
+// (Eq. 1), the log-sum-exp combine, operand tiling, and the plain fp32 path.
 //
 // All reductions run in a fixed order, so every result is bitwise
 // reproducible run to run. No kernel uses atomics.
@@ -153,7 +153,7 @@ __global__ void __launch_bounds__(256) k_pack_count(const uint8_t* __restrict__ 
 // Exclusive scan of counts -> base[b]; base[B] and hdr->num_valid = total.
 __global__ void __launch_bounds__(256) k_pack_scan(const int32_t* __restrict__ counts, int64_t B,
                                                    int32_t* __restrict__ base, WsHeader* hdr,
-                                                   int32_t* num_valid_out) {
+                                                   int32_t* num_valid_out, int64_t cap) {
   __shared__ int32_t part[256];
   // each thread scans a contiguous slice
   int64_t per = ceil_div(B, 256);
@@ -168,6 +168,10 @@ __global__ void __launch_bounds__(256) k_pack_scan(const int32_t* __restrict__ c
       int32_t t = part[i];
       part[i] = run;
       run += t;
+    }
+    if (run > cap) {  // the workspace holds fewer rows: the call counts none as valid
+      hdr->err_capacity = 1;
+      run = 0;
     }
     hdr->num_valid = run;
     base[B] = run;
@@ -195,6 +199,7 @@ __global__ void __launch_bounds__(256) k_pack_scatter(
   seq_range(cu, seg, b, B, N, lo, hi, hdr);
   int32_t next = base[b];
   int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (hdr->err_capacity) return;  // no row is valid (pidx stays -1)
   for (int64_t r0 = lo; r0 < hi; r0 += 256) {
     int64_t r = r0 + threadIdx.x;
     bool v = r < hi && row_valid(mask, tokens, V, r, hdr);
@@ -226,12 +231,13 @@ __global__ void __launch_bounds__(256) k_pack_scatter(
 __global__ void k_reset_flags(WsHeader* hdr) {
   hdr->err_token = 0;
   hdr->err_seqlens = 0;
+  hdr->err_capacity = 0;
 }
 
 // status of the most recent call on the workspace header: GRPO_ERR_SEQLENS
 // (10), GRPO_ERR_TOKEN_RANGE (9) or 0
 __global__ void k_copy_status(const WsHeader* hdr, int32_t* out) {
-  *out = hdr->err_seqlens ? 10 : hdr->err_token ? 9 : 0;
+  *out = hdr->err_seqlens ? 10 : hdr->err_token ? 9 : hdr->err_capacity ? 11 : 0;
 }
 
 void launch_copy_status(const WsHeader* hdr, int32_t* out, hipStream_t s) {
@@ -247,7 +253,7 @@ void launch_pack(const PackArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_pack_count, dim3((unsigned)a.B), dim3(256), 0, s, a.mask, a.tokens, a.V,
                      a.cu, a.seg, a.B, a.N, a.counts, a.hdr);
   hipLaunchKernelGGL(k_pack_scan, dim3(1), dim3(256), 0, s, a.counts, a.B, a.base, a.hdr,
-                     a.num_valid_out);
+                     a.num_valid_out, a.cap);
   hipLaunchKernelGGL(k_pack_scatter, dim3((unsigned)a.B), dim3(256), 0, s, a.mask, a.tokens,
                      a.V, a.cu, a.seg, a.B, a.N, a.base, a.rows_p, a.seq_p, a.y_p, a.pidx, a.hdr);
 }
@@ -447,75 +453,7 @@ void launch_gather_dot_bf16(const uint16_t* hidden, const uint16_t* W, int64_t H
                      W, H, rows_p, y_p, hdr, zy);
 }
 
-// ------------------------------------------------------- transposes
-// out(k, i) = in[src_row(i)][k] for i < n_valid, 0 for n_valid <= i < n_pad,
-// with src_row(i) = rows ? rows[i] : i. `out` is in the tiled layout with k
-// as the row and i as the column: block (k/256, i/64) of n_pad/64 blocks per
-// tile-row, row k%256, column i%64. 64x64 bf16 tiles go through LDS.
-__global__ void __launch_bounds__(256) k_transpose_tiled(const uint16_t* __restrict__ in,
-                                                         int64_t ld_in,
-                                                         const int32_t* __restrict__ rows,
-                                                         int64_t n_static,
-                                                         const WsHeader* __restrict__ hdr,
-                                                         int64_t n_pad, int64_t K,
-                                                         int64_t stride,
-                                                         uint16_t* __restrict__ out) {
-  __shared__ uint16_t tile[64][66];
-  int64_t i0 = (int64_t)blockIdx.x * 64, k0 = (int64_t)blockIdx.y * 64;
-  int64_t nvalid = hdr ? (int64_t)hdr->num_valid : n_static;
-  int t = threadIdx.x;
-  // load: 64 source rows x 64 columns; thread -> (row t/4, 16 columns)
-  {
-    int ri = t >> 2, c0 = (t & 3) * 16;
-    int64_t i = i0 + ri;
-    uint16_t vals[16];
-    if (i < nvalid) {
-      int64_t src = rows ? rows[i] : i;
-      const uint16_t* p = in + src * ld_in + k0 + c0;
-      if (k0 + c0 + 16 <= K && ((((uintptr_t)p) & 15) == 0)) {
-        u32x4 a = *(const u32x4*)p, b = *(const u32x4*)(p + 8);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          vals[2 * q] = (uint16_t)(a[q] & 0xffff);
-          vals[2 * q + 1] = (uint16_t)(a[q] >> 16);
-          vals[8 + 2 * q] = (uint16_t)(b[q] & 0xffff);
-          vals[8 + 2 * q + 1] = (uint16_t)(b[q] >> 16);
-        }
-      } else {
-#pragma unroll
-        for (int q = 0; q < 16; ++q) vals[q] = (k0 + c0 + q < K) ? p[q] : (uint16_t)0;
-      }
-    } else {
-#pragma unroll
-      for (int q = 0; q < 16; ++q) vals[q] = 0;
-    }
-#pragma unroll
-    for (int q = 0; q < 16; ++q) tile[ri][c0 + q] = vals[q];
-  }
-  __syncthreads();
-  // store: 64 output rows (k) x 64 columns (i), one 128-byte block row each
-  {
-    int kk = t >> 2, c0 = (t & 3) * 16;
-    int64_t k = k0 + kk;
-    if (k < K) {
-      const int64_t i = i0 + c0;  // 16 consecutive columns, within one 32-wide block
-      uint16_t* p = out + ((k >> 8) * stride + (i >> 5)) * kTileElems + (k & 255) * 32 + (i & 31);
-      u32x4 a, b;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        a[q] = (uint32_t)tile[c0 + 2 * q][kk] | ((uint32_t)tile[c0 + 2 * q + 1][kk] << 16);
-        b[q] = (uint32_t)tile[c0 + 8 + 2 * q][kk] | ((uint32_t)tile[c0 + 8 + 2 * q + 1][kk] << 16);
-      }
-      *(u32x4*)p = a;
-      *(u32x4*)(p + 8) = b;
-    }
-  }
-}
-
-// --------------------------------------- row-major rows -> tiled layout
-// One workgroup per 256 x 32 output block; thread t writes 16 bytes of rows
-// t/4 + 64i (i = 0..3), chunk t%4, so that the block is written contiguously
-// and each source row is read as one 64-byte piece.
+// ------------------------------------------------------- operand tiling
 __global__ void __launch_bounds__(256) k_tile_rows(const uint16_t* __restrict__ in, int64_t ld_in,
                                                    const int32_t* __restrict__ rows,
                                                    int64_t n_static,
@@ -560,15 +498,6 @@ void launch_tile_rows(const uint16_t* in, int64_t ld_in, const int32_t* rows, in
 }
 
 // n_pad must be a multiple of 64; `out` holds round_up(K, 256) x n_pad elements.
-void launch_transpose_tiled(const uint16_t* in, int64_t ld_in, const int32_t* rows,
-                            int64_t n_static, const WsHeader* hdr, int64_t n_pad, int64_t K,
-                            int64_t stride, uint16_t* out, hipStream_t s) {
-  dim3 grid((unsigned)(n_pad / 64), (unsigned)ceil_div(K, 64));
-  hipLaunchKernelGGL(k_transpose_tiled, grid, dim3(256), 0, s, in, ld_in, rows, n_static, hdr,
-                     n_pad, K, stride, out);
-}
-
-// ------------------------------------------ zero the masked output rows
 __global__ void __launch_bounds__(256) k_zero_masked_rows(const int32_t* __restrict__ pidx,
                                                           int64_t N, int64_t H, void* out,
                                                           int out_bf16) {

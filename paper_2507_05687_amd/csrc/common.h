@@ -17,10 +17,11 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // Workspace header (first 256 bytes of every workspace). Each error kind has
 // its own word so that kernels can raise it with a plain store.
 struct WsHeader {
-  int32_t err_token;    // nonzero: some valid row had a token id outside [0, V)
-  int32_t err_seqlens;  // nonzero: cu_seqlens was not monotone from 0 to N
-  int32_t num_valid;    // number of valid rows after packing
-  int32_t pad_[61];
+  int32_t err_token;     // nonzero: some valid row had a token id outside [0, V)
+  int32_t err_seqlens;   // nonzero: cu_seqlens was not monotone from 0 to N
+  int32_t num_valid;     // number of valid rows after packing
+  int32_t err_capacity;  // nonzero: more valid rows than the workspace was sized for
+  int32_t pad_[60];
 };
 
 constexpr int kTile = 256;  // GEMM tile edge (rows and columns)

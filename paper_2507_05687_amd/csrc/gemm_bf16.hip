@@ -6,9 +6,9 @@
 //                 to online (max, sum-exp) partials and picks out z at the
 //                 sampled id.
 //   EpiDz         backward: the same tile recomputed and turned into
-//                 dz = -g * exp(z - lse), stored in bf16 both token-major and
-//                 vocabulary-major (the sampled id's +g is applied in fp32 by
-//                 the two products below and by the one-hot kernel).
+//                 dz = -g * exp(z - lse), stored in bf16 token-major (the
+//                 sampled id's +g is applied in fp32 by the two products below
+//                 and by the one-hot kernel).
 //   EpiGradHidden dL/dh = dz . W, and EpiGradWeight dL/dW = dz^T . h: fp32
 //                 stores, optionally accumulating, gathering output rows,
 //                 converting to bf16, or adding the sampled id's term.
@@ -57,6 +57,23 @@ __device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, char* lds, 
                                            uint32_t soff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)lds, 16, voff, soff, 0, 0);
 }
+// The same load issued from inline assembly, for kernels that read LDS with
+// ds_read_b64_tr_b16: the compiler cannot tell those reads apart from the
+// loads' LDS destinations and would wait for every load in flight before each
+// of them. Here the compiler sees no load at all, so the kernel itself waits
+// (vmcnt) before LDS that a load writes is read or reused. M0 is set in the
+// same statement; no other code of these kernels uses it.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void load_lds16_asm(__amdgpu_buffer_rsrc_t r, uint32_t lds,
+                                               uint32_t voff, uint32_t soff) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :
+               : "s"(m0), "v"(voff), "s"(r), "s"(soff)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
 
 // Maps a workgroup id to its (tile_m, tile_n); returns false for the
 // padding workgroups of the last band. With fewer than 8 kGM tile-rows there
@@ -85,9 +102,33 @@ __device__ inline bool column_tile_of(int bid, int tiles_m, int tiles_n, int& tm
   return tn < tiles_n;
 }
 
+// Tile-rows that make 1, 2 or 4 whole bands: the 8 XCDs are shared out over
+// the bands (8, 4 or 2 per band), each band's tile-columns over its XCDs, and
+// each XCD walks its part of its band as tile_of does.
+__host__ __device__ inline bool split_bands(int tiles_m) {
+  return tiles_m < 8 * kGM && tiles_m % kGM == 0 && 8 % (tiles_m / kGM) == 0;
+}
+__host__ __device__ inline int split_band_cols(int tiles_m, int tiles_n) {
+  const int parts = 8 / (tiles_m / kGM);
+  return (tiles_n + parts - 1) / parts;  // tile-columns per XCD
+}
+__device__ inline bool split_band_tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int xcd = bid & 7, loc = bid >> 3;
+  const int bands = tiles_m / kGM;
+  const int cols = split_band_cols(tiles_m, tiles_n);
+  const int nb = loc / (kGM * kGN), r2 = loc - nb * (kGM * kGN);
+  const int c = nb * kGN + r2 / kGM;
+  tm = (xcd % bands) * kGM + r2 % kGM;
+  tn = (xcd / bands) * cols + c;
+  return c < cols && tn < tiles_n;
+}
+
 // Tile of this workgroup, or false if it has none (or only rows or columns
 // past the valid counts). The mapping is chosen by the grid's tile-rows.
 __device__ inline bool gemm_tile(const GemmArgs& g, int m_valid, int n_valid, int& tm, int& tn) {
+  if (split_bands(g.tiles_m))
+    return split_band_tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn) && tm * kTile < m_valid &&
+           tn * kTile < n_valid;
   if (g.tiles_m < 8 * kGM) {
     if (m_valid <= 0 || n_valid <= 0) return false;
     return column_tile_of(blockIdx.x, min(g.tiles_m, (int)ceil_div(m_valid, kTile)),
@@ -98,6 +139,7 @@ __device__ inline bool gemm_tile(const GemmArgs& g, int m_valid, int n_valid, in
 }
 
 int gemm_grid(int tiles_m, int tiles_n) {
+  if (split_bands(tiles_m)) return 8 * kGM * (int)round_up(split_band_cols(tiles_m, tiles_n), kGN);
   if (tiles_m < 8 * kGM) return 8 * tiles_m * (int)ceil_div(tiles_n, 8);
   return (int)ceil_div(tiles_m, 8 * kGM) * 8 * kGM * tiles_n;
 }
@@ -118,16 +160,17 @@ struct Frag {
 };
 typedef f32x4 Acc[8][8];
 
-// Forward scoring on the 16x16 layout: A = vocabulary rows, B = tokens. Each
-// token column of a wave's 128-row half tile is spread over four lanes (32
-// rows each); each lane reduces its rows to (max, sum exp(z - max)), the four
-// partials are merged by two cross-lane exchanges, and the half tile writes
-// one partial per token. z at the sampled id is taken from the accumulator.
+// Forward scoring: A = vocabulary rows, B = tokens. Each token column of a
+// wave's 128-row half tile is spread over four lanes (32 rows each); each lane
+// reduces its rows to (max, sum exp(z - max)), the four partials are merged by
+// two cross-lane exchanges, the two half tiles through LDS, and the tile
+// writes one partial per token. z at the sampled id is taken from the
+// accumulator.
 struct EpiLse {
   static constexpr bool kKPositive = true;  // K = H >= 32
   const int32_t* y_p;  // sampled id of each packed token
   float* zy;           // z at the sampled id, per packed token
-  float2* ms;          // [2 * tiles_m][ldms] partial (max, sum-exp) per 128-row half tile
+  float2* ms;          // [tiles_m][ldms] partial (max, sum-exp) per tile and token
   int64_t ldms;
   int64_t V;
 
@@ -176,46 +219,60 @@ struct EpiLse {
     s_out = sum;
   }
 
-  static __device__ __forceinline__ void merge(float& m, float& s, int lanes) {
-    const float m2 = __shfl_xor(m, lanes, 64), s2 = __shfl_xor(s, lanes, 64);
+  // merges (m2, s2) into (m, s); an empty partial is (-inf, 0)
+  static __device__ __forceinline__ void merge2(float& m, float& s, float m2, float s2) {
     const float mm = fmaxf(m, m2);
     s = (s == 0.f ? 0.f : s * __expf(m - mm)) + (s2 == 0.f ? 0.f : s2 * __expf(m2 - mm));
     m = mm;
   }
+  static __device__ __forceinline__ void merge(float& m, float& s, int lanes) {
+    merge2(m, s, __shfl_xor(m, lanes, 64), __shfl_xor(s, lanes, 64));
+  }
 
-  __device__ __forceinline__ void operator()(Acc& acc, const Frag& f, int, int n_valid, char*,
-                                             const Pre& pre) const {
+  __device__ __forceinline__ void operator()(Acc& acc, const Frag& f, int, int n_valid,
+                                             char* smem, const Pre& pre) const {
     const int vbase = f.tm * kTile + f.row(0, 0);
     const int vlim = (int)(V - vbase);  // row offset o of this lane is valid iff o < vlim
     const bool full = (int64_t)f.tm * kTile + f.wm * 128 + 128 <= V;  // wave-uniform
+    float pm[8], ps[8];
     static_for<8>([&](auto j) {
       const int64_t t = (int64_t)f.tn * kTile + f.col(j);
       const int y = t < n_valid ? pre.y[j] - vbase : -1;  // y as a row offset of this lane
-      float m, sum;
       if (full)
-        column<true>(acc, j, m, sum, vlim, y, zy + t);
+        column<true>(acc, j, pm[j], ps[j], vlim, y, zy + t);
       else
-        column<false>(acc, j, m, sum, vlim, y, zy + t);
-      merge(m, sum, 16);
-      merge(m, sum, 32);
-      if (f.lane < 16 && t < n_valid) ms[(int64_t)(2 * f.tm + f.wm) * ldms + t] = make_float2(m, sum);
+        column<false>(acc, j, pm[j], ps[j], vlim, y, zy + t);
+      merge(pm[j], ps[j], 16);
+      merge(pm[j], ps[j], 32);
       __builtin_amdgcn_sched_barrier(0);  // one column at a time (bounds live registers)
     });
+    // the two waves of a column block (rows 0-127 and 128-255) merge into one
+    // partial per token: the lower half's wave adds the upper half's (fixed order)
+    float2* xchg = (float2*)smem + f.wn * 128;
+    if (f.wm == 1 && f.lane < 16)
+      static_for<8>([&](auto j) { xchg[j * 16 + f.lane] = make_float2(pm[j], ps[j]); });
+    __syncthreads();
+    if (f.wm == 0 && f.lane < 16) {
+      static_for<8>([&](auto j) {
+        const int64_t t = (int64_t)f.tn * kTile + f.col(j);
+        const float2 u = xchg[j * 16 + f.lane];
+        merge2(pm[j], ps[j], u.x, u.y);
+        if (t < n_valid) ms[(int64_t)f.tm * ldms + t] = make_float2(pm[j], ps[j]);
+      });
+    }
   }
 };
 
-// Backward on the 16x16 layout: the tile recomputed and turned into
-// dz = -g * exp(z - lse) (the sampled id's +g is applied exactly in fp32 by
-// the callers of the two gradient products), stored in bf16 token-major and
-// vocabulary-major.
+// Backward: the tile recomputed and turned into dz = -g * exp(z - lse) (the
+// sampled id's +g is applied exactly in fp32 by the callers of the two
+// gradient products), stored in bf16, token-major: the dL/dh product reads it
+// as is, the dL/dW product through transposing LDS reads.
 struct EpiDz {
   static constexpr bool kKPositive = true;  // K = H >= 32
   const float* lse_p;
   const float* g_p;
   uint16_t* dz;    // tiled [tokens][chunk vocabulary], dz_kt 32-wide blocks per tile-row
   int64_t dz_kt;
-  uint16_t* dzT;   // tiled [chunk vocabulary][tokens] (may be NULL), dzT_kt blocks per tile-row
-  int64_t dzT_kt;
   int64_t V;       // vocabulary size
   int64_t v0;      // first vocabulary row of this chunk
 
@@ -233,92 +290,41 @@ struct EpiDz {
     return p;
   }
 
-  // Physical 16-byte chunk of logical chunk c in staging row tl (a row-dependent
-  // XOR, the same for the writes and for both readbacks)
-  static __device__ __forceinline__ int stage_chunk(int tl, int c) {
-    const int m = (tl >> 1) & 3;
-    return c ^ m ^ ((m & 1) << 1);
-  }
-
-  __device__ __forceinline__ void operator()(Acc& acc, const Frag& f, int, int n_valid,
-                                             char* smem, const Pre& pre) const {
+  __device__ __forceinline__ void operator()(Acc& acc, const Frag& f, int, int n_valid, char*,
+                                             const Pre& pre) const {
     const int64_t vbase = v0 + (int64_t)f.tm * kTile + f.row(0, 0);
     const int vlim = (int)((V - vbase) < (1 << 20) ? (V - vbase) : (1 << 20));
     const bool full = v0 + (int64_t)f.tm * kTile + f.wm * 128 + 128 <= V;  // wave-uniform
-    // this wave's 128 vocabulary x 128 token part of the tile, staged as four
-    // 32-wide vocabulary blocks of 128 token rows (64 bytes each)
-    char* stage = smem + (f.wn * 2 + f.wm) * 32768;
     if (full)
-      body(acc, f, pre, n_valid, vlim, stage, std::true_type{});
+      body(acc, f, pre, n_valid, vlim, std::true_type{});
     else
-      body(acc, f, pre, n_valid, vlim, stage, std::false_type{});
-    // The LDS operations of one wave complete in order; the wait only makes
-    // the staged values visible before any lane reads another lane's.
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
-    const int64_t t0 = (int64_t)f.tn * kTile + f.wn * 128;  // the wave's first token
-    // Token-major dz: the wave's part of each vocabulary block is 128
-    // consecutive 64-byte rows of one tiled block, written 16 bytes per lane
-    // in whole lines.
-    static_for<4>([&](auto mi) {
-      uint16_t* pb = dz + ((t0 >> 8) * dz_kt + f.tm * 8 + f.wm * 4 + mi) * kTileElems;
-      static_for<8>([&](auto it) {
-        const int tl = it * 16 + (f.lane >> 2), c = f.lane & 3;
-        const u32x4 v = *(const u32x4*)(stage + mi * 8192 + tl * 64 + (stage_chunk(tl, c) << 4));
-        *(u32x4*)(pb + ((t0 & 255) + tl) * 32 + c * 8) = v;
-      });
-    });
-    if (dzT == nullptr) return;
-    // Vocabulary-major dzT: transposing LDS reads (ds_read_b64_tr_b16: within
-    // each 16 lanes, lane i receives element i%4 of lanes i/4, 4 + i/4,
-    // 8 + i/4, 12 + i/4) give each lane 8 consecutive tokens of one vocabulary
-    // row; one store covers 16 rows x 32 tokens of a tiled block, 1 KiB.
-    const int g4 = f.lane >> 4, i16 = f.lane & 15;
-    const int jr = (f.lane >> 2) & 3, qv = f.lane & 3;  // source row / vocabulary quad
-    static_for<4>([&](auto nb) {
-      uint16_t* pbt = dzT + ((int64_t)f.tm * dzT_kt + ((t0 >> 5) + nb)) * kTileElems +
-                      (f.wm * 128) * 32;
-      static_for<4>([&](auto mi) {
-        static_for<2>([&](auto vh) {
-          i16x4 r[2];
-          static_for<2>([&](auto h) {
-            const int tl = nb * 32 + g4 * 8 + h * 4 + jr;
-            const int vq = vh * 16 + qv * 4;  // first of the 4 vocabulary entries read
-            r[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (lds_i16x4_ptr_t)(stage + mi * 8192 + tl * 64 + (stage_chunk(tl, vq >> 3) << 4) +
-                                  (vq & 7) * 2));
-          });
-          const u32x4 v = {__builtin_bit_cast(uint32_t, __builtin_shufflevector(r[0], r[0], 0, 1)),
-                           __builtin_bit_cast(uint32_t, __builtin_shufflevector(r[0], r[0], 2, 3)),
-                           __builtin_bit_cast(uint32_t, __builtin_shufflevector(r[1], r[1], 0, 1)),
-                           __builtin_bit_cast(uint32_t, __builtin_shufflevector(r[1], r[1], 2, 3))};
-          *(u32x4*)(pbt + (mi * 32 + vh * 16 + i16) * 32 + g4 * 8) = v;
-        });
-      });
-    });
+      body(acc, f, pre, n_valid, vlim, std::false_type{});
   }
 
-  // -g * p of this lane's values, in bf16, staged in LDS (token-major): the
-  // four rows i*16 + (l/16)*4 .. +3 of column j are 8 consecutive bytes of
-  // token row j*16 + l%16
+  // -g * p of this lane's values in bf16: the four rows i*16 + (l/16)*4 .. +3 of
+  // column j are 8 consecutive bytes of token row j*16 + l%16 of the tiled
+  // token-major buffer (each store instruction covers 16 rows x 32 bytes)
   template <class Full>
   __device__ __forceinline__ void body(Acc& acc, const Frag& f, const Pre& pre, int n_valid,
-                                       int vlim, char* stage, Full) const {
+                                       int vlim, Full) const {
     const int q = f.lane >> 4;
+    // block (token tile-row tn, vocabulary block tm*8 + wm*4 + i/2), row
+    // wn*128 + j*16 + l%16, column (i%2)*16 + q*4
+    uint16_t* base = dz + ((int64_t)f.tn * dz_kt + f.tm * 8 + f.wm * 4) * kTileElems +
+                     (f.wn * 128 + (f.lane & 15)) * kBK + q * 4;
     static_for<8>([&](auto j) {
       const int64_t t = (int64_t)f.tn * kTile + f.col(j);
       const bool tv = t < n_valid;
       // p = exp(z - lse) = exp2(z*log2e - lse*log2e); invalid columns get g = 0
       const float l2 = tv ? pre.lse[j] * kLog2e : 0.f;
       const float ng = tv ? -pre.g[j] : 0.f;
-      const int tl = j * 16 + (f.lane & 15);
       static_for<8>([&](auto i) {
         float d[4];
         static_for<4>([&](auto r) {
           const float v = ng * __builtin_amdgcn_exp2f(fmaf(acc[i][j][r.value], kLog2e, -l2));
           d[r] = (Full::value || i * 16 + r < vlim) ? v : 0.f;
         });
-        const int c = (i & 1) * 2 + (q >> 1);
-        *(uint2*)(stage + (i >> 1) * 8192 + tl * 64 + (stage_chunk(tl, c) << 4) + (q & 1) * 8) =
+        *(uint2*)(base + (i / 2) * kTileElems + j * 16 * kBK + (i % 2) * 16) =
             make_uint2(bf16_pack2(d[0], d[1]), bf16_pack2(d[2], d[3]));
       });
       __builtin_amdgcn_sched_barrier(0);  // one column at a time (bounds live registers)
@@ -440,12 +446,38 @@ struct EpiGradWeight : EpiStore {};
 // kt+2 have landed) frees the stage of step kt+1. 16-byte chunks of a stage
 // row are XOR-swizzled by row bits 1-2, which keeps both the fragment reads
 // (16 rows x 4 chunks per instruction) and the loads free of bank conflicts.
+// The fragment reads of one K step as a list of instructions: fragments in
+// the order the step's MFMAs first use them (A0, B0..B7, A1..A7), a
+// transposed operand's fragment as its two halves. q(k) is the fragment of
+// instruction k, part(k) -1 for a whole fragment, else the half.
+template <bool TA, bool TB>
+struct ReadSchedule {
+  static constexpr int frag_at(int n) { return n == 0 ? 0 : n <= 8 ? n + 7 : n - 8; }
+  static constexpr int width(int q) { return (q < 8 ? TA : TB) ? 2 : 1; }
+  static constexpr int kOps = 8 * width(0) + 8 * width(8);
+  static constexpr int q(int k) {
+    for (int n = 0; n < 16; ++n) {
+      if (k < width(frag_at(n))) return frag_at(n);
+      k -= width(frag_at(n));
+    }
+    return -1;
+  }
+  static constexpr int part(int k) {
+    for (int n = 0; n < 16; ++n) {
+      const int wd = width(frag_at(n));
+      if (k < wd) return wd == 1 ? -1 : k;
+      k -= wd;
+    }
+    return -1;
+  }
+};
+
 constexpr int kWaves = 4;
 constexpr int kStage = 2 * kTileElems * 2;              // bytes of one A + B stage
 constexpr int kStages = 5;
 constexpr int kJ = kTileElems * 2 / 1024 / kWaves;      // 1 KiB loads per operand per wave per step
 
-template <class Epi>
+template <class Epi, bool TA, bool TB>
 __global__ void __launch_bounds__(256, 1) k_gemm(GemmArgs g, Epi epi) {
   __shared__ __attribute__((aligned(16))) char smem[kStages * kStage];
   const int m_valid = g.m_dev ? min(*g.m_dev, g.M) : g.M;
@@ -486,13 +518,49 @@ __global__ void __launch_bounds__(256, 1) k_gemm(GemmArgs g, Epi epi) {
   const __amdgpu_buffer_rsrc_t rb =
       tile_rsrc(g.B + ((int64_t)tn * g.b_kt + g.b_kb0 + kb0) * kTileElems);
   const uint32_t lofs = (uint32_t)(qrow * 32 + qch * 8) * 2;
+  // A transposed operand's K step is 32 rows of its 8 column blocks: 8 runs of
+  // 2 KiB, each row 64 contiguous bytes. Load j (of 16) moves rows 16 (j%2)
+  // .. +15 of column block j/2 into stage bytes j * 1024; the buffer resource
+  // is rebased on every step (K crosses block-rows every 8 steps). A row r
+  // with bit 1 xor bit 3 set holds its two 32-byte halves swapped (lane l of
+  // a load fills row l/4 of its 16, physical chunk l%4), so that the rows of a
+  // transposing read spread over all banks (see the fragment reads).
+  const int tsw = ((lane >> 3) ^ (lane >> 5)) & 1;
+  const int tsrc = (lane & ~3) * 8 + ((lane & 3) ^ (tsw << 1)) * 8;
+  const uint32_t tofs[kJ] = {
+      (uint32_t)(((w >> 1) * 8192 + (w & 1) * 512 + tsrc) * 2),
+      (uint32_t)((((w + 4) >> 1) * 8192 + (w & 1) * 512 + tsrc) * 2),
+      (uint32_t)((((w + 8) >> 1) * 8192 + (w & 1) * 512 + tsrc) * 2),
+      (uint32_t)((((w + 12) >> 1) * 8192 + (w & 1) * 512 + tsrc) * 2)};
+  auto trsrc = [&](const uint16_t* X, int64_t x_kt, int64_t x_kb0, int64_t x_cb0, int t, int kt) {
+    const int64_t kr = (x_kb0 + kb0 + kt) * kBK;  // first storage row of this K step
+    return tile_rsrc(X + (((kr >> 8) * x_kt + x_cb0 + (int64_t)t * 8) * kTileElems +
+                          (kr & 255) * kBK));
+  };
+  // LDS address of smem (the kernel's only LDS object, so in practice 0)
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
+  auto ld = [&](__amdgpu_buffer_rsrc_t r, char* lds, uint32_t voff, uint32_t soff) {
+    if constexpr (TA || TB)
+      load_lds16_asm(r, lds0 + (uint32_t)(lds - smem), voff, soff);
+    else
+      load_lds16(r, lds, voff, soff);
+  };
   auto load = [&](int kt, char* la, auto l) {
     const uint32_t so = (uint32_t)kt * (kTileElems * 2);
-    if constexpr (l.value < kJ)
-      load_lds16(ra, la + l.value * 1024 * kWaves, lofs + l.value * 16 * kWaves * 64, so);
-    else
-      load_lds16(rb, la + kTileElems * 2 + (l.value - kJ) * 1024 * kWaves,
-                 lofs + (l.value - kJ) * 16 * kWaves * 64, so);
+    if constexpr (l.value < kJ) {
+      if constexpr (TA)
+        ld(trsrc(g.A, g.a_kt, g.a_kb0, g.a_cb0, tm, kt), la - w * 1024 + (w + 4 * l.value) * 1024,
+           tofs[l.value], 0);
+      else
+        ld(ra, la + l.value * 1024 * kWaves, lofs + l.value * 16 * kWaves * 64, so);
+    } else {
+      if constexpr (TB)
+        ld(trsrc(g.B, g.b_kt, g.b_kb0, g.b_cb0, tn, kt),
+           la - w * 1024 + kTileElems * 2 + (w + 4 * (l.value - kJ)) * 1024, tofs[l.value - kJ], 0);
+      else
+        ld(rb, la + kTileElems * 2 + (l.value - kJ) * 1024 * kWaves,
+           lofs + (l.value - kJ) * 16 * kWaves * 64, so);
+    }
   };
   auto load_step = [&](int kt, int stage) {
     char* la = smem + stage * kStage + w * 1024;
@@ -504,23 +572,60 @@ __global__ void __launch_bounds__(256, 1) k_gemm(GemmArgs g, Epi epi) {
   const int rch = ((lane >> 4) ^ ((fr >> 1) & 3)) << 4;
   const int rd_a = (wm * 128 + fr) * 64 + rch;
   const int rd_b = kTileElems * 2 + (wn * 128 + fr) * 64 + rch;
+  // A transposed operand's fragment: two transposing reads (ds_read_b64_tr_b16:
+  // within 16 lanes, lane i receives element i%4 of the 8 bytes lanes i/4,
+  // 4 + i/4, 8 + i/4, 12 + i/4 address). Lane a of 16-lane group g addresses
+  // row 8g + 4r + a/4 and the 4 columns 4 (a%4) .. +3 of the block's 16, so
+  // that lane i gets K rows 8g + 4r .. +3 of column i; r = 0, 1 give 8 rows.
+  // A group's 16 lanes read 4 rows x 32 bytes, two groups 8 rows: with the
+  // halves swapped on bit 1 xor bit 3 of the row, the 4 rows fall on distinct
+  // 32-byte quarters of 128 bytes of banks and the 8 rows on distinct eighths
+  // of 256 bytes.
+  const int tr_row = 8 * (lane >> 4) + ((lane & 15) >> 2);
+  const int tr_sw = (((lane >> 3) ^ (lane >> 4)) & 1) * 32;  // bit 1 ^ bit 3 of tr_row
+  const int tr_a = tr_row * 64 + (lane & 3) * 8 + wm * 4 * 2048;
+  const int tr_b = kTileElems * 2 + tr_row * 64 + (lane & 3) * 8 + wn * 4 * 2048;
+  const int tr_h[2] = {tr_sw, 32 - tr_sw};  // byte offset of half 0 / half 1
   bf16x8 fs[2][16];
-  auto fread = [&](auto slot, auto st, auto q) {
+  i16x4 fh[2][16][2];  // the halves of a transposed operand's fragments
+  // part: -1 the whole fragment, 0 / 1 one half of a transposed fragment
+  auto fread = [&](auto slot, auto st, auto q, auto part) {
     const char* base = smem + st.value * kStage;
-    if constexpr (q.value < 8)
+    constexpr bool T = q.value < 8 ? TA : TB;
+    if constexpr (T) {
+      constexpr int blk = q.value % 8;  // column block blk/2 of the wave's four, half blk%2
+      const char* pr = base + (q.value < 8 ? tr_a : tr_b) + tr_h[blk % 2] + (blk / 2) * 2048;
+      static_for<2>([&](auto r) {
+        if constexpr (part.value < 0 || part.value == r.value)
+          fh[slot.value][q.value][r.value] =
+              __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_ptr_t)(pr + r.value * 4 * 64));
+      });
+    } else if constexpr (q.value < 8) {
       fs[slot.value][q.value] = *(const bf16x8*)(base + rd_a + q.value * 16 * 64);
-    else
+    } else {
       fs[slot.value][q.value] = *(const bf16x8*)(base + rd_b + (q.value - 8) * 16 * 64);
+    }
   };
   // MFMA m of a step: block row i = m/8, block column j in a snake order
   // (each MFMA changes one operand from the one before)
+  auto frag = [&](auto slot, auto q) {
+    constexpr bool T = q.value < 8 ? TA : TB;
+    if constexpr (T)
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(fh[slot.value][q.value][0],
+                                                                fh[slot.value][q.value][1], 0, 1,
+                                                                2, 3, 4, 5, 6, 7));
+    else
+      return fs[slot.value][q.value];
+  };
   auto mfma = [&](auto slot, auto m) {
     constexpr int i = m.value / 8, jj = m.value % 8, j = (i & 1) ? 7 - jj : jj;
-    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fs[slot.value][i], fs[slot.value][8 + j],
-                                                        acc[i][j], 0, 0, 0);
+    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+        frag(slot, std::integral_constant<int, i>{}),
+        frag(slot, std::integral_constant<int, 8 + j>{}), acc[i][j], 0, 0, 0);
   };
-  // the reads of a step in the order its MFMAs first use them: A0, B0..B7, A1..A7
-  auto read_order = [](int m) { return m == 0 ? 0 : m <= 8 ? m + 7 : m - 8; };
+  // the reads of a step in the order its MFMAs first use them (A0, B0..B7,
+  // A1..A7), one instruction after each MFMA: a transposed fragment takes two
+  using ReadOps = ReadSchedule<TA, TB>;
   constexpr int kPerStep = 2 * kJ;  // loads per wave per step
   constexpr int kMfmas = 64;        // MFMAs per wave per step
   constexpr int kSpread = kMfmas / kPerStep;
@@ -531,7 +636,7 @@ __global__ void __launch_bounds__(256, 1) k_gemm(GemmArgs g, Epi epi) {
   static_for<kStages>([&](auto st) { load_step(min((int)st.value, last), st.value); });
   __builtin_amdgcn_s_waitcnt(wait_vm((kStages - 1) * kPerStep));  // step 0 has landed
   __builtin_amdgcn_s_barrier();
-  static_for<16>([&](auto q) { fread(I0{}, I0{}, q); });
+  static_for<16>([&](auto q) { fread(I0{}, I0{}, q, std::integral_constant<int, -1>{}); });
   __builtin_amdgcn_s_waitcnt(wait_vm((kStages - 2) * kPerStep));  // step 1 has landed
   __builtin_amdgcn_s_barrier();  // and every wave holds step 0: its stage is free
 
@@ -545,8 +650,9 @@ __global__ void __launch_bounds__(256, 1) k_gemm(GemmArgs g, Epi epi) {
     char* nl = smem + st.value * kStage + w * 1024;
     static_for<kMfmas>([&](auto m) {
       mfma(cur, m);
-      if constexpr (m.value < 16)
-        fread(Nxt{}, StNxt{}, std::integral_constant<int, read_order(m.value)>{});
+      if constexpr (m.value < ReadOps::kOps)
+        fread(Nxt{}, StNxt{}, std::integral_constant<int, ReadOps::q(m.value)>{},
+              std::integral_constant<int, ReadOps::part(m.value)>{});
       if constexpr (m.value % kSpread == kSpread - 1)
         load(nkt, nl, std::integral_constant<int, m.value / kSpread>{});
       __builtin_amdgcn_sched_barrier(0);
@@ -567,7 +673,10 @@ __global__ void __launch_bounds__(256, 1) k_gemm(GemmArgs g, Epi epi) {
         step(kt0 + u.value, std::integral_constant<int, u.value % 2>{},
              std::integral_constant<int, u.value % kStages>{});
     });
-  __syncthreads();  // every load has landed before LDS is reused
+  // every load (including the clamped ones past the last step) has landed
+  // before the epilogue reuses LDS
+  __builtin_amdgcn_s_waitcnt(wait_vm(0));
+  __syncthreads();
 
   // The epilogue recomputes its indexes from an opaque copy of the lane id,
   // so that none of them is computed before the main loop and held in
@@ -579,15 +688,14 @@ __global__ void __launch_bounds__(256, 1) k_gemm(GemmArgs g, Epi epi) {
 
 void launch_gemm_lse(const GemmArgs& g, const int32_t* y_p, float* zy, float2* ms, int64_t ldms,
                      int64_t V, hipStream_t s) {
-  hipLaunchKernelGGL((k_gemm<EpiLse>), dim3(gemm_grid(g.tiles_m, g.tiles_n)), dim3(256), 0, s,
-                     g, EpiLse{y_p, zy, ms, ldms, V});
+  hipLaunchKernelGGL((k_gemm<EpiLse, false, false>), dim3(gemm_grid(g.tiles_m, g.tiles_n)),
+                     dim3(256), 0, s, g, EpiLse{y_p, zy, ms, ldms, V});
 }
 
 void launch_gemm_dz(const GemmArgs& g, const float* lse_p, const float* g_p, uint16_t* dz,
-                    int64_t dz_kt, uint16_t* dzT, int64_t dzT_kt, int64_t V, int64_t v0,
-                    hipStream_t s) {
-  hipLaunchKernelGGL((k_gemm<EpiDz>), dim3(gemm_grid(g.tiles_m, g.tiles_n)), dim3(256), 0, s,
-                     g, EpiDz{lse_p, g_p, dz, dz_kt, dzT, dzT_kt, V, v0});
+                    int64_t dz_kt, int64_t V, int64_t v0, hipStream_t s) {
+  hipLaunchKernelGGL((k_gemm<EpiDz, false, false>), dim3(gemm_grid(g.tiles_m, g.tiles_n)),
+                     dim3(256), 0, s, g, EpiDz{lse_p, g_p, dz, dz_kt, V, v0});
 }
 
 // Distinct kernel symbols (hence distinct entries in profiles) for the two
@@ -596,9 +704,11 @@ void launch_gemm_store(const GemmArgs& g, const StoreArgs& a, bool grad_weight, 
   const EpiStore e{a};
   const dim3 blocks(gemm_grid(g.tiles_m, g.tiles_n), g.splits > 1 ? g.splits : 1);
   if (grad_weight)
-    hipLaunchKernelGGL((k_gemm<EpiGradWeight>), blocks, dim3(256), 0, s, g, EpiGradWeight{e});
+    hipLaunchKernelGGL((k_gemm<EpiGradWeight, true, true>), blocks, dim3(256), 0, s, g,
+                       EpiGradWeight{e});
   else
-    hipLaunchKernelGGL((k_gemm<EpiGradHidden>), blocks, dim3(256), 0, s, g, EpiGradHidden{e});
+    hipLaunchKernelGGL((k_gemm<EpiGradHidden, false, true>), blocks, dim3(256), 0, s, g,
+                       EpiGradHidden{e});
 }
 
 }  // namespace grpo

@@ -18,13 +18,13 @@ namespace {
 
 // --------------------------------------------------------- kernel timing
 enum Kind {
-  K_PACK, K_ADV, K_GEMM_LSE, K_LSE_FIN, K_TOKEN, K_TRANSPOSE, K_GEMM_DZ, K_GEMM_DH, K_GEMM_DW,
+  K_PACK, K_ADV, K_GEMM_LSE, K_LSE_FIN, K_TOKEN, K_GEMM_DZ, K_GEMM_DH, K_GEMM_DW,
   K_F32_SCORE, K_F32_DH, K_F32_DW, K_ZERO_ROWS, K_GATHER_DOT, K_TILE, K_ADAMW,
   K_RULE_REWARD, K_SUM_SPLITS, K_ONEHOT, K_NUM_KINDS
 };
 const char* kKindNames[K_NUM_KINDS] = {
     "pack_valid",  "group_advantages", "gemm_logits_lse", "lse_finalize",   "token_objective",
-    "transpose",   "gemm_recompute_dz", "gemm_grad_hidden", "gemm_grad_weight", "f32_score",
+    "gemm_recompute_dz", "gemm_grad_hidden", "gemm_grad_weight", "f32_score",
     "f32_grad_hidden", "f32_grad_weight", "zero_masked_rows", "gather_dot", "tile", "adamw",
     "rule_reward", "sum_splits", "onehot_grad_weight"};
 
@@ -141,40 +141,27 @@ grpo_status static_scratch(char** out) {
 constexpr size_t kAlign = 256;
 constexpr int64_t kPackSeg = 4096;  // rows per packing workgroup without cu_seqlens
 constexpr int64_t kMaxAdvPrompts = 4 * ((1ll << 24) - 1);  // group_advantages' grid limit
-#ifndef GRPO_DZ_BUDGET_GIB
-#define GRPO_DZ_BUDGET_GIB 48
-#endif
-#ifndef GRPO_VC_MAX
-#define GRPO_VC_MAX 8192
-#endif
-#ifndef GRPO_DH_GROUP
-#define GRPO_DH_GROUP 2
-#endif
-constexpr int64_t kDzBudget = (int64_t)GRPO_DZ_BUDGET_GIB << 30;  // bytes for the two bf16 dz buffers
-constexpr int64_t kVcMax = GRPO_VC_MAX;
-// dz chunks per dL/dh product: dz and dL/dW run per chunk, dL/dh once per
-// group of chunks (fewer passes over its fp32 accumulator)
-constexpr int64_t kDhGroup = GRPO_DH_GROUP;
+constexpr size_t kDefaultDzBudget = (size_t)48 << 30;  // bytes for the bf16 dz chunks
+constexpr int64_t kVcMax = 8192;                        // columns per vocabulary chunk
 
 struct Layout {
-  int64_t Npad = 0, Vpad = 0, tiles_v = 0, Vc = 0, nchunks = 0;
+  int64_t Npad = 0, Vpad = 0, tiles_v = 0, Vc = 0, nchunks = 0, dh_group = 0;
+  int dw_splits_max = 1;  // the most K splits of a dL/dW product (its partials' room)
+  int64_t R = 0;  // rows of the token-indexed tiled buffers: the valid-row capacity, padded
   size_t hdr = 0, rows = 0, seq = 0, y = 0, pidx = 0, counts = 0, base = 0;
   size_t lse = 0, zy = 0, logp = 0, g = 0, ms = 0, lpart = 0;
   int64_t Hk = 0;  // H rounded up to the tiled block width
   // tiled buffers and their tile-row strides in blocks
-  size_t WK = 0, hK = 0, hT = 0, WT = 0, dz = 0, dzT = 0, dhacc = 0, dwpart = 0;
+  size_t WK = 0, hK = 0, dz = 0, dhacc = 0, dwpart = 0;
   size_t okeys[2] = {0, 0}, ovals[2] = {0, 0}, ocounts = 0;  // sort of the sampled ids
-  int64_t sK = 0, sTok = 0, sVoc = 0, sChunk = 0;
+  int64_t sK = 0, sChunk = 0;
   size_t total = 0;
 };
 
 // Tile-rows of a tiled buffer are one block further apart than their length,
 // so that the blocks that concurrent tiles read at the same K step do not
 // all share the same low address bits (and L2 sets).
-#ifndef GRPO_TILE_SKEW
-#define GRPO_TILE_SKEW 1
-#endif
-int64_t tile_stride(int64_t K) { return ceil_div(K, kBK) + GRPO_TILE_SKEW; }
+int64_t tile_stride(int64_t K) { return ceil_div(K, kBK) + 1; }
 
 // K splits for a product of `tiles` output tiles: the count up to kMaxSplits
 // that best fills whole rounds of 256 workgroups (one per CU), taking more
@@ -202,24 +189,69 @@ size_t take(size_t& cur, size_t bytes) {
   return at;
 }
 
-// Vocabulary chunk for the backward pass: the two bf16 dz buffers (token-major
-// for a group of kDhGroup chunks, vocabulary-major for one chunk) together
-// stay within kDzBudget, chunks are at most kVcMax rows, and all chunks but
-// the last have equal size.
-void chunking(int64_t Npad, int64_t Vpad, int64_t& Vc, int64_t& nchunks) {
-  int64_t cap = kDzBudget / (2 * (kDhGroup + 1) * Npad) / kTile * kTile;
-  if (cap < kTile) cap = kTile;
-  if (cap > kVcMax) cap = kVcMax;
-  nchunks = ceil_div(Vpad, cap);
-  Vc = round_up(ceil_div(Vpad, nchunks), kTile);
+// Estimated seconds of the parts of the backward pass that depend on the
+// vocabulary chunking: the dL/dW products (whole rounds of 256 workgroups,
+// each a 256 x 256 tile over K = R tokens at about 1.9 PFLOP/s), the fp32
+// partials of a split K (written and read once), the passes over the fp32
+// dL/dh accumulator (read and written by every dL/dh product after the
+// first) at about 5 TB/s, and a few launches per chunk.
+double chunking_cost(int64_t R, int64_t Vpad, int64_t Hpad, int64_t Vc, int64_t group) {
+  const double kFlops = 1.9e15, kBytes = 5e12, kLaunch = 20e-6;
+  const double t_round = 256.0 * 2 * kTile * kTile * (double)R / kFlops;
+  const int64_t n = ceil_div(Vpad, Vc);
+  double t = 0;
+  for (int c = 0; c < 2; ++c) {  // the n - 1 full chunks, then the last
+    const int64_t cols = c == 0 ? Vc : Vpad - (n - 1) * Vc;
+    const int64_t cnt = c == 0 ? n - 1 : 1;
+    const int64_t tiles = cols / kTile * (Hpad / kTile);
+    const int sp = dw_splits(tiles);
+    double tc = (double)ceil_div(sp * tiles, 256) / sp * t_round + 3 * kLaunch;
+    if (sp > 1) tc += 2.0 * sp * (double)cols * Hpad * 4 / kBytes;
+    t += cnt * tc;
+  }
+  t += (ceil_div(n, group) - 1) * 8.0 * (double)R * Hpad / kBytes;
+  return t;
+}
+
+// Vocabulary chunks of the backward pass and how many of them one dL/dh
+// product takes. The token-major bf16 dz buffer holds `group` chunks of Vc
+// columns for R rows: it stays within `budget` bytes (0: kDefaultDzBudget) and
+// within a quarter of the vocabulary (the logits gradient is never held
+// whole). Vc (a multiple of 256, at most kVcMax) and the group are the pair
+// of least chunking_cost; all chunks but the last are Vc wide.
+void chunking(int64_t R, int64_t Vpad, int64_t Hpad, size_t budget, int64_t& Vc,
+              int64_t& nchunks, int64_t& group) {
+  if (budget == 0) budget = kDefaultDzBudget;
+  int64_t cols = (int64_t)(budget / (2 * (size_t)R)) / kTile * kTile;
+  const int64_t quarter = round_up(ceil_div(Vpad, 4), kTile);
+  if (cols > quarter) cols = quarter;
+  if (cols < kTile) cols = kTile;
+  int64_t cap = cols < kVcMax ? cols : kVcMax;
+  if (cap > Vpad) cap = Vpad;
+  double best = 0;
+  for (int64_t c = cap; c >= kTile; c -= kTile) {
+    const int64_t n = ceil_div(Vpad, c);
+    int64_t gr = cols / c;
+    if (gr > n) gr = n;
+    const double cost = chunking_cost(R, Vpad, Hpad, c, gr);
+    if (c == cap || cost < best * 0.999) {
+      best = cost;
+      Vc = c;
+      group = gr;
+    }
+  }
   nchunks = ceil_div(Vpad, Vc);
 }
 
-Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_t B) {
+// max_valid: the most valid rows a call will have (0: all N); dz_budget: bytes
+// for the logits-gradient chunks (0: the default).
+Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_t B,
+              int64_t max_valid, size_t dz_budget) {
   Layout L;
   L.Npad = round_up(N, kTile);
   L.Vpad = round_up(V, kTile);
   L.tiles_v = L.Vpad / kTile;
+  L.R = round_up(max_valid > 0 && max_valid < N ? max_valid : N, kTile);
   size_t c = 0;
   L.hdr = take(c, sizeof(WsHeader));
   L.rows = take(c, 4 * L.Npad);
@@ -236,33 +268,31 @@ Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_
   L.g = take(c, 4 * L.Npad);
   L.lpart = take(c, 4 * token_objective_blocks(N));
   if (dt == GRPO_BF16) {
-    L.ms = take(c, 8 * 2 * L.tiles_v * L.Npad);  // one partial per 128-row half tile
+    L.ms = take(c, 8 * L.tiles_v * L.R);  // one (max, sum-exp) partial per vocabulary tile
     // tiled copies of W and of the valid hidden rows (K = H contiguous blocks)
     L.Hk = round_up(H, kBK);
     L.sK = tile_stride(H);
     L.WK = take(c, 2 * L.Vpad * L.sK * kBK);
-    L.hK = take(c, 2 * L.Npad * L.sK * kBK);
+    L.hK = take(c, 2 * L.R * L.sK * kBK);
     if (op == GRPO_OP_LOSS_FWD_BWD) {
-      chunking(L.Npad, L.Vpad, L.Vc, L.nchunks);
-      int64_t Hpad = round_up(H, kTile);
-      L.sTok = tile_stride(L.Npad);
-      L.sVoc = tile_stride(L.Vpad);
-      L.sChunk = tile_stride(kDhGroup * L.Vc);
-      L.hT = take(c, 2 * Hpad * L.sTok * kBK);
-      L.WT = take(c, 2 * Hpad * L.sVoc * kBK);
-      L.dz = take(c, 2 * L.Npad * L.sChunk * kBK);
-      L.dzT = take(c, 2 * L.Vc * L.sTok * kBK);
+      const int64_t Hpad = round_up(H, kTile);
+      chunking(L.R, L.Vpad, Hpad, dz_budget, L.Vc, L.nchunks, L.dh_group);
+      L.sChunk = tile_stride(L.dh_group * L.Vc);
+      L.dz = take(c, 2 * L.R * L.sChunk * kBK);
       // fp32 dh accumulator with every row and column of every tile present
-      if (L.nchunks > kDhGroup) L.dhacc = take(c, 4 * L.Npad * Hpad);
+      if (L.nchunks > L.dh_group) L.dhacc = take(c, 4 * L.R * Hpad);
       // dW partials of a split K (chunks too narrow to fill the GPU)
-      if (dw_splits(L.Vc / kTile * (Hpad / kTile)) > 1)
-        L.dwpart = take(c, 4 * kMaxSplits * L.Vc * Hpad);
+      const int64_t last = L.Vpad - (L.nchunks - 1) * L.Vc;
+      const int sp_full = dw_splits(L.Vc / kTile * (Hpad / kTile));
+      const int sp_last = dw_splits(last / kTile * (Hpad / kTile));
+      L.dw_splits_max = sp_full > sp_last ? sp_full : sp_last;
+      if (L.dw_splits_max > 1) L.dwpart = take(c, 4 * L.dw_splits_max * L.Vc * Hpad);
       // the stable sort of the packed ids for the sampled-id term of dL/dW
       for (int b = 0; b < 2; ++b) {
-        L.okeys[b] = take(c, 4 * L.Npad);
-        L.ovals[b] = take(c, 4 * L.Npad);
+        L.okeys[b] = take(c, 4 * L.R);
+        L.ovals[b] = take(c, 4 * L.R);
       }
-      L.ocounts = take(c, 4 * onehot_count_entries(L.Npad));
+      L.ocounts = take(c, 4 * onehot_count_entries(L.R));
     }
   }
   L.total = c;
@@ -317,6 +347,7 @@ GemmArgs gemm_args(const void* A, int64_t a_kt, int64_t M, const void* B, int64_
   g.a_kt = a_kt;
   g.b_kt = b_kt;
   g.a_kb0 = g.b_kb0 = 0;
+  g.a_cb0 = g.b_cb0 = 0;
   g.K = (int)K;
   g.k_dev = k_dev;
   g.tiles_m = (int)ceil_div(M, kTile);
@@ -329,6 +360,8 @@ GemmArgs gemm_args(const void* A, int64_t a_kt, int64_t M, const void* B, int64_
 grpo_status run_pack(const Layout& L, void* ws, const uint8_t* mask, const int64_t* tokens,
                      int64_t V, const int64_t* cu, int64_t B, int64_t N, int32_t* rows_out,
                      int32_t* counts_out, int32_t* nvalid_out, hipStream_t s) {
+  // the valid rows the workspace's token buffers hold (all N for the fp32 path)
+  const int64_t cap = L.hK ? L.R : N;
   PackArgs a;
   a.mask = mask;
   a.tokens = tokens;
@@ -346,6 +379,7 @@ grpo_status run_pack(const Layout& L, void* ws, const uint8_t* mask, const int64
   a.y_p = tokens ? at<int32_t>(ws, L.y) : nullptr;
   a.pidx = at<int32_t>(ws, L.pidx);
   a.num_valid_out = nvalid_out;
+  a.cap = cap;
   a.hdr = at<WsHeader>(ws, L.hdr);
   return timed(K_PACK, s, [&] { launch_pack(a, s); });
 }
@@ -361,7 +395,7 @@ grpo_status run_tiles(const Layout& L, void* ws, const void* hidden, const void*
                      at<uint16_t>(ws, L.WK), s);
   }));
   return timed(K_TILE, s, [&] {
-    launch_tile_rows((const uint16_t*)hidden, H, rows_p, 0, hdr, L.Npad, H, L.sK,
+    launch_tile_rows((const uint16_t*)hidden, H, rows_p, 0, hdr, L.R, H, L.sK,
                      at<uint16_t>(ws, L.hK), s);
   });
 }
@@ -382,11 +416,11 @@ grpo_status run_scoring(const Layout& L, void* ws, grpo_dtype dt, const void* hi
     });
   }
   float2* ms = at<float2>(ws, L.ms);
-  GemmArgs g = gemm_args(at<uint16_t>(ws, L.WK), L.sK, V, at<uint16_t>(ws, L.hK), L.sK, L.Npad,
+  GemmArgs g = gemm_args(at<uint16_t>(ws, L.WK), L.sK, V, at<uint16_t>(ws, L.hK), L.sK, L.R,
                          nullptr, &hdr->num_valid, L.Hk, nullptr);
-  TRY(timed(K_GEMM_LSE, s, [&] { launch_gemm_lse(g, y_p, zy, ms, L.Npad, V, s); }));
+  TRY(timed(K_GEMM_LSE, s, [&] { launch_gemm_lse(g, y_p, zy, ms, L.R, V, s); }));
   return timed(K_LSE_FIN, s, [&] {
-    launch_lse_finalize(ms, L.Npad, (int)(2 * L.tiles_v), zy, hdr, lse_p, logp_p, N, s);
+    launch_lse_finalize(ms, L.R, (int)L.tiles_v, zy, hdr, lse_p, logp_p, L.R, s);
   });
 }
 
@@ -421,47 +455,34 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
     return GRPO_OK;
   }
 
-  uint16_t* hT = at<uint16_t>(ws, L.hT);
-  uint16_t* WT = at<uint16_t>(ws, L.WT);
   uint16_t* dz = at<uint16_t>(ws, L.dz);
-  uint16_t* dzT = at<uint16_t>(ws, L.dzT);
-  float* dhacc = L.nchunks > kDhGroup ? at<float>(ws, L.dhacc) : nullptr;
-  // Intermediates in the tiled layout: h^T [H x tokens], W^T [H x V],
-  // dz [tokens x group of chunks] and dz^T [chunk x tokens].
-  const int64_t kt_tok = L.sTok, kt_voc = L.sVoc, kt_chunk = L.sChunk, kt_h = L.sK;
-  if (grad_weight) {
-    TRY(timed(K_TRANSPOSE, s, [&] {
-      launch_transpose_tiled((const uint16_t*)hidden, H, rows_p, 0, hdr, L.Npad, H, kt_tok, hT,
-                             s);
-    }));
-  }
-  if (grad_hidden) {
-    TRY(timed(K_TRANSPOSE, s, [&] {
-      launch_transpose_tiled((const uint16_t*)weight, H, nullptr, V, nullptr, L.Vpad, H, kt_voc,
-                             WT, s);
-    }));
-  }
+  uint16_t* WK = at<uint16_t>(ws, L.WK);
+  uint16_t* hK = at<uint16_t>(ws, L.hK);
+  float* dhacc = L.nchunks > L.dh_group ? at<float>(ws, L.dhacc) : nullptr;
+  // The tiled operands: W [V x H] and the valid hidden rows [R x H] (the
+  // scoring's), and dz [R tokens x group of chunks]. dz and the chunk's W rows
+  // feed the recompute natively; dL/dh reads W transposed (K = vocabulary),
+  // dL/dW reads both dz and h transposed (K = tokens).
+  const int64_t kt_chunk = L.sChunk, kt_h = L.sK;
   for (int64_t c = 0; c < L.nchunks; ++c) {
     int64_t v0 = c * L.Vc;
     int64_t Mc = V - v0 < L.Vc ? V - v0 : L.Vc;
     if (Mc <= 0) break;
     bool last = (c == L.nchunks - 1) || (v0 + L.Vc >= V);
-    const int64_t j = c % kDhGroup;    // position of the chunk in its dL/dh group
+    const int64_t j = c % L.dh_group;  // position of the chunk in its dL/dh group
     const int64_t vg = v0 - j * L.Vc;  // first vocabulary row of the group
-    // recompute the logits of this chunk and form dz (both layouts; the
-    // token-major copy at the chunk's place in the group buffer)
-    GemmArgs gz = gemm_args(at<uint16_t>(ws, L.WK) + (v0 / kTile) * kt_h * kTileElems, kt_h, Mc,
-                            at<uint16_t>(ws, L.hK), kt_h, L.Npad, nullptr, &hdr->num_valid, L.Hk,
-                            nullptr);
+    // recompute the logits of this chunk and form dz at the chunk's place in
+    // the group buffer
+    GemmArgs gz = gemm_args(WK + (v0 / kTile) * kt_h * kTileElems, kt_h, Mc, hK, kt_h, L.R,
+                            nullptr, &hdr->num_valid, L.Hk, nullptr);
     uint16_t* dz_c = dz + j * (L.Vc / kBK) * kTileElems;
-    TRY(timed(K_GEMM_DZ, s, [&] {
-      launch_gemm_dz(gz, lse_p, g_p, dz_c, kt_chunk, grad_weight ? dzT : nullptr, kt_tok, V, v0,
-                     s);
-    }));
+    TRY(timed(K_GEMM_DZ, s, [&] { launch_gemm_dz(gz, lse_p, g_p, dz_c, kt_chunk, V, v0, s); }));
     if (grad_weight) {
-      // dW[v, :] = sum_t dz[t, v] h[t, :] over the valid tokens
-      GemmArgs gw = gemm_args(dzT, kt_tok, Mc, hT, kt_tok, H, nullptr, nullptr, 0,
+      // dW[v, :] = sum_t dz[t, v] h[t, :] over the valid tokens: A = dz and
+      // B = h, both read transposed from their token-major tiled buffers
+      GemmArgs gw = gemm_args(dz, kt_chunk, Mc, hK, kt_h, H, nullptr, nullptr, 0,
                               &hdr->num_valid);
+      gw.a_cb0 = j * (L.Vc / kBK);
       StoreArgs sa{};
       sa.out_bf16 = 0;
       sa.out_rows = nullptr;
@@ -493,9 +514,9 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
         TRY(timed(K_GEMM_DW, s, [&] { launch_gemm_store(gw, sa, true, s); }));
       }
     }
-    if (grad_hidden && (j == kDhGroup - 1 || last)) {
-      // dh[t, :] (+)= sum_{v in group} dz[t, v] W[v, :]
-      GemmArgs gh = gemm_args(dz, kt_chunk, L.Npad, WT, kt_voc, H, &hdr->num_valid, nullptr,
+    if (grad_hidden && (j == L.dh_group - 1 || last)) {
+      // dh[t, :] (+)= sum_{v in group} dz[t, v] W[v, :]: W read transposed
+      GemmArgs gh = gemm_args(dz, kt_chunk, L.R, WK, kt_h, H, &hdr->num_valid, nullptr,
                               round_up(v0 + Mc - vg, kBK), nullptr);
       gh.b_kb0 = vg / kBK;
       StoreArgs sa{};
@@ -513,7 +534,7 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
       }
       sa.add_out = 0;
       sa.out_rows = rows_p;
-      sa.m_limit = L.Npad;
+      sa.m_limit = L.R;
       sa.n_limit = H;
       TRY(timed(K_GEMM_DH, s, [&] { launch_gemm_store(gh, sa, false, s); }));
     }
@@ -528,7 +549,7 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
     oa.hidden = (const uint16_t*)hidden;
     oa.H = H;
     oa.V = V;
-    oa.n = L.Npad;
+    oa.n = L.R;
     for (int b = 0; b < 2; ++b) {
       oa.keys[b] = at<int32_t>(ws, L.okeys[b]);
       oa.vals[b] = at<int32_t>(ws, L.ovals[b]);
@@ -563,18 +584,21 @@ const char* grpo_status_string(grpo_status st) {
     case GRPO_ERR_HIP: return "a HIP runtime call failed";
     case GRPO_ERR_TOKEN_RANGE: return "a token id was outside [0, V)";
     case GRPO_ERR_SEQLENS: return "cu_seqlens was not monotone from 0 to N";
+    case GRPO_ERR_CAPACITY: return "more valid rows than the workspace was sized for (max_valid)";
   }
   return "unknown status";
 }
 
 size_t grpo_workspace_bytes(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V,
-                            int64_t num_seqs) {
+                            int64_t num_seqs, int64_t max_valid, size_t dz_budget) {
   if (op != GRPO_OP_LOGPROB_FWD && op != GRPO_OP_LOSS_FWD_BWD && op != GRPO_OP_SFT_FWD_BWD)
     return 0;
   if (check_sizes(dt, N, H, V) != GRPO_OK || num_seqs < 1) return 0;
+  if (max_valid < 0 || max_valid > N) return 0;
   if (op != GRPO_OP_LOGPROB_FWD && check_bwd_sizes(dt, N, H, V) != GRPO_OK) return 0;
-  if (op == GRPO_OP_SFT_FWD_BWD) return layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, 1).total;
-  return layout(op, dt, N, H, V, num_seqs).total;
+  if (op == GRPO_OP_SFT_FWD_BWD)
+    return layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, 1, max_valid, dz_budget).total;
+  return layout(op, dt, N, H, V, num_seqs, max_valid, dz_budget).total;
 }
 
 grpo_status group_advantages(const float* rewards, int64_t num_prompts, int32_t group_size,
@@ -598,7 +622,7 @@ grpo_status grpo_pack_valid(const uint8_t* mask, const int64_t* cu_seqlens, int6
                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (!cu_seqlens || !rows || !counts || !num_valid) return GRPO_ERR_NULL;
   if (N < 1 || N >= (1ll << 31) - kTile || num_seqs < 1 || num_seqs > N) return GRPO_ERR_SHAPE;
-  Layout L = layout(GRPO_OP_LOGPROB_FWD, GRPO_F32, N, 1, 1, num_seqs);
+  Layout L = layout(GRPO_OP_LOGPROB_FWD, GRPO_F32, N, 1, 1, num_seqs, 0, 0);
   TRY(check_ws(workspace, workspace_bytes, L));
   TRY(check_device());
   return run_pack(L, workspace, mask, nullptr, 1, cu_seqlens, num_seqs, N, rows, counts,
@@ -629,6 +653,7 @@ grpo_status grpo_pack_valid_static(const uint8_t* mask, const int64_t* cu_seqlen
   a.y_p = nullptr;
   a.pidx = nullptr;
   a.num_valid_out = num_valid;
+  a.cap = N;
   a.hdr = (WsHeader*)sc;
   TRY(timed(K_PACK, stream, [&] { launch_pack(a, stream); }));
   if (error_out)
@@ -639,13 +664,14 @@ grpo_status grpo_pack_valid_static(const uint8_t* mask, const int64_t* cu_seqlen
 grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weight,
                              const int64_t* tokens, const uint8_t* mask, int64_t N, int64_t H,
                              int64_t V, float* logp, float* lse, void* workspace,
-                             size_t workspace_bytes, hipStream_t stream) {
+                             size_t workspace_bytes, int64_t max_valid, hipStream_t stream) {
   TRY(check_sizes(dt, N, H, V));
+  if (max_valid < 0 || max_valid > N) return GRPO_ERR_SHAPE;
   if (!hidden || !weight || !tokens) return GRPO_ERR_NULL;
   size_t al = dt == GRPO_BF16 ? 16 : 4;
   if (!aligned(hidden, al) || !aligned(weight, al) || !aligned(tokens, 8)) return GRPO_ERR_ALIGN;
   if ((logp && !aligned(logp, 4)) || (lse && !aligned(lse, 4))) return GRPO_ERR_ALIGN;
-  Layout L = layout(GRPO_OP_LOGPROB_FWD, dt, N, H, V, 1);
+  Layout L = layout(GRPO_OP_LOGPROB_FWD, dt, N, H, V, 1, max_valid, 0);
   TRY(check_ws(workspace, workspace_bytes, L));
   TRY(check_device());
   // one "rollout" covering every row (cu_seqlens = NULL means {0, N})
@@ -670,8 +696,10 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
                               float* token_loss, float* dlogp, uint8_t* clip_flag,
                               void* grad_hidden, grpo_dtype grad_hidden_dt, float* grad_weight,
                               int32_t accumulate_grad_weight, void* workspace,
-                              size_t workspace_bytes, hipStream_t stream) {
+                              size_t workspace_bytes, int64_t max_valid, size_t dz_budget,
+                              hipStream_t stream) {
   TRY(check_bwd_sizes(dt, N, H, V));
+  if (max_valid < 0 || max_valid > N) return GRPO_ERR_SHAPE;
   if (!hidden || !weight || !tokens || !cu_seqlens || !old_logp || !adv || !loss)
     return GRPO_ERR_NULL;
   if (num_seqs < 1 || num_seqs > N) return GRPO_ERR_SHAPE;
@@ -691,7 +719,7 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
   for (const void* p : {(const void*)ref_logp, (const void*)lse_in, (const void*)logp_out,
                         (const void*)lse_out, (const void*)token_loss, (const void*)dlogp})
     if (p && !aligned(p, 4)) return GRPO_ERR_ALIGN;
-  Layout L = layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, num_seqs);
+  Layout L = layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, num_seqs, max_valid, dz_budget);
   TRY(check_ws(workspace, workspace_bytes, L));
   TRY(check_device());
 
@@ -764,8 +792,10 @@ grpo_status sft_ce_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight
                            int64_t V, float* loss, float* logp_out, void* grad_hidden,
                            grpo_dtype grad_hidden_dt, float* grad_weight,
                            int32_t accumulate_grad_weight, void* workspace,
-                           size_t workspace_bytes, hipStream_t stream) {
+                           size_t workspace_bytes, int64_t max_valid, size_t dz_budget,
+                           hipStream_t stream) {
   TRY(check_bwd_sizes(dt, N, H, V));
+  if (max_valid < 0 || max_valid > N) return GRPO_ERR_SHAPE;
   if (!hidden || !weight || !tokens || !loss) return GRPO_ERR_NULL;
   if (grad_hidden && grad_hidden_dt != GRPO_F32 && grad_hidden_dt != GRPO_BF16)
     return GRPO_ERR_DTYPE;
@@ -776,7 +806,7 @@ grpo_status sft_ce_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight
   if ((logp_out && !aligned(logp_out, 4)) || (grad_hidden && !aligned(grad_hidden, 4)) ||
       (grad_weight && !aligned(grad_weight, 4)))
     return GRPO_ERR_ALIGN;
-  Layout L = layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, 1);
+  Layout L = layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, 1, max_valid, dz_budget);
   TRY(check_ws(workspace, workspace_bytes, L));
   TRY(check_device());
   void* ws = workspace;
@@ -874,9 +904,10 @@ grpo_status grpo_check_error(void* workspace, hipStream_t stream) {
   grpo_status st = GRPO_OK;
   if (h.err_seqlens) st = GRPO_ERR_SEQLENS;
   else if (h.err_token) st = GRPO_ERR_TOKEN_RANGE;
-  if (h.err_seqlens || h.err_token) {
-    int32_t zero[2] = {0, 0};
-    if (hipMemcpy(workspace, zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess)
+  else if (h.err_capacity) st = GRPO_ERR_CAPACITY;
+  if (st != GRPO_OK) {
+    h.err_seqlens = h.err_token = h.err_capacity = 0;
+    if (hipMemcpy(workspace, &h, 4 * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess)
       return GRPO_ERR_HIP;
   }
   return st;

@@ -14,8 +14,13 @@ struct GemmArgs {
   int N;                  // rows of B (static bound)
   const int32_t* m_dev;   // optional device bound on M (e.g. the valid-token count)
   const int32_t* n_dev;   // optional device bound on N
-  int64_t a_kt, a_kb0;    // A: blocks per tile-row, first block used
-  int64_t b_kt, b_kb0;    // B: same
+  // Operand storage (tiled layout, 256 x 32 blocks). A natural operand is
+  // stored [rows = its M (or N)][columns = K]: x_kt blocks per block-row, K
+  // starting at block x_kb0. A transposed operand is stored [rows = K]
+  // [columns = its M (or N)]: x_kt blocks per block-row, K starting at row
+  // 32 * x_kb0, its columns starting at block x_cb0.
+  int64_t a_kt, a_kb0, a_cb0;
+  int64_t b_kt, b_kb0, b_cb0;
   int K;                  // contraction length, a multiple of 32 (when k_dev is NULL)
   const int32_t* k_dev;   // optional device K, rounded up to 32 (operands zero-padded)
   int tiles_m, tiles_n;   // 256x256 tiles covering the static M x N
@@ -48,8 +53,7 @@ void launch_gemm_lse(const GemmArgs& g, const int32_t* y_p, float* zy, float2* m
 // dz = -g * exp(z - lse) for a vocabulary chunk starting at row v0 (the
 // sampled id's +g is left to the gradient products' callers)
 void launch_gemm_dz(const GemmArgs& g, const float* lse_p, const float* g_p, uint16_t* dz,
-                    int64_t dz_kt, uint16_t* dzT, int64_t dzT_kt, int64_t V, int64_t v0,
-                    hipStream_t s);
+                    int64_t dz_kt, int64_t V, int64_t v0, hipStream_t s);
 void launch_gemm_store(const GemmArgs& g, const StoreArgs& a, bool grad_weight, hipStream_t s);
 
 // ------------------------------------------------------------- packing
@@ -67,6 +71,7 @@ struct PackArgs {
   int32_t* y_p;      // [N] packed -> token id (optional)
   int32_t* pidx;     // [N] row -> packed or -1 (optional)
   int32_t* num_valid_out;  // optional extra copy of the count
+  int64_t cap;             // more valid rows than this: err_capacity, and no row is valid
   WsHeader* hdr;
 };
 void launch_pack(const PackArgs& a, hipStream_t s);
@@ -175,11 +180,6 @@ void launch_gather_dot_bf16(const uint16_t* hidden, const uint16_t* W, int64_t H
 void launch_tile_rows(const uint16_t* in, int64_t ld_in, const int32_t* rows, int64_t n_static,
                       const WsHeader* hdr, int64_t r_pad, int64_t K, int64_t stride,
                       uint16_t* out, hipStream_t s);
-// Tiled layout of the transpose of those rows: round_up(K, 256) rows x
-// n_pad columns (n_pad a multiple of 64), invalid rows as zero columns.
-void launch_transpose_tiled(const uint16_t* in, int64_t ld_in, const int32_t* rows,
-                            int64_t n_static, const WsHeader* hdr, int64_t n_pad, int64_t K,
-                            int64_t stride, uint16_t* out, hipStream_t s);
 void launch_zero_masked_rows(const int32_t* pidx, int64_t N, int64_t H, void* out, int out_bf16,
                              hipStream_t s);
 void launch_f32_score(const float* hidden, const float* W, int64_t H, int64_t V,

@@ -23,7 +23,7 @@ OP_LOGPROB_FWD, OP_LOSS_FWD_BWD, OP_SFT_FWD_BWD = 0, 1, 2
 STATUS = {0: "GRPO_OK", 1: "GRPO_ERR_NULL", 2: "GRPO_ERR_SHAPE", 3: "GRPO_ERR_DTYPE",
           4: "GRPO_ERR_PARAM", 5: "GRPO_ERR_ALIGN", 6: "GRPO_ERR_WORKSPACE",
           7: "GRPO_ERR_DEVICE", 8: "GRPO_ERR_HIP", 9: "GRPO_ERR_TOKEN_RANGE",
-          10: "GRPO_ERR_SEQLENS"}
+          10: "GRPO_ERR_SEQLENS", 11: "GRPO_ERR_CAPACITY"}
 
 # Every symbol include/grpo.h declares, with its ctypes signature.
 _vp, _i64, _i32, _f32, _sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float,
@@ -33,17 +33,17 @@ SIGNATURES = {
     "grpo_pack_valid": (_i32, [_vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _sz, _vp]),
     "grpo_pack_valid_static": (_i32, [_vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp]),
     "grpo_logprob_fwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp, _sz,
-                                _vp]),
+                                _i64, _vp]),
     "grpo_loss_fwd_bwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _vp, _vp,
                                  _vp, _f32, _f32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
-                                 _i32, _vp, _i32, _vp, _sz, _vp]),
+                                 _i32, _vp, _i32, _vp, _sz, _i64, _sz, _vp]),
     "sft_ce_fwd_bwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp, _i32,
-                              _vp, _i32, _vp, _sz, _vp]),
+                              _vp, _i32, _vp, _sz, _i64, _sz, _vp]),
     "adamw_step": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _f32, _f32, _f32, _f32, _f32, _i64,
                           _vp]),
     "triton_rule_reward": (_i32, [_vp, _i64, _vp, _i64, _vp, _i32, _i32, _f32, _f32, _vp, _vp,
                                _vp]),
-    "grpo_workspace_bytes": (_sz, [_i32, _i32, _i64, _i64, _i64, _i64]),
+    "grpo_workspace_bytes": (_sz, [_i32, _i32, _i64, _i64, _i64, _i64, _i64, _sz]),
     "grpo_check_error": (_i32, [_vp, _vp]),
     "grpo_status_string": (ctypes.c_char_p, [_i32]),
     "grpo_profile_enable": (None, [_i32]),
@@ -156,8 +156,9 @@ def _on_tensor_device(fn):
 _ws_cache: dict = {}
 
 
-def workspace_bytes(op: int, dt: int, N: int, H: int, V: int, num_seqs: int = 1) -> int:
-    return int(load().grpo_workspace_bytes(op, dt, N, H, V, num_seqs))
+def workspace_bytes(op: int, dt: int, N: int, H: int, V: int, num_seqs: int = 1,
+                    max_valid: int = 0, dz_budget: int = 0) -> int:
+    return int(load().grpo_workspace_bytes(op, dt, N, H, V, num_seqs, max_valid, dz_budget))
 
 
 def workspace(nbytes: int, device=None) -> torch.Tensor:
@@ -221,8 +222,9 @@ def pack_valid(mask: torch.Tensor | None, cu_seqlens: torch.Tensor):
 
 @_on_tensor_device
 def logprob_fwd(hidden: torch.Tensor, weight: torch.Tensor, tokens: torch.Tensor,
-                mask: torch.Tensor | None = None, check: bool = False):
-    """Per-token log-prob and log-sum-exp over the vocabulary: (logp, lse), fp32 [N]."""
+                mask: torch.Tensor | None = None, check: bool = False, max_valid: int = 0):
+    """Per-token log-prob and log-sum-exp over the vocabulary: (logp, lse), fp32 [N].
+    max_valid: the most valid rows the mask has (0: N), which sizes the workspace."""
     _need(hidden, "hidden")
     _need(weight, "weight", hidden.dtype)
     _need(tokens, "tokens", torch.int64)
@@ -233,10 +235,11 @@ def logprob_fwd(hidden: torch.Tensor, weight: torch.Tensor, tokens: torch.Tensor
     dt = _dt(hidden)
     logp = torch.empty(N, dtype=torch.float32, device=hidden.device)
     lse = torch.empty(N, dtype=torch.float32, device=hidden.device)
-    ws = workspace(workspace_bytes(OP_LOGPROB_FWD, dt, N, H, V, 1), hidden.device)
+    ws = workspace(workspace_bytes(OP_LOGPROB_FWD, dt, N, H, V, 1, max_valid), hidden.device)
     m = None if mask is None else _need(mask, "mask").view(torch.uint8)
     st = load().grpo_logprob_fwd(dt, _ptr(hidden), _ptr(weight), _ptr(tokens), _ptr(m), N, H, V,
-                                 _ptr(logp), _ptr(lse), _ptr(ws), ws.numel(), _stream())
+                                 _ptr(logp), _ptr(lse), _ptr(ws), ws.numel(), max_valid,
+                                 _stream())
     _check(st, "grpo_logprob_fwd")
     if check:
         check_error(ws)
@@ -249,10 +252,11 @@ def loss_fwd_bwd(hidden, weight, tokens, mask, cu_seqlens, old_logp, ref_logp, a
                  lse_in=None, grad_hidden: bool = True, grad_weight: bool = True,
                  grad_hidden_dtype=None, grad_weight_out: torch.Tensor | None = None,
                  accumulate_grad_weight: bool = False, token_outputs: bool = True,
-                 check: bool = False) -> dict:
+                 check: bool = False, max_valid: int = 0, dz_budget: int = 0) -> dict:
     """GRPO loss (Eq. 1, k3 KL) and its gradients. Returns a dict of tensors:
     loss [1], logp/lse/token_loss/dlogp [N], clip_flag uint8 [N],
-    grad_hidden [N,H], grad_weight [V,H] fp32 (as requested)."""
+    grad_hidden [N,H], grad_weight [V,H] fp32 (as requested). max_valid (0: N)
+    and dz_budget (bytes, 0: default) size the workspace (see grpo.h)."""
     _need(hidden, "hidden")
     _need(weight, "weight", hidden.dtype)
     _need(tokens, "tokens", torch.int64)
@@ -290,7 +294,7 @@ def loss_fwd_bwd(hidden, weight, tokens, mask, cu_seqlens, old_logp, ref_logp, a
                                                torch.float32), "grad_weight_out", V, H)
         else:
             out["grad_weight"] = torch.empty(V, H, **f32)
-    ws = workspace(workspace_bytes(OP_LOSS_FWD_BWD, dt, N, H, V, B), dev)
+    ws = workspace(workspace_bytes(OP_LOSS_FWD_BWD, dt, N, H, V, B, max_valid, dz_budget), dev)
     m = None if mask is None else _need(mask, "mask").view(torch.uint8)
     g = out.get
     st = load().grpo_loss_fwd_bwd(
@@ -299,7 +303,7 @@ def loss_fwd_bwd(hidden, weight, tokens, mask, cu_seqlens, old_logp, ref_logp, a
         _ptr(out["loss"]), _ptr(g("logp")), _ptr(g("lse")), _ptr(g("token_loss")),
         _ptr(g("dlogp")), _ptr(g("clip_flag")), _ptr(g("grad_hidden")),
         _dt(out["grad_hidden"]) if grad_hidden else F32, _ptr(g("grad_weight")),
-        int(accumulate_grad_weight), _ptr(ws), ws.numel(), _stream())
+        int(accumulate_grad_weight), _ptr(ws), ws.numel(), max_valid, dz_budget, _stream())
     _check(st, "grpo_loss_fwd_bwd")
     if check:
         check_error(ws)
@@ -311,7 +315,7 @@ def sft_ce_fwd_bwd(hidden, weight, tokens, mask=None, grad_hidden: bool = True,
                    grad_weight: bool = True, grad_hidden_dtype=None,
                    grad_weight_out: torch.Tensor | None = None,
                    accumulate_grad_weight: bool = False, logp_out: bool = True,
-                   check: bool = False) -> dict:
+                   check: bool = False, max_valid: int = 0, dz_budget: int = 0) -> dict:
     """SFT next-token cross-entropy (mean over supervised tokens) and its gradients.
     Returns loss [1], logp [N] (if logp_out), grad_hidden [N,H], grad_weight [V,H] fp32."""
     _need(hidden, "hidden")
@@ -336,14 +340,14 @@ def sft_ce_fwd_bwd(hidden, weight, tokens, mask=None, grad_hidden: bool = True,
                                                torch.float32), "grad_weight_out", V, H)
         else:
             out["grad_weight"] = torch.empty(V, H, **f32)
-    ws = workspace(workspace_bytes(OP_SFT_FWD_BWD, dt, N, H, V, 1), dev)
+    ws = workspace(workspace_bytes(OP_SFT_FWD_BWD, dt, N, H, V, 1, max_valid, dz_budget), dev)
     m = None if mask is None else _need(mask, "mask").view(torch.uint8)
     g = out.get
     st = load().sft_ce_fwd_bwd(
         dt, _ptr(hidden), _ptr(weight), _ptr(tokens), _ptr(m), N, H, V, _ptr(out["loss"]),
         _ptr(g("logp")), _ptr(g("grad_hidden")),
         _dt(out["grad_hidden"]) if grad_hidden else F32, _ptr(g("grad_weight")),
-        int(accumulate_grad_weight), _ptr(ws), ws.numel(), _stream())
+        int(accumulate_grad_weight), _ptr(ws), ws.numel(), max_valid, dz_budget, _stream())
     _check(st, "sft_ce_fwd_bwd")
     if check:
         check_error(ws)

@@ -47,14 +47,15 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_status_strings(lib):
-    for st in range(11):
+    for st in range(12):
         s = lib.grpo_status_string(st)
         assert s and s != b"unknown status"
     assert lib.grpo_status_string(99) == b"unknown status"
 
 
 def test_workspace_bytes(lib):
-    ws = lib.grpo_workspace_bytes
+    def ws(op, dt, N, H, V, B, max_valid=0, dz_budget=0):
+        return lib.grpo_workspace_bytes(op, dt, N, H, V, B, max_valid, dz_budget)
     assert ws(0, 1, 100, 64, 1000, 1) > 0
     assert ws(1, 1, 100, 64, 1000, 4) > ws(0, 1, 100, 64, 1000, 4)
     assert ws(1, 1, 1000, 64, 1000, 4) > ws(1, 1, 100, 64, 1000, 4)
@@ -74,6 +75,16 @@ def test_workspace_bytes(lib):
     assert ws(2, 1, (1 << 22) + 1, 64, 1000, 1) == 0
     assert ws(0, 1, (1 << 22) + 1, 64, 1000, 1) > 0
     assert ws(1, 0, (1 << 22) + 1, 64, 1000, 1) > 0
+    # max_valid caps the token-indexed buffers; beyond N (or negative) it is an error
+    full = ws(1, 1, 131072, 4096, 155136, 64)
+    assert ws(1, 1, 131072, 4096, 155136, 64, 131072) == full
+    assert ws(1, 1, 131072, 4096, 155136, 64, 65536) < full * 0.6
+    assert ws(1, 1, 131072, 4096, 155136, 64, 131073) == 0
+    assert ws(1, 1, 131072, 4096, 155136, 64, -1) == 0
+    assert ws(0, 1, 1000, 64, 1000, 1, 100) < ws(0, 1, 1000, 64, 1000, 1)
+    # a smaller logits-gradient budget gives a smaller workspace
+    assert ws(1, 1, 131072, 4096, 155136, 64, 0, 4 << 30) < full - (2 << 30)
+    assert ws(2, 1, 131072, 4096, 155136, 1, 0, 4 << 30) < ws(2, 1, 131072, 4096, 155136, 1)
 
 
 NULL = None
@@ -84,7 +95,7 @@ def _loss(lib, **kw):
     a = dict(dt=1, hidden=P, weight=P, tokens=P, mask=NULL, cu=P, B=2, N=8, H=64, V=100,
              old=P, ref=P, adv=P, eps=0.2, beta=0.01, agg=0, lse_in=NULL, loss=P, logp=NULL,
              lse=NULL, tl=NULL, dlogp=NULL, clip=NULL, gh=NULL, gh_dt=1, gw=NULL, acc=0,
-             ws=NULL, ws_bytes=0, stream=NULL)
+             ws=NULL, ws_bytes=0, max_valid=0, dz_budget=0, stream=NULL)
     a.update(kw)
     return lib.grpo_loss_fwd_bwd(*a.values())
 
@@ -112,6 +123,8 @@ def test_loss_argument_errors(lib):
     assert _loss(lib) == 6                          # no workspace
     assert _loss(lib, ws=ctypes.c_void_p(0x1010), ws_bytes=1 << 40) == 6  # misaligned
     assert _loss(lib, ws=P, ws_bytes=16) == 6       # too small
+    assert _loss(lib, max_valid=-1) == 2
+    assert _loss(lib, max_valid=9) == 2             # more than N
 
 
 def test_other_entry_point_errors(lib):
@@ -123,14 +136,15 @@ def test_other_entry_point_errors(lib):
     # one wave per prompt: the grid's thread count must stay below 2^32
     assert adv(P, 4 * ((1 << 24) - 1) + 1, 2, 1e-6, 1, P, NULL) == 2
     fwd = lib.grpo_logprob_fwd
-    assert fwd(1, NULL, P, P, NULL, 8, 64, 100, P, P, P, 1 << 30, NULL) == 1
-    assert fwd(1, P, P, P, NULL, 8, 12, 100, P, P, P, 1 << 30, NULL) == 2
-    assert fwd(1, P, P, P, NULL, 8, 64, 0, P, P, P, 1 << 30, NULL) == 2
-    assert fwd(2, P, P, P, NULL, 8, 64, 100, P, P, P, 1 << 30, NULL) == 3
-    assert fwd(1, P, P, P, NULL, 8, 64, 100, P, P, P, 8, NULL) == 6
+    assert fwd(1, NULL, P, P, NULL, 8, 64, 100, P, P, P, 1 << 30, 0, NULL) == 1
+    assert fwd(1, P, P, P, NULL, 8, 12, 100, P, P, P, 1 << 30, 0, NULL) == 2
+    assert fwd(1, P, P, P, NULL, 8, 64, 0, P, P, P, 1 << 30, 0, NULL) == 2
+    assert fwd(2, P, P, P, NULL, 8, 64, 100, P, P, P, 1 << 30, 0, NULL) == 3
+    assert fwd(1, P, P, P, NULL, 8, 64, 100, P, P, P, 8, 0, NULL) == 6
     # bf16 scoring grid beyond 32 bits; fp32 H beyond its LDS rows
-    assert fwd(1, P, P, P, NULL, 1 << 22, 8, (1 << 31) - 512, P, P, P, 1 << 30, NULL) == 2
-    assert fwd(0, P, P, P, NULL, 8, 8200, 100, P, P, P, 1 << 30, NULL) == 2
+    assert fwd(1, P, P, P, NULL, 1 << 22, 8, (1 << 31) - 512, P, P, P, 1 << 30, 0, NULL) == 2
+    assert fwd(0, P, P, P, NULL, 8, 8200, 100, P, P, P, 1 << 30, 0, NULL) == 2
+    assert fwd(1, P, P, P, NULL, 8, 64, 100, P, P, P, 1 << 30, 9, NULL) == 2
     pk = lib.grpo_pack_valid
     assert pk(NULL, NULL, 2, 8, P, P, P, P, 1 << 30, NULL) == 1
     assert pk(NULL, P, 0, 8, P, P, P, P, 1 << 30, NULL) == 2
@@ -140,7 +154,8 @@ def test_other_entry_point_errors(lib):
 
 def _sft(lib, **kw):
     a = dict(dt=1, hidden=P, weight=P, tokens=P, mask=NULL, N=8, H=64, V=100, loss=P,
-             logp=NULL, gh=NULL, gh_dt=1, gw=NULL, acc=0, ws=NULL, ws_bytes=0, stream=NULL)
+             logp=NULL, gh=NULL, gh_dt=1, gw=NULL, acc=0, ws=NULL, ws_bytes=0, max_valid=0,
+             dz_budget=0, stream=NULL)
     a.update(kw)
     return lib.sft_ce_fwd_bwd(*a.values())
 
@@ -159,6 +174,7 @@ def test_sft_argument_errors(lib):
     assert _sft(lib, logp=ctypes.c_void_p(0x1002)) == 5
     assert _sft(lib) == 6                           # no workspace
     assert _sft(lib, ws=P, ws_bytes=16) == 6        # too small
+    assert _sft(lib, max_valid=9) == 2
 
 
 def test_adamw_argument_errors(lib):
