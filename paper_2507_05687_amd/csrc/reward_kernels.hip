@@ -17,16 +17,22 @@
 //   launch: the name, not preceded by an identifier byte, blanks, "[", a
 //     bracket-balanced run to the matching "]", blanks, "(".
 //
-// One 256-thread workgroup per completion. The completion is first copied
-// into LDS (when it fits; a longer one is read from global memory by the
-// same code), so the byte-at-a-time parsing below runs at LDS latency.
-// Phase 1: each thread tests one position in 256 for a decorator and parses
-// the function after it; the names go to a list in LDS. Phase 2: all threads
-// search the completion for a launch of each name, 256 positions at a time.
-// is_Triton is an "exists" over decorators, so the order in which threads
-// find them does not change the result. If more decorated functions are
-// found than the list holds, one wave goes through all decorators in text
-// order instead.
+// One 256-thread workgroup per completion. A completion that fits is first
+// copied into LDS, and its check costs a bounded amount of work per byte:
+//   1. every thread tests 16 bytes in 4 KiB for a decorator; the functions
+//      they decorate are followed up (by whole waves when there are few
+//      decorators, else by the thread that found each) and their names go
+//      into a hash table in LDS, each distinct name once;
+//   2. a prefix-depth index of "[" / "]" over 32-byte chunks (depth at each
+//      chunk's start, lowest depth within each chunk and each 1 KiB block)
+//      lets a bracket find its match in at most a few hundred LDS reads;
+//   3. every thread tests 16 bytes in 4 KiB for a "[" after an identifier
+//      (and blanks) whose match is followed by blanks and "(" (a launch
+//      site), and looks the identifier up in the table.
+// is_Triton is an "exists" over decorators and launch sites, so the order in
+// which threads find them does not change the result. A completion longer
+// than the LDS copy is checked from global memory by simpler code: one name
+// list, and a text scan per listed name.
 #include "kernels.h"
 
 namespace grpo {
@@ -197,9 +203,20 @@ __device__ __forceinline__ bool launch_at(const T& X, int64_t r, int64_t ns, int
 }
 
 constexpr int kRrThreads = 256;
-constexpr int kRrLds = 128 * 1024;  // completions up to this size (less 15 bytes) go to LDS
-constexpr int kRrNames = 64;        // decorated functions listed per completion
-constexpr int kRrList = 256;        // decorators / launch candidates listed per completion
+constexpr int kRrLds = 96 * 1024;  // completions up to this size (less 15 bytes) go to LDS
+constexpr int kRrNames = 64;       // decorated functions listed per completion (global path)
+constexpr int kRrList = 256;       // decorators followed up by whole waves (LDS path)
+constexpr int kRrChunk = 32;                        // bytes per entry of the bracket index
+constexpr int kRrChunks = kRrLds / kRrChunk;        // chunks of the longest LDS completion
+constexpr int kRrBlock = 32;                        // chunks per block of the bracket index
+constexpr int kRrBlocks = kRrChunks / kRrBlock;
+// Name table slots: half again as many as the decorated functions a
+// completion in LDS can hold (each takes at least "@triton.jit", a newline,
+// "def ", one byte of name and "(", 18 bytes), so the table is at most two
+// thirds full and probing always ends at an empty slot.
+constexpr int kRrTable = 8192;
+constexpr uint32_t kRrEmpty = 0xffffffffu;
+static_assert(kRrLds / 18 * 3 / 2 < kRrTable && kRrLds < (1 << 17), "name table sizing");
 
 struct RrShared {
   int count;  // decorated functions found (may exceed kRrNames)
@@ -418,87 +435,299 @@ __device__ bool wave_decorated_name(const LdsText& X, int64_t p, int64_t& ns, in
   return false;
 }
 
-// position of the "[" of a launch candidate name [ at r, or -1
-__device__ __forceinline__ int64_t launch_open(const LdsText& X, int64_t r, int64_t ns, int64_t nl) {
-  if (!(r + nl <= X.n && X[r] == X[ns] && (r == 0 || !is_ident(X[r - 1])))) return -1;
-  for (int64_t k = 1; k < nl; ++k)
-    if (X[r + k] != X[ns + k]) return -1;
-  const int64_t s = skip_blanks(X, r + nl);
-  return s < X.n && X[s] == '[' ? s : -1;
+// ---- the LDS path's name table and bracket index
+
+// A 16-byte aligned LDS chunk holding X[i] (i >= 0): its bytes, and the text
+// index of its first byte.
+__device__ __forceinline__ u32x4 lds_chunk(const LdsText& X, int64_t i, int64_t& c0) {
+  const int64_t a = (i + X.sh) & ~(int64_t)15;
+  c0 = a - X.sh;
+  return *(const u32x4*)(X.base + a);
+}
+__device__ __forceinline__ uint8_t chunk_byte(const u32x4& w, int k) {
+  return (uint8_t)(w[k >> 2] >> (8 * (k & 3)));
 }
 
-// is_Triton of an LDS completion, the same in every thread: decorators and
-// launch candidates are listed by all threads, then followed up by whole
-// waves; an overflowing list falls back to is_triton_block.
-__device__ bool is_triton_waves(const LdsText& X, int require_launch, RrShared& sh) {
+// skip_blanks reading 16 bytes at a time
+__device__ int64_t lds_skip_blanks(const LdsText& X, int64_t i) {
+  while (i < X.n) {
+    int64_t c0;
+    const u32x4 w = lds_chunk(X, i, c0);
+    for (int k = (int)(i - c0); k < 16; ++k, ++i)
+      if (i >= X.n || !is_blank(chunk_byte(w, k))) return i < X.n ? i : X.n;
+  }
+  return X.n;
+}
+
+// last index <= i holding a byte other than a blank, or -1, walking back 16
+// bytes at a time
+__device__ int64_t lds_back_skip_blanks(const LdsText& X, int64_t i) {
+  while (i >= 0) {
+    int64_t c0;
+    const u32x4 w = lds_chunk(X, i, c0);
+    for (int k = (int)(i - c0); k >= 0; --k, --i)
+      if (c0 + k < 0 || !is_blank(chunk_byte(w, k))) return c0 + k < 0 ? -1 : i;
+  }
+  return -1;
+}
+
+// first byte of the identifier run that ends at r (X[r] is an identifier
+// byte), walking back 16 bytes at a time
+__device__ int64_t lds_ident_start(const LdsText& X, int64_t r) {
+  int64_t i = r;
+  while (i > 0) {
+    int64_t c0;
+    const u32x4 w = lds_chunk(X, i - 1, c0);
+    for (int k = (int)(i - 1 - c0); k >= 0; --k, --i)
+      if (c0 + k < 0 || !is_ident(chunk_byte(w, k))) return i;
+  }
+  return 0;
+}
+
+// FNV-1a hash of the identifier run [s, e)
+__device__ uint32_t ident_hash(const LdsText& X, int64_t s, int64_t e) {
+  uint32_t h = 2166136261u;
+  int64_t i = s;
+  while (i < e) {
+    int64_t c0;
+    const u32x4 w = lds_chunk(X, i, c0);
+    for (int k = (int)(i - c0); k < 16 && i < e; ++k, ++i) h = (h ^ chunk_byte(w, k)) * 16777619u;
+  }
+  return h;
+}
+
+// the identifier runs starting at a and at b are equal
+__device__ bool same_ident(const LdsText& X, int64_t a, int64_t b) {
+  for (int64_t k = 0;; ++k) {
+    const bool ia = a + k < X.n && is_ident(X[a + k]);
+    const bool ib = b + k < X.n && is_ident(X[b + k]);
+    if (ia != ib) return false;
+    if (!ia) return true;
+    if (X[a + k] != X[b + k]) return false;
+  }
+}
+
+// A slot holds the position of a name's first byte (17 bits) and 15 more
+// bits of its hash; kRrEmpty is free. Insertion keeps one slot per distinct
+// name.
+__device__ void name_insert(const LdsText& X, int64_t ns, int64_t nl, uint32_t* table) {
+  const uint32_t h = ident_hash(X, ns, ns + nl);
+  const uint32_t v = (uint32_t)ns | ((h >> 13) << 17);
+  for (uint32_t slot = h & (kRrTable - 1);; slot = (slot + 1) & (kRrTable - 1)) {
+    const uint32_t old = atomicCAS(&table[slot], kRrEmpty, v);
+    if (old == kRrEmpty) return;
+    if ((old >> 17) == (v >> 17) && same_ident(X, old & 0x1ffff, ns)) return;
+  }
+}
+__device__ bool name_lookup(const LdsText& X, int64_t s, int64_t e, const uint32_t* table) {
+  const uint32_t h = ident_hash(X, s, e);
+  for (uint32_t slot = h & (kRrTable - 1);; slot = (slot + 1) & (kRrTable - 1)) {
+    const uint32_t v = table[slot];
+    if (v == kRrEmpty) return false;
+    if ((v >> 17) == ((h >> 13) & 0x7fff) && same_ident(X, v & 0x1ffff, s)) return true;
+  }
+}
+
+// The bracket index covers the LDS copy in 32-byte chunks aligned to the
+// copy (chunk c holds text bytes 32c - sh .. 32c - sh + 31; bytes outside the
+// text count as neither bracket).
+struct BracketIndex {
+  int32_t* cst;  // depth ("[" minus "]") before each chunk
+  int32_t* cmn;  // lowest depth after any text byte of each chunk (2^30 if none)
+  int32_t* bmn;  // lowest of cmn over each block of 32 chunks
+  int nch, nbl;
+};
+
+__device__ __forceinline__ int bracket_step(uint8_t b) { return (b == '[') - (b == ']'); }
+
+// net depth change and lowest relative depth of chunk c
+__device__ __forceinline__ void chunk_stats(const LdsText& X, int c, int& net, int& lo) {
+  const u32x4 w0 = *(const u32x4*)(X.base + c * kRrChunk);
+  const u32x4 w1 = *(const u32x4*)(X.base + c * kRrChunk + 16);
+  const int64_t t0 = (int64_t)c * kRrChunk - X.sh;  // text index of the chunk's first byte
+  int d = 0, l = 1 << 30;
+  static_for<kRrChunk>([&](auto k) {
+    const u32x4& w = k.value < 16 ? w0 : w1;
+    const uint8_t b = chunk_byte(w, k.value & 15);
+    if (t0 + k.value >= 0 && t0 + k.value < X.n) {
+      d += bracket_step(b);
+      l = d < l ? d : l;
+    }
+  });
+  net = d;
+  lo = l;
+}
+
+// Builds the index (all threads; ends with a barrier). Lane l of a row of 256
+// takes chunk 256 row + l (consecutive chunks, free of bank conflicts); depths
+// are carried from row to row. wtot: 4 ints of LDS.
+__device__ void build_bracket_index(const LdsText& X, BracketIndex& bi, int32_t* wtot) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  bi.nch = (int)((X.n + X.sh + kRrChunk - 1) / kRrChunk);
+  bi.nbl = (bi.nch + kRrBlock - 1) / kRrBlock;
+  int carry = 0;  // depth before this row
+  for (int row = 0; row * kRrThreads < bi.nch; ++row) {
+    const int c = row * kRrThreads + tid;
+    int net = 0, lo = 1 << 30;
+    if (c < bi.nch) chunk_stats(X, c, net, lo);
+    int incl = net;  // inclusive scan within the wave
+    static_for<6>([&](auto sft) {
+      const int t = __shfl_up(incl, 1 << sft.value, 64);
+      if (lane >= (1 << sft.value)) incl += t;
+    });
+    if (lane == 63) wtot[wave] = incl;
+    __syncthreads();
+    int before = carry + incl - net, total = 0;
+    for (int v = 0; v < kRrThreads / 64; ++v) {
+      before += v < wave ? wtot[v] : 0;
+      total += wtot[v];
+    }
+    if (c < bi.nch) {
+      bi.cst[c] = before;
+      bi.cmn[c] = lo == (1 << 30) ? lo : before + lo;
+    }
+    carry += total;
+    __syncthreads();
+  }
+  for (int b = tid; b < bi.nbl; b += kRrThreads) {
+    int m = 1 << 30;
+    const int e = (b + 1) * kRrBlock < bi.nch ? (b + 1) * kRrBlock : bi.nch;
+    for (int c = b * kRrBlock; c < e; ++c) m = bi.cmn[c] < m ? bi.cmn[c] : m;
+    bi.bmn[b] = m;
+  }
+  __syncthreads();
+}
+
+// Over the text bytes j of chunk c with from <= j < to, from depth d: the
+// index just past the first byte after which the depth equals k, else -1
+// (d is then the depth after the last byte taken). The chunk is read into
+// registers once.
+__device__ __forceinline__ int64_t chunk_find_depth(const LdsText& X, int c, int64_t from,
+                                                    int64_t to, int& d, int k) {
+  const u32x4 w0 = *(const u32x4*)(X.base + c * kRrChunk);
+  const u32x4 w1 = *(const u32x4*)(X.base + c * kRrChunk + 16);
+  const int64_t t0 = (int64_t)c * kRrChunk - X.sh;
+  if (from < 0) from = 0;
+  if (to > X.n) to = X.n;
+  int64_t hit = -1;
+  static_for<kRrChunk>([&](auto q) {
+    const int64_t j = t0 + q.value;
+    if (hit < 0 && j >= from && j < to) {
+      d += bracket_step(chunk_byte(q.value < 16 ? w0 : w1, q.value & 15));
+      if (d == k) hit = j + 1;
+    }
+  });
+  return hit;
+}
+
+// X[s] == '[': index just past its matching ']', or -1 (match_close's
+// result). The match is the first byte after s where the depth returns to
+// its value before s: found in s's chunk, else in the first later chunk of
+// s's block, else of the first later block, whose lowest depth reaches it.
+__device__ int64_t bracket_match(const LdsText& X, int64_t s, const BracketIndex& bi) {
+  const int c = (int)((s + X.sh) / kRrChunk);
+  int d = bi.cst[c];
+  chunk_find_depth(X, c, 0, s, d, -(1 << 30));  // the depth before s
+  const int k = d++;  // the target depth; d is now the depth after s
+  const int64_t r = chunk_find_depth(X, c, s + 1, X.n, d, k);
+  if (r >= 0) return r;
+  const int be = (c / kRrBlock + 1) * kRrBlock < bi.nch ? (c / kRrBlock + 1) * kRrBlock : bi.nch;
+  int cc = c + 1;
+  while (cc < be && bi.cmn[cc] > k) ++cc;
+  if (cc >= be) {
+    int b = c / kRrBlock + 1;
+    while (b < bi.nbl && bi.bmn[b] > k) ++b;
+    if (b >= bi.nbl) return -1;
+    cc = b * kRrBlock;
+    while (bi.cmn[cc] > k) ++cc;  // some chunk of block b reaches k
+  }
+  d = bi.cst[cc];
+  return chunk_find_depth(X, cc, 0, X.n, d, k);  // found: cmn[cc] <= k
+}
+
+struct RrTables {
+  uint32_t* names;  // kRrTable slots
+  BracketIndex bi;
+  int32_t* wtot;    // 4 ints
+};
+
+// is_Triton of an LDS completion, the same in every thread.
+__device__ bool is_triton_lds(const LdsText& X, int require_launch, RrShared& sh, RrTables& tb) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   constexpr int kWaves = kRrThreads / 64;
-  for (int64_t base = 0; base < X.n; base += kRrThreads) {
-    const int64_t p = base + tid;
-    if (p < X.n && X[p] == '@' && decorator_at(X, p)) {
-      const int slot = atomicAdd(&sh.nlist, 1);
-      if (slot < kRrList) sh.list[slot] = p;
+  for (int i = tid; i < kRrTable; i += kRrThreads) tb.names[i] = kRrEmpty;
+  // 1. decorators; with at most kRrList of them the waves follow each up
+  // (long scans shared by the wave), else the thread that found it does
+  const int64_t nq = (X.n + X.sh + 15) / 16;  // 16-byte chunks of the copy
+  for (int64_t q = tid; q < nq; q += kRrThreads) {
+    const int64_t t0 = 16 * q - X.sh;  // text index of the chunk's first byte
+    uint32_t m = mask16(*(const u32x4*)(X.base + 16 * q), '@') & range16(t0, 0, X.n);
+    for (; m != 0; m &= m - 1) {
+      const int64_t p = t0 + __builtin_ctz(m);
+      if (decorator_at(X, p)) {
+        const int slot = atomicAdd(&sh.nlist, 1);
+        if (slot < kRrList) sh.list[slot] = p;
+      }
     }
   }
   __syncthreads();
   const int ndeco = sh.nlist;
-  bool overflow = ndeco > kRrList;
-  if (!overflow) {
+  if (ndeco <= kRrList) {
     for (int d = wave; d < ndeco; d += kWaves) {
       int64_t ns = 0, nl = 0;
       if (wave_decorated_name(X, sh.list[d], ns, nl) && lane == 0) {
-        const int slot = atomicAdd(&sh.count, 1);
-        if (slot < kRrNames) {
-          sh.ns[slot] = ns;
-          sh.nl[slot] = nl;
+        atomicAdd(&sh.count, 1);
+        name_insert(X, ns, nl, tb.names);
+      }
+    }
+  } else {
+    for (int64_t q = tid; q < nq; q += kRrThreads) {
+      const int64_t t0 = 16 * q - X.sh;
+      uint32_t m = mask16(*(const u32x4*)(X.base + 16 * q), '@') & range16(t0, 0, X.n);
+      for (; m != 0; m &= m - 1) {
+        const int64_t p = t0 + __builtin_ctz(m);
+        int64_t ns = 0, nl = 0;
+        if (decorator_at(X, p) && decorated_name(X, p, ns, nl)) {
+          atomicAdd(&sh.count, 1);
+          name_insert(X, ns, nl, tb.names);
         }
       }
     }
   }
   __syncthreads();
-  const int count = sh.count;
-  overflow = overflow || count > kRrNames;
-  bool found = false;
-  if (!overflow && (!require_launch || count == 0)) return count > 0;
-  for (int i = 0; i < count && !overflow && !found; ++i) {
-    const int64_t ns = sh.ns[i], nl = sh.nl[i];
-    if (tid == 0) sh.nlist = 0;
-    __syncthreads();
-    for (int64_t base = 0; base < X.n; base += kRrThreads) {
-      const int64_t s = base + tid < X.n ? launch_open(X, base + tid, ns, nl) : -1;
-      if (s >= 0) {
-        const int slot = atomicAdd(&sh.nlist, 1);
-        if (slot < kRrList) sh.list[slot] = s;
-      }
-    }
-    __syncthreads();
-    const int nc = sh.nlist;
-    overflow = nc > kRrList;
+  if (!require_launch || sh.count == 0) return sh.count > 0;
+  // 2. the bracket index
+  build_bracket_index(X, tb.bi, tb.wtot);
+  // 3. launch sites and their names: each thread takes 16-byte chunks of the
+  // copy; every "[" whose preceding non-blank byte ends an identifier is
+  // matched through the index
+  for (int64_t q0 = 0; q0 < nq; q0 += kRrThreads) {
+    const int64_t q = q0 + tid;
     bool hit = false;
-    if (!overflow) {
-      for (int q = wave; q < nc && !hit; q += kWaves) {
-        int64_t e = wave_match_close(X, sh.list[q], '[', ']');
-        if (e >= 0) {
-          e = skip_blanks(X, e);
-          hit = e < X.n && X[e] == '(';
-        }
+    if (q < nq) {
+      const int64_t t0 = 16 * q - X.sh;  // text index of the chunk's first byte
+      uint32_t m = mask16(*(const u32x4*)(X.base + 16 * q), '[') & range16(t0, 0, X.n);
+      while (m != 0 && !hit) {
+        const int64_t s = t0 + __builtin_ctz(m);
+        m &= m - 1;
+        const int64_t r = lds_back_skip_blanks(X, s - 1);
+        if (r < 0 || !is_ident(X[r])) continue;
+        int64_t e = bracket_match(X, s, tb.bi);
+        if (e < 0) continue;
+        e = lds_skip_blanks(X, e);
+        if (e < X.n && X[e] == '(') hit = name_lookup(X, lds_ident_start(X, r), r + 1, tb.names);
       }
     }
-    found = __syncthreads_or(hit);
+    if (__syncthreads_or(hit)) return true;
   }
-  if (!overflow) return found;
-  __syncthreads();
-  if (tid == 0) {
-    sh.count = 0;
-    sh.found = 0;
-  }
-  __syncthreads();
-  return is_triton_block(X, require_launch, sh);
+  return false;
 }
 
 __global__ void __launch_bounds__(kRrThreads) k_rule_reward(RewardArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[kRrLds];
   __shared__ RrShared sh;
+  __shared__ uint32_t names[kRrTable];
+  __shared__ int32_t cst[kRrChunks], cmn[kRrChunks], bmn[kRrBlocks], wtot[kRrThreads / 64];
   const int64_t b = blockIdx.x;
   const int tid = threadIdx.x;
   // a pair outside [0, text_bytes] is an empty completion, like a decreasing one
@@ -522,7 +751,8 @@ __global__ void __launch_bounds__(kRrThreads) k_rule_reward(RewardArgs a) {
     for (int64_t g = (mid > start ? mid : start) + tid; g < s1; g += kRrThreads)
       lds[g - start] = a.text[g];
     __syncthreads();
-    found = is_triton_waves(LdsText{lds, s0 - start, n}, a.require_launch, sh);
+    RrTables tb{names, BracketIndex{cst, cmn, bmn, 0, 0}, wtot};
+    found = is_triton_lds(LdsText{lds, s0 - start, n}, a.require_launch, sh, tb);
   } else {
     __syncthreads();
     found = is_triton_block(GlobalText{a.text + s0, n}, a.require_launch, sh);

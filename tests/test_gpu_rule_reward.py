@@ -165,3 +165,87 @@ def test_offsets_outside_the_text_are_empty_completions():
     f = flags.cpu().numpy()
     assert list(f) == [1, 1, 0, 1, 0, 0, 0, 0]
     assert np.allclose(reward.cpu().numpy(), np.where(f == 1, 0.75, 0.5))
+
+
+# ---- adversarial completions: the check's cost per completion is bounded
+
+KERNEL_K = b"@triton.jit\ndef k(x):pass\n"
+
+
+def _distinct_names(count, launch=None):
+    """count decorated functions with distinct names (28 bytes each), then
+    optionally a launch line."""
+    text = b"".join(b"@triton.jit\ndef n%04d(x):pass\n" % i for i in range(count))
+    return text + (launch or b"")
+
+
+def _unclosed(count, tail=b""):
+    """a decorated k, then count unclosed launch candidates k[ (2 bytes each)"""
+    return KERNEL_K + b"k[" * count + tail
+
+
+def _timed_flags(texts, require_launch):
+    data, offsets = workloads.pack_completions(texts)
+    d, o = torch.from_numpy(data).cuda(), torch.from_numpy(offsets).cuda()
+    p = torch.ones(len(texts), dtype=torch.uint8, device="cuda")
+    grpo.triton_rule_reward(d, o, p, require_launch=require_launch)  # warm-up
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    f, _ = grpo.triton_rule_reward(d, o, p, require_launch=require_launch)
+    e1.record()
+    torch.cuda.synchronize()
+    return f.cpu().numpy(), e0.elapsed_time(e1)
+
+
+def test_many_distinct_names_parity():
+    # parity with the oracle at full size: 2,200 names per completion (61.6 KB)
+    texts = [_distinct_names(2200),
+             _distinct_names(2200, b"n2199[(1,)](0)\n"),
+             _distinct_names(2200, b"n2200[(1,)](0)\n"),   # not a decorated name
+             _distinct_names(2200, b"n0000 [g]\t(1)\n"),
+             _distinct_names(2200, b"xn0001[g](1)\n"),      # preceded by an identifier byte
+             _distinct_names(3000)]
+    _check(texts, np.ones(len(texts), np.uint8))
+
+
+def test_many_distinct_names_batch_time():
+    texts = [_distinct_names(2200)] * 64
+    f, ms = _timed_flags(texts, require_launch=True)
+    print(f"64 completions x 2,200 distinct names, no launch: {ms:.2f} ms")
+    assert not f.any()
+    assert ms < 10.0
+
+
+def test_unclosed_candidates_parity():
+    # the oracle's bracket matching is quadratic here: parity at 4,000 candidates
+    texts = [_unclosed(4000), _unclosed(4000, b"](0)"), _unclosed(4000, b"]"),
+             _unclosed(4000, b"]" * 3999 + b" (1)"), _unclosed(4000, b"]" * 4000 + b"(1)"),
+             _unclosed(4000, b"\n" + b"]" * 2000 + b"(1)")]
+    _check(texts, np.ones(len(texts), np.uint8))
+
+
+def test_unclosed_candidates_batch_time():
+    # 32,000 unclosed k[ per completion (64 KB); the answer follows from the
+    # construction: no "[" is ever closed, so there is no launch; closing the
+    # last one with "](" makes a launch of k
+    texts = [_unclosed(32000)] * 63 + [_unclosed(32000, b"](0)")]
+    f, ms = _timed_flags(texts, require_launch=True)
+    print(f"64 completions x 32,000 unclosed k[: {ms:.2f} ms")
+    assert not f[:63].any() and f[63] == 1
+    assert ms < 10.0
+    f0, _ = _timed_flags(texts, require_launch=False)
+    assert f0.all()
+
+
+def test_bracket_soup():
+    # random runs of launch-like tokens over decorated k and j: every bracket
+    # match of the index against the oracle's scan
+    rng = np.random.default_rng(11)
+    alphabet = [b"k", b"j", b"q", b"[", b"]", b"(", b")", b" ", b"\n", b"[", b"]", b"x"]
+    texts = []
+    for i in range(64):
+        n = int(rng.integers(200, 3000))
+        body = b"".join(alphabet[c] for c in rng.integers(0, len(alphabet), n))
+        head = b"@triton.jit\ndef k(x):pass\n@triton.jit\ndef j(y):pass\n"
+        texts.append(head + body if i % 2 else body + b"\n" + head)
+    _check(texts, np.ones(len(texts), np.uint8))
