@@ -37,11 +37,13 @@
  *    call will see: the token-indexed scratch is sized for it (a ragged
  *    batch with half its rows masked needs about half). A call whose mask
  *    has more valid rows records GRPO_ERR_CAPACITY and treats no row as
- *    valid (all outputs as for masked rows). dz_budget (0 = 48 GiB) bounds
+ *    valid (all outputs as for masked rows). dz_budget (0 = 16 GiB) bounds
  *    the bytes of the logits-gradient chunks of the backward pass; a smaller
  *    budget means narrower vocabulary chunks and more passes over the fp32
- *    dL/dhidden accumulator, never a different result. Pass the same values
- *    to grpo_workspace_bytes and to the call.
+ *    dL/dhidden accumulator: the gradients are then summed in another
+ *    grouping (equal up to fp32 rounding; the same arguments always give the
+ *    same bits). Pass the same values to grpo_workspace_bytes and to the
+ *    call.
  */
 #ifndef GRPO_H_
 #define GRPO_H_

@@ -629,6 +629,12 @@ __global__ void __launch_bounds__(256, 1) k_gemm(GemmArgs g, Epi epi) {
   constexpr int kPerStep = 2 * kJ;  // loads per wave per step
   constexpr int kMfmas = 64;        // MFMAs per wave per step
   constexpr int kSpread = kMfmas / kPerStep;
+  // The loads of a step are issued evenly over the MFMAs that follow its
+  // fragment reads, except in the dL/dh product (only B transposed), which
+  // keeps one load per kSpread MFMAs from the start of the step: each was
+  // the faster order for its product (a load issued in the same slots as the
+  // reads holds the wave's MFMA issue back longer).
+  constexpr bool kLoadsAfterReads = TA || !TB;
   using I0 = std::integral_constant<int, 0>;
 
   const int nk = K / kBK;
@@ -653,8 +659,13 @@ __global__ void __launch_bounds__(256, 1) k_gemm(GemmArgs g, Epi epi) {
       if constexpr (m.value < ReadOps::kOps)
         fread(Nxt{}, StNxt{}, std::integral_constant<int, ReadOps::q(m.value)>{},
               std::integral_constant<int, ReadOps::part(m.value)>{});
-      if constexpr (m.value % kSpread == kSpread - 1)
+      if constexpr (kLoadsAfterReads) {
+        constexpr int l0 = ReadOps::kOps, ls = (kMfmas - l0) / kPerStep;
+        if constexpr (m.value >= l0 && (m.value - l0) % ls == 0 && (m.value - l0) / ls < kPerStep)
+          load(nkt, nl, std::integral_constant<int, (m.value - l0) / ls>{});
+      } else if constexpr (m.value % kSpread == kSpread - 1) {
         load(nkt, nl, std::integral_constant<int, m.value / kSpread>{});
+      }
       __builtin_amdgcn_sched_barrier(0);
     });
     // reads of step kt+1 returned; this wave's loads of step kt+2 landed

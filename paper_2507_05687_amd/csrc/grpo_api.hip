@@ -141,7 +141,7 @@ grpo_status static_scratch(char** out) {
 constexpr size_t kAlign = 256;
 constexpr int64_t kPackSeg = 4096;  // rows per packing workgroup without cu_seqlens
 constexpr int64_t kMaxAdvPrompts = 4 * ((1ll << 24) - 1);  // group_advantages' grid limit
-constexpr size_t kDefaultDzBudget = (size_t)48 << 30;  // bytes for the bf16 dz chunks
+constexpr size_t kDefaultDzBudget = (size_t)16 << 30;  // bytes for the bf16 dz chunks
 constexpr int64_t kVcMax = 8192;                        // columns per vocabulary chunk
 
 struct Layout {
@@ -215,16 +215,15 @@ double chunking_cost(int64_t R, int64_t Vpad, int64_t Hpad, int64_t Vc, int64_t 
 
 // Vocabulary chunks of the backward pass and how many of them one dL/dh
 // product takes. The token-major bf16 dz buffer holds `group` chunks of Vc
-// columns for R rows: it stays within `budget` bytes (0: kDefaultDzBudget) and
-// within a quarter of the vocabulary (the logits gradient is never held
-// whole). Vc (a multiple of 256, at most kVcMax) and the group are the pair
+// columns for R rows and stays within `budget` bytes (0: kDefaultDzBudget):
+// a small batch may hold the whole vocabulary (one dL/dh product, no
+// accumulator). Vc (a multiple of 256, at most kVcMax) and the group are the pair
 // of least chunking_cost; all chunks but the last are Vc wide.
 void chunking(int64_t R, int64_t Vpad, int64_t Hpad, size_t budget, int64_t& Vc,
               int64_t& nchunks, int64_t& group) {
   if (budget == 0) budget = kDefaultDzBudget;
   int64_t cols = (int64_t)(budget / (2 * (size_t)R)) / kTile * kTile;
-  const int64_t quarter = round_up(ceil_div(Vpad, 4), kTile);
-  if (cols > quarter) cols = quarter;
+  if (cols > Vpad) cols = Vpad;
   if (cols < kTile) cols = kTile;
   int64_t cap = cols < kVcMax ? cols : kVcMax;
   if (cap > Vpad) cap = Vpad;
