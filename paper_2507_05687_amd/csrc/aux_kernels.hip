@@ -589,6 +589,46 @@ void launch_sum_splits(const float* part, int splits, int64_t stride, int64_t ld
                      out, ld_out, rows, cols, accumulate);
 }
 
+// dL/dh rows from the K-split partials of the one dL/dh product: for packed
+// row t < num_valid, the partials summed in split order, plus the sampled
+// id's term g_t W[y_t] in fp32, rounded once into row rows_p[t] of the
+// output. One workgroup per packed row, 4 columns per thread.
+__global__ void __launch_bounds__(256) k_dh_finish(const float* __restrict__ part, int splits,
+                                                   int64_t stride, int64_t ld,
+                                                   const WsHeader* __restrict__ hdr, int64_t H,
+                                                   const float* __restrict__ g_p,
+                                                   const int32_t* __restrict__ y_p,
+                                                   const uint16_t* __restrict__ W,
+                                                   const int32_t* __restrict__ rows_p, void* out,
+                                                   int out_bf16) {
+  const int64_t t = blockIdx.x;
+  if (t >= hdr->num_valid) return;
+  const float g = g_p[t];
+  const uint16_t* wr = W + (int64_t)y_p[t] * H;
+  const int64_t orow = (int64_t)rows_p[t] * H;
+  for (int64_t c = 4 * (int64_t)threadIdx.x; c < H; c += 4 * 256) {
+    const float* p = part + t * ld + c;
+    float v[4] = {p[0], p[1], p[2], p[3]};
+    for (int sp = 1; sp < splits; ++sp)
+      for (int k = 0; k < 4; ++k) v[k] += p[sp * stride + k];
+    for (int k = 0; k < 4; ++k) v[k] += g * __uint_as_float((uint32_t)wr[c + k] << 16);
+    if (out_bf16) {
+      for (int k = 0; k < 4; ++k) ((uint16_t*)out)[orow + c + k] = bf16_bits(v[k]);
+    } else {
+      for (int k = 0; k < 4; ++k) ((float*)out)[orow + c + k] = v[k];
+    }
+  }
+}
+
+void launch_dh_finish(const float* part, int splits, int64_t stride, int64_t ld,
+                      const WsHeader* hdr, int64_t rows, int64_t H, const float* g_p,
+                      const int32_t* y_p, const uint16_t* W, const int32_t* rows_p, void* out,
+                      int out_bf16, hipStream_t s) {
+  if (rows <= 0) return;
+  hipLaunchKernelGGL(k_dh_finish, dim3((unsigned)rows), dim3(256), 0, s, part, splits, stride, ld,
+                     hdr, H, g_p, y_p, W, rows_p, out, out_bf16);
+}
+
 void launch_adamw(const AdamArgs& a, hipStream_t s) {
   const int64_t n4 = a.n >> 2;
   int64_t blocks = ceil_div(n4 > 0 ? n4 : 1, 256);

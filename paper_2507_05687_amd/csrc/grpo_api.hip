@@ -20,13 +20,13 @@ namespace {
 enum Kind {
   K_PACK, K_ADV, K_GEMM_LSE, K_LSE_FIN, K_TOKEN, K_GEMM_DZ, K_GEMM_DH, K_GEMM_DW,
   K_F32_SCORE, K_F32_DH, K_F32_DW, K_ZERO_ROWS, K_GATHER_DOT, K_TILE, K_ADAMW,
-  K_RULE_REWARD, K_SUM_SPLITS, K_ONEHOT, K_NUM_KINDS
+  K_RULE_REWARD, K_SUM_SPLITS, K_ONEHOT, K_DH_FINISH, K_NUM_KINDS
 };
 const char* kKindNames[K_NUM_KINDS] = {
     "pack_valid",  "group_advantages", "gemm_logits_lse", "lse_finalize",   "token_objective",
     "gemm_recompute_dz", "gemm_grad_hidden", "gemm_grad_weight", "f32_score",
     "f32_grad_hidden", "f32_grad_weight", "zero_masked_rows", "gather_dot", "tile", "adamw",
-    "rule_reward", "sum_splits", "onehot_grad_weight"};
+    "rule_reward", "sum_splits", "onehot_grad_weight", "dh_finish"};
 
 struct Prof {
   std::mutex mu;
@@ -147,12 +147,13 @@ constexpr int64_t kVcMax = 8192;                        // columns per vocabular
 struct Layout {
   int64_t Npad = 0, Vpad = 0, tiles_v = 0, Vc = 0, nchunks = 0, dh_group = 0;
   int dw_splits_max = 1;  // the most K splits of a dL/dW product (its partials' room)
+  int dh_splits = 1;      // K splits of the dL/dh product when there is only one
   int64_t R = 0;  // rows of the token-indexed tiled buffers: the valid-row capacity, padded
   size_t hdr = 0, rows = 0, seq = 0, y = 0, pidx = 0, counts = 0, base = 0;
   size_t lse = 0, zy = 0, logp = 0, g = 0, ms = 0, lpart = 0;
   int64_t Hk = 0;  // H rounded up to the tiled block width
   // tiled buffers and their tile-row strides in blocks
-  size_t WK = 0, hK = 0, dz = 0, dhacc = 0, dwpart = 0;
+  size_t WK = 0, hK = 0, dz = 0, dhacc = 0, dwpart = 0, dhpart = 0;
   size_t okeys[2] = {0, 0}, ovals[2] = {0, 0}, ocounts = 0;  // sort of the sampled ids
   int64_t sK = 0, sChunk = 0;
   size_t total = 0;
@@ -168,7 +169,7 @@ int64_t tile_stride(int64_t K) { return ceil_div(K, kBK) + 1; }
 // splits only for at least 2% more fill (each adds a pass over fp32
 // partials). 512 tiles stay whole; 336 (a 5376-row chunk at H = 4096) take 3.
 constexpr int kMaxSplits = 8;
-int dw_splits(int64_t tiles) {
+int fill_splits(int64_t tiles) {
   if (tiles <= 0) return 1;
   int best = 1;
   double best_fill = 0;
@@ -204,7 +205,7 @@ double chunking_cost(int64_t R, int64_t Vpad, int64_t Hpad, int64_t Vc, int64_t 
     const int64_t cols = c == 0 ? Vc : Vpad - (n - 1) * Vc;
     const int64_t cnt = c == 0 ? n - 1 : 1;
     const int64_t tiles = cols / kTile * (Hpad / kTile);
-    const int sp = dw_splits(tiles);
+    const int sp = fill_splits(tiles);
     double tc = (double)ceil_div(sp * tiles, 256) / sp * t_round + 3 * kLaunch;
     if (sp > 1) tc += 2.0 * sp * (double)cols * Hpad * 4 / kBytes;
     t += cnt * tc;
@@ -230,7 +231,7 @@ void chunking(int64_t R, int64_t Vpad, int64_t Hpad, size_t budget, int64_t& Vc,
   double best = 0;
   for (int64_t c = cap; c >= kTile; c -= kTile) {
     const int64_t n = ceil_div(Vpad, c);
-    int64_t gr = cols / c;
+    int64_t gr = cols >= Vpad ? n : cols / c;  // the whole vocabulary: one group
     if (gr > n) gr = n;
     const double cost = chunking_cost(R, Vpad, Hpad, c, gr);
     if (c == cap || cost < best * 0.999) {
@@ -276,16 +277,24 @@ Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_
     if (op == GRPO_OP_LOSS_FWD_BWD) {
       const int64_t Hpad = round_up(H, kTile);
       chunking(L.R, L.Vpad, Hpad, dz_budget, L.Vc, L.nchunks, L.dh_group);
-      L.sChunk = tile_stride(L.dh_group * L.Vc);
+      // the group buffer: dh_group chunks, or the padded vocabulary when one
+      // group holds every chunk (the last one narrower)
+      L.sChunk = tile_stride(L.dh_group == L.nchunks ? L.Vpad : L.dh_group * L.Vc);
       L.dz = take(c, 2 * L.R * L.sChunk * kBK);
       // fp32 dh accumulator with every row and column of every tile present
       if (L.nchunks > L.dh_group) L.dhacc = take(c, 4 * L.R * Hpad);
       // dW partials of a split K (chunks too narrow to fill the GPU)
       const int64_t last = L.Vpad - (L.nchunks - 1) * L.Vc;
-      const int sp_full = dw_splits(L.Vc / kTile * (Hpad / kTile));
-      const int sp_last = dw_splits(last / kTile * (Hpad / kTile));
+      const int sp_full = fill_splits(L.Vc / kTile * (Hpad / kTile));
+      const int sp_last = fill_splits(last / kTile * (Hpad / kTile));
       L.dw_splits_max = sp_full > sp_last ? sp_full : sp_last;
       if (L.dw_splits_max > 1) L.dwpart = take(c, 4 * L.dw_splits_max * L.Vc * Hpad);
+      // a single dL/dh product over few row tiles: a split K fills the GPU
+      // (fp32 partials, summed with the sampled id's term by k_dh_finish)
+      if (L.dh_group == L.nchunks) {
+        L.dh_splits = fill_splits(L.R / kTile * (Hpad / kTile));
+        if (L.dh_splits > 1) L.dhpart = take(c, 4 * (size_t)L.dh_splits * L.R * Hpad);
+      }
       // the stable sort of the packed ids for the sampled-id term of dL/dW
       for (int b = 0; b < 2; ++b) {
         L.okeys[b] = take(c, 4 * L.R);
@@ -487,7 +496,7 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
       sa.out_rows = nullptr;
       sa.m_limit = Mc;
       sa.n_limit = H;
-      const int splits = L.dwpart ? dw_splits((int64_t)gw.tiles_m * gw.tiles_n) : 1;
+      const int splits = L.dwpart ? fill_splits((int64_t)gw.tiles_m * gw.tiles_n) : 1;
       if (splits > 1) {
         // split K: fp32 partials per split (every row/column of every tile),
         // then their sum into dW in split order
@@ -518,6 +527,25 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
       GemmArgs gh = gemm_args(dz, kt_chunk, L.R, WK, kt_h, H, &hdr->num_valid, nullptr,
                               round_up(v0 + Mc - vg, kBK), nullptr);
       gh.b_kb0 = vg / kBK;
+      if (L.dh_splits > 1) {  // the one dL/dh product, K split: partials, then their sum
+        const int64_t Hpad = round_up(H, kTile);
+        float* part = at<float>(ws, L.dhpart);
+        gh.splits = L.dh_splits;
+        StoreArgs sp{};
+        sp.acc_buf = part;
+        sp.ld_acc = Hpad;
+        sp.split_stride = L.R * Hpad;
+        sp.out = nullptr;
+        sp.m_limit = L.R;
+        sp.n_limit = H;
+        TRY(timed(K_GEMM_DH, s, [&] { launch_gemm_store(gh, sp, false, s); }));
+        TRY(timed(K_DH_FINISH, s, [&] {
+          launch_dh_finish(part, L.dh_splits, L.R * Hpad, Hpad, hdr, L.R, H, g_p, y_p,
+                           (const uint16_t*)weight, rows_p, grad_hidden,
+                           grad_hidden_dt == GRPO_BF16, s);
+        }));
+        break;  // one product: this was the last chunk
+      }
       StoreArgs sa{};
       sa.acc_buf = dhacc;
       sa.ld_acc = round_up(H, kTile);

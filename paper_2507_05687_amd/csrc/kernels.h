@@ -141,6 +141,13 @@ struct AdamArgs {
   float inv_sqrt_bc2;  // 1 / sqrt(1 - beta2^t)
 };
 void launch_adamw(const AdamArgs& a, hipStream_t s);
+// dL/dh of packed row t < num_valid (rows of the grid: `rows`) into output row
+// rows_p[t]: the split partials part[s * stride + t * ld + c] summed in split
+// order, plus g_t W[y_t, c], rounded once (bf16 or fp32 output)
+void launch_dh_finish(const float* part, int splits, int64_t stride, int64_t ld,
+                      const WsHeader* hdr, int64_t rows, int64_t H, const float* g_p,
+                      const int32_t* y_p, const uint16_t* W, const int32_t* rows_p, void* out,
+                      int out_bf16, hipStream_t s);
 // out[r, c] (+)= the sum over s < splits of part[s * stride + r * ld_part + c], summed in
 // split order before it is added
 void launch_sum_splits(const float* part, int splits, int64_t stride, int64_t ld_part, float* out,

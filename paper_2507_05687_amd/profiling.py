@@ -74,7 +74,19 @@ PROFILED = {
         desc="8 prompts x G = 8 generated completions of up to 65,536 bytes, launch check on",
         note="the warm-up step is included"),
 }
+# the streaming kernels of the loss and scoring calls (HBM-bound; their
+# counter bytes are reported with GB/s against the HBM peak)
+STREAMING = {"tile_rows": "k_tile_rows", "lse_finalize": "k_lse_finalize",
+             "token_objective": "k_token_objective", "loss_final": "k_loss_final",
+             "pack_count": "k_pack_count", "pack_scan": "k_pack_scan",
+             "pack_scatter": "k_pack_scatter", "sum_splits": "k_sum_splits",
+             "sort_init": "k_sort_init", "radix_count": "k_radix_count",
+             "radix_scan": "k_radix_scan", "radix_scatter": "k_radix_scatter",
+             "onehot_dw": "k_onehot_dw", "zero_masked_rows": "k_zero_masked_rows",
+             "group_advantages": "k_group_advantages", "rows_out": "k_rows_out"}
+STREAMING_SOURCES = [os.path.join(CSRC, "aux_kernels.hip"), os.path.join(CSRC, "onehot.hip")]
 COPY_BYTES = 1 << 30
+PEAK_HBM = 8e12     # MI355X HBM3E, bytes/s
 PEAK_BF16 = 2.5e15  # MI355X dense bf16 MFMA, flop/s
 SIMDS = 256 * 4
 XCDS = 8
@@ -111,8 +123,9 @@ def source_sha(rel: str) -> str:
 
 
 def sources_sha(cfg: dict) -> dict:
-    """SHA-256 of the workload's kernel source and of the host launch code."""
-    return {rel.replace(os.sep, "/"): source_sha(rel) for rel in (cfg["source"], HOST_SOURCE)}
+    """SHA-256 of the workload's kernel sources and of the host launch code."""
+    rels = [cfg["source"], *(STREAMING_SOURCES if cfg["kinds"] is GEMM_KINDS else []), HOST_SOURCE]
+    return {rel.replace(os.sep, "/"): source_sha(rel) for rel in rels}
 
 
 def sha_lines(cfg: dict) -> list[str]:
@@ -180,6 +193,33 @@ def counters(wl: str, raw: str, out: str):
                                 "hbm_bytes_per_launch": fb + wb}
         lines.append(f"{kind:22s} {len(f[0]):8d} {fb / 1e9:10.3f} {wb / 1e9:10.3f} "
                      f"{(fb + wb) / 1e9:10.3f}")
+    if cfg["kinds"] is GEMM_KINDS:
+        # the streaming kernels: bytes per launch, and GB/s over their average
+        # duration in the trace run of the same workload (when it is in --raw)
+        lines += ["# streaming kernels: counter bytes per launch; GB/s = bytes / average "
+                  "duration in the kernel trace; frac = GB/s / 8000",
+                  f"{'kind':22s} {'launches':>8} {'fetch_MB':>10} {'write_MB':>10} "
+                  f"{'total_MB':>10} {'avg_us':>9} {'GB/s':>8} {'frac':>6}"]
+        rec["streaming"] = {}
+        for kind, sym in STREAMING.items():
+            f = [v for k, v in res["FETCH_SIZE"][0].items() if sym in k]
+            w = [v for k, v in res["WRITE_SIZE"][0].items() if sym in k]
+            if not f or not w:
+                continue
+            fv = [x for lst in f for x in lst]
+            wv = [x for lst in w for x in lst]
+            fb = sum(fv) / len(fv) * 1024 * f_scale
+            wb = sum(wv) / len(wv) * 1024 * w_scale
+            tms = _trace_avg_ms(raw, wl, sym)
+            gbs = (fb + wb) / (tms / 1e3) / 1e9 if tms else None
+            rec["streaming"][kind] = {"symbol": sym, "launches": len(fv),
+                                      "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+                                      "trace_avg_ms": tms, "gb_per_s": gbs,
+                                      "frac_of_hbm_peak": gbs * 1e9 / PEAK_HBM if gbs else None}
+            lines.append(f"{kind:22s} {len(fv):8d} {fb / 1e6:10.3f} {wb / 1e6:10.3f} "
+                         f"{(fb + wb) / 1e6:10.3f} {tms * 1e3 if tms else float('nan'):9.1f} "
+                         f"{gbs if gbs else float('nan'):8.0f} "
+                         f"{gbs * 1e9 / PEAK_HBM if gbs else float('nan'):6.3f}")
     json.dump(rec, open(os.path.join(out, f"traffic_{wl}.json"), "w"), indent=1)
     open(os.path.join(out, f"traffic_{wl}.txt"), "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
