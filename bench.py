@@ -373,8 +373,10 @@ def main():
     op_main = grpo.OP_SFT_FWD_BWD if sft else grpo.OP_LOSS_FWD_BWD
 
     def ws_need(budget):
-        return max(grpo.workspace_bytes(op_main, grpo.BF16, N, H, V, B, max_valid, budget),
-                   grpo.workspace_bytes(grpo.OP_LOGPROB_FWD, grpo.BF16, N, H, V, 1, max_valid))
+        fwd = grpo.workspace_bytes(grpo.OP_LOGPROB_FWD, grpo.BF16, N, H, V, 1, max_valid)
+        if args.workload == "fwd_bf16":  # scoring only
+            return fwd
+        return max(grpo.workspace_bytes(op_main, grpo.BF16, N, H, V, B, max_valid, budget), fwd)
     dz_budget = 48 << 30
     while dz_budget > (1 << 30) and ws_need(dz_budget) > args.scratch_gb * 1e9:
         dz_budget -= 1 << 30

@@ -35,8 +35,9 @@
  *    workspace must be ordered by the caller.
  *  - Workspace size. max_valid (0 = N) bounds the number of valid rows a
  *    call will see: the token-indexed scratch is sized for it (a ragged
- *    batch with half its rows masked needs about half). A call whose mask
- *    has more valid rows records GRPO_ERR_CAPACITY and treats no row as
+ *    batch with half its rows masked needs about half). The capacity is
+ *    max_valid rounded up to a multiple of 256; a call whose mask has more
+ *    valid rows than that records GRPO_ERR_CAPACITY and treats no row as
  *    valid (all outputs as for masked rows). dz_budget (0 = 16 GiB) bounds
  *    the bytes of the logits-gradient chunks of the backward pass; a smaller
  *    budget means narrower vocabulary chunks and more passes over the fp32
@@ -69,7 +70,7 @@ typedef enum grpo_status {
   GRPO_ERR_HIP = 8,         /* a HIP runtime call failed */
   GRPO_ERR_TOKEN_RANGE = 9, /* (device) a token id was outside [0, V) */
   GRPO_ERR_SEQLENS = 10,    /* (device) cu_seqlens not monotone from 0 to N */
-  GRPO_ERR_CAPACITY = 11    /* (device) more valid rows than max_valid */
+  GRPO_ERR_CAPACITY = 11    /* (device) more valid rows than the max_valid capacity */
 } grpo_status;
 
 /* GRPO_BF16 is the production path (MFMA contractions). GRPO_F32 is an

@@ -515,3 +515,49 @@ def test_adamw_parity(n, lr, wd):
             got = wb.view(torch.int16).cpu().numpy().view(np.uint16)
             assert np.array_equal(got, want)
 
+
+
+# ------------------------------------------------------------ workspace bounds
+# ragged rows, several vocabulary tiles, H over two gradient tile-columns
+BUDGET_CASE = dict(prompts=3, group=4, seq_len=50, hidden=320, vocab=40000, ragged=True,
+                   min_len=1, forced_equal_groups=1)
+
+
+def test_bf16_max_valid_and_small_budgets():
+    # The logits-gradient budget sets the vocabulary chunk width, how many
+    # chunks one dL/dh product takes (so the passes over the fp32 dL/dh
+    # accumulator) and the dL/dW K splits; max_valid sizes the token-indexed
+    # buffers. Each combination against the full oracle; the same arguments
+    # give the same bits.
+    kw = dict(BUDGET_CASE, dtype="bf16", rms_norm_hidden=True, beta=0.01, noise_sigma=0.1,
+              seed=31)
+    w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    nv = int(b["mask"].sum())
+    for max_valid in (0, nv):
+        rows = -(-(w.num_tokens if max_valid == 0 else nv) // 256) * 256
+        for cols in (256, 768, 2560, 8192):  # dz columns the budget holds
+            budget = 2 * rows * cols
+            out = _run_loss(w, W, h, b, adv, old, ref, max_valid=max_valid, dz_budget=budget)
+            _compare_loss(w, W, h, b, adv, old, ref, out, BF16_TOL, BF16_GRAD_TOL)
+    again = _run_loss(w, W, h, b, adv, old, ref, max_valid=nv, dz_budget=2 * rows * 768)
+    first = _run_loss(w, W, h, b, adv, old, ref, max_valid=nv, dz_budget=2 * rows * 768)
+    for k in ("loss", "logp", "grad_hidden", "grad_weight"):
+        assert torch.equal(again[k].view(torch.uint8), first[k].view(torch.uint8)), k
+
+
+def test_capacity_error_leaves_outputs_as_for_masked_rows():
+    kw = dict(BUDGET_CASE, dtype="bf16", rms_norm_hidden=True, beta=0.01, seed=32)
+    w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    nv = int(b["mask"].sum())
+    assert nv > 256  # a max_valid of 200 gives a capacity of 256 rows
+    with pytest.raises(grpo.GrpoError) as e:
+        _run_loss(w, W, h, b, adv, old, ref, max_valid=200)
+    assert e.value.status == 11
+    out = grpo.loss_fwd_bwd(to_dev(h, w.dtype), to_dev(W, w.dtype), dev(b["tokens"]),
+                            dev(b["mask"]), dev(b["cu_seqlens"]), dev(old), dev(ref), dev(adv),
+                            w.clip_eps, w.beta, 0, check=False, max_valid=200)
+    torch.cuda.synchronize()
+    for k in ("loss", "logp", "lse", "token_loss", "dlogp", "grad_hidden", "grad_weight"):
+        assert torch.count_nonzero(out[k]).item() == 0, k
+    # the next call on the same workspace starts clean
+    _run_loss(w, W, h, b, adv, old, ref, max_valid=nv)
