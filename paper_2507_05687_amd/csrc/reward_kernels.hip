@@ -17,8 +17,8 @@
 //   launch: the name, not preceded by an identifier byte, blanks, "[", a
 //     bracket-balanced run to the matching "]", blanks, "(".
 //
-// One 256-thread workgroup per completion. A completion that fits is first
-// copied into LDS, and its check costs a bounded amount of work per byte:
+// One 256-thread workgroup per completion. A completion that fits (96 KiB)
+// is first copied into LDS; its check costs a bounded amount of work per byte:
 //   1. every thread tests 16 bytes in 4 KiB for a decorator; the functions
 //      they decorate are followed up (by whole waves when there are few
 //      decorators, else by the thread that found each) and their names go
@@ -30,17 +30,23 @@
 //      (and blanks) whose match is followed by blanks and "(" (a launch
 //      site), and looks the identifier up in the table.
 // is_Triton is an "exists" over decorators and launch sites, so the order in
-// which threads find them does not change the result. A completion longer
-// than the LDS copy is checked from global memory by simpler code: one name
-// list, and a text scan per listed name.
+// which threads find them does not change the result. A longer completion
+// goes through the same passes reading the caller's text (never past
+// text_bytes), with its name table in the idle LDS copy and index chunks of
+// 32 bytes times ceil(length / 96 KiB), so a bracket match costs O(length /
+// 3072) reads. More distinct decorated names than that table takes (6,144)
+// are handled in rounds, each holding the names of one hash class; beyond 64
+// rounds (some 390,000 names) the check falls back to simpler code: a name
+// list and a text scan per name.
 #include "kernels.h"
 
 namespace grpo {
 namespace {
 
-// A completion: n bytes, in global memory (at t) or in the LDS copy (byte i
-// at base[i + sh], the copy 16-byte aligned and readable to a multiple of 16
-// bytes), where long scans read 16 bytes at a time.
+// A completion: n bytes, in global memory (at t), or at base[i + sh] for
+// byte i with base 16-byte aligned and cap bytes readable from it (the LDS
+// copy, cap = its size; or the caller's text, cap = what is left of it), where
+// long scans read 16 bytes at a time.
 struct GlobalText {
   static constexpr bool kLds = false;
   const uint8_t* t;
@@ -52,7 +58,17 @@ struct LdsText {
   const uint8_t* base;
   int64_t sh;
   int64_t n;
+  int64_t cap;
   __device__ __forceinline__ uint8_t operator[](int64_t i) const { return base[i + sh]; }
+  // the 16 bytes at base + a (a multiple of 16); bytes at or past cap read as 0
+  __device__ __forceinline__ u32x4 ld16(int64_t a) const {
+    if (a + 16 <= cap) return *(const u32x4*)(base + a);
+    u32x4 w = {0u, 0u, 0u, 0u};
+    static_for<16>([&](auto k) {
+      if (a + k.value < cap) w[k.value >> 2] |= (uint32_t)base[a + k.value] << (8 * (k.value & 3));
+    });
+    return w;
+  }
 };
 
 __device__ __forceinline__ bool is_blank(uint8_t c) { return c == ' ' || c == '\t' || c == '\r'; }
@@ -84,7 +100,7 @@ __device__ __forceinline__ int64_t line_end(const T& X, int64_t i) {
     for (; i < X.n && ((i + X.sh) & 15) != 0; ++i)
       if (X[i] == '\n') return i;
     for (; i + 16 <= X.n; i += 16) {
-      const u32x4 w = *(const u32x4*)(X.base + i + X.sh);
+      const u32x4 w = X.ld16(i + X.sh);
       if (count_eq(w, '\n') != 0) break;
     }
   }
@@ -101,7 +117,7 @@ __device__ __forceinline__ int64_t match_close(const T& X, int64_t i, uint8_t o,
   while (i < X.n) {
     if constexpr (T::kLds) {
       if (((i + X.sh) & 15) == 0 && i + 16 <= X.n && depth > 0) {
-        const u32x4 w = *(const u32x4*)(X.base + i + X.sh);
+        const u32x4 w = X.ld16(i + X.sh);
         const int closes = count_eq(w, c);
         if (depth > closes) {
           depth += count_eq(w, o) - closes;
@@ -217,10 +233,14 @@ constexpr int kRrBlocks = kRrChunks / kRrBlock;
 constexpr int kRrTable = 8192;
 constexpr uint32_t kRrEmpty = 0xffffffffu;
 static_assert(kRrLds / 18 * 3 / 2 < kRrTable && kRrLds < (1 << 17), "name table sizing");
+constexpr int kRrTable64Max = kRrTable * 3 / 4;  // names a Table64 takes
+static_assert(kRrTable * 8 <= kRrLds, "a Table64 lives in the idle LDS copy");
 
 struct RrShared {
   int count;  // decorated functions found (may exceed kRrNames)
   int found;
+  int overflow;  // a Table64 would take more than kRrTable64Max names
+  int ntab;      // names a Table64 holds
   int nlist;  // entries of `list` found (may exceed kRrList)
   int64_t ns[kRrNames];
   int64_t nl[kRrNames];
@@ -330,7 +350,7 @@ __device__ int64_t wave_find(const LdsText& X, int64_t i, uint8_t v1, uint8_t v2
     const int64_t cs = c0 + 16 * lane;
     uint32_t hit = 0;
     if (cs < X.n && cs + 16 > i) {
-      const u32x4 w = *(const u32x4*)(X.base + cs + X.sh);
+      const u32x4 w = X.ld16(cs + X.sh);
       hit = (mask16(w, v1) | mask16(w, v2)) & range16(cs, i, X.n);
     }
     const uint64_t any = __ballot(hit != 0);
@@ -355,7 +375,7 @@ __device__ int64_t wave_match_close(const LdsText& X, int64_t i, uint8_t o, uint
     int net = 0, low = 1 << 30;
     uint32_t mo = 0, mc = 0, valid = 0;
     if (cs < X.n && cs + 16 > i) {
-      const u32x4 w = *(const u32x4*)(X.base + cs + X.sh);
+      const u32x4 w = X.ld16(cs + X.sh);
       valid = range16(cs, i, X.n);
       mo = mask16(w, o) & valid;
       mc = mask16(w, c) & valid;
@@ -442,7 +462,7 @@ __device__ bool wave_decorated_name(const LdsText& X, int64_t p, int64_t& ns, in
 __device__ __forceinline__ u32x4 lds_chunk(const LdsText& X, int64_t i, int64_t& c0) {
   const int64_t a = (i + X.sh) & ~(int64_t)15;
   c0 = a - X.sh;
-  return *(const u32x4*)(X.base + a);
+  return X.ld16(a);
 }
 __device__ __forceinline__ uint8_t chunk_byte(const u32x4& w, int k) {
   return (uint8_t)(w[k >> 2] >> (8 * (k & 3)));
@@ -507,69 +527,115 @@ __device__ bool same_ident(const LdsText& X, int64_t a, int64_t b) {
   }
 }
 
-// A slot holds the position of a name's first byte (17 bits) and 15 more
-// bits of its hash; kRrEmpty is free. Insertion keeps one slot per distinct
-// name.
-__device__ void name_insert(const LdsText& X, int64_t ns, int64_t nl, uint32_t* table) {
-  const uint32_t h = ident_hash(X, ns, ns + nl);
-  const uint32_t v = (uint32_t)ns | ((h >> 13) << 17);
-  for (uint32_t slot = h & (kRrTable - 1);; slot = (slot + 1) & (kRrTable - 1)) {
-    const uint32_t old = atomicCAS(&table[slot], kRrEmpty, v);
-    if (old == kRrEmpty) return;
-    if ((old >> 17) == (v >> 17) && same_ident(X, old & 0x1ffff, ns)) return;
+// Hash tables of the decorated names, one slot per distinct name. Table32
+// (the LDS copy): a slot holds the position of the name's first byte (17
+// bits) and 15 more bits of its hash; it has room for every name such a
+// completion can hold. Table64 (longer completions): the position and the
+// whole hash; it takes at most kRrTable64Max names and reports an overflow
+// beyond that. kRrEmpty / ~0 mark free slots.
+struct Table32 {
+  uint32_t* s;
+  __device__ void clear() const {
+    for (int i = threadIdx.x; i < kRrTable; i += kRrThreads) s[i] = kRrEmpty;
   }
-}
-__device__ bool name_lookup(const LdsText& X, int64_t s, int64_t e, const uint32_t* table) {
-  const uint32_t h = ident_hash(X, s, e);
-  for (uint32_t slot = h & (kRrTable - 1);; slot = (slot + 1) & (kRrTable - 1)) {
-    const uint32_t v = table[slot];
-    if (v == kRrEmpty) return false;
-    if ((v >> 17) == ((h >> 13) & 0x7fff) && same_ident(X, v & 0x1ffff, s)) return true;
+  __device__ bool insert(const LdsText& X, int64_t ns, uint32_t h, int*) const {
+    const uint32_t v = (uint32_t)ns | ((h >> 13) << 17);
+    for (uint32_t slot = h & (kRrTable - 1);; slot = (slot + 1) & (kRrTable - 1)) {
+      const uint32_t old = atomicCAS(&s[slot], kRrEmpty, v);
+      if (old == kRrEmpty) return true;
+      if ((old >> 17) == (v >> 17) && same_ident(X, old & 0x1ffff, ns)) return true;
+    }
   }
-}
+  __device__ bool find(const LdsText& X, int64_t st, uint32_t h) const {
+    for (uint32_t slot = h & (kRrTable - 1);; slot = (slot + 1) & (kRrTable - 1)) {
+      const uint32_t v = s[slot];
+      if (v == kRrEmpty) return false;
+      if ((v >> 17) == ((h >> 13) & 0x7fff) && same_ident(X, v & 0x1ffff, st)) return true;
+    }
+  }
+};
+struct Table64 {
+  unsigned long long* s;
+  __device__ void clear() const {
+    for (int i = threadIdx.x; i < kRrTable; i += kRrThreads) s[i] = ~0ull;
+  }
+  // count: distinct names taken so far (shared); false once it would pass the limit
+  __device__ bool insert(const LdsText& X, int64_t ns, uint32_t h, int* count) const {
+    const unsigned long long v = ((unsigned long long)ns << 32) | h;
+    for (uint32_t slot = h & (kRrTable - 1);; slot = (slot + 1) & (kRrTable - 1)) {
+      const unsigned long long old = s[slot];
+      if (old != ~0ull) {
+        if ((uint32_t)old == h && same_ident(X, (int64_t)(old >> 32), ns)) return true;
+        continue;
+      }
+      if (atomicAdd(count, 1) >= kRrTable64Max) return false;
+      const unsigned long long got = atomicCAS(&s[slot], ~0ull, v);
+      if (got == ~0ull) return true;
+      atomicSub(count, 1);  // lost the slot to another name: look at it again
+      slot = (slot - 1) & (kRrTable - 1);
+    }
+  }
+  __device__ bool find(const LdsText& X, int64_t st, uint32_t h) const {
+    for (uint32_t slot = h & (kRrTable - 1);; slot = (slot + 1) & (kRrTable - 1)) {
+      const unsigned long long v = s[slot];
+      if (v == ~0ull) return false;
+      if ((uint32_t)v == h && same_ident(X, (int64_t)(v >> 32), st)) return true;
+    }
+  }
+};
 
-// The bracket index covers the LDS copy in 32-byte chunks aligned to the
-// copy (chunk c holds text bytes 32c - sh .. 32c - sh + 31; bytes outside the
-// text count as neither bracket).
+// The bracket index covers the text in chunks of C = 32 csub bytes aligned
+// to base (chunk c holds text bytes C c - sh .. C c - sh + C - 1; bytes
+// outside the text count as neither bracket). csub is 1 for the LDS copy and
+// grows with a longer completion so that the index keeps kRrChunks entries.
 struct BracketIndex {
   int32_t* cst;  // depth ("[" minus "]") before each chunk
   int32_t* cmn;  // lowest depth after any text byte of each chunk (2^30 if none)
-  int32_t* bmn;  // lowest of cmn over each block of 32 chunks
-  int nch, nbl;
+  int32_t* bmn;  // lowest of cmn over each block of kRrBlock chunks
+  int nch, nbl, csub;
 };
 
 __device__ __forceinline__ int bracket_step(uint8_t b) { return (b == '[') - (b == ']'); }
 
-// net depth change and lowest relative depth of chunk c
-__device__ __forceinline__ void chunk_stats(const LdsText& X, int c, int& net, int& lo) {
-  const u32x4 w0 = *(const u32x4*)(X.base + c * kRrChunk);
-  const u32x4 w1 = *(const u32x4*)(X.base + c * kRrChunk + 16);
-  const int64_t t0 = (int64_t)c * kRrChunk - X.sh;  // text index of the chunk's first byte
-  int d = 0, l = 1 << 30;
-  static_for<kRrChunk>([&](auto k) {
-    const u32x4& w = k.value < 16 ? w0 : w1;
-    const uint8_t b = chunk_byte(w, k.value & 15);
-    if (t0 + k.value >= 0 && t0 + k.value < X.n) {
-      d += bracket_step(b);
-      l = d < l ? d : l;
+// Over the text bytes j of the 32-byte part at base + 32 u with from <= j < to,
+// from depth d: the index just past the first byte after which the depth
+// equals k, else -1 (d is then the depth after the last byte taken); lo
+// tracks the lowest depth reached. The part is read into registers once.
+__device__ __forceinline__ int64_t part_scan(const LdsText& X, int64_t u, int64_t from, int64_t to,
+                                             int& d, int k, int& lo) {
+  const u32x4 w0 = X.ld16(32 * u);
+  const u32x4 w1 = X.ld16(32 * u + 16);
+  const int64_t t0 = 32 * u - X.sh;
+  if (from < 0) from = 0;
+  if (to > X.n) to = X.n;
+  int64_t hit = -1;
+  static_for<32>([&](auto q) {
+    const int64_t j = t0 + q.value;
+    if (hit < 0 && j >= from && j < to) {
+      d += bracket_step(chunk_byte(q.value < 16 ? w0 : w1, q.value & 15));
+      lo = d < lo ? d : lo;
+      if (d == k) hit = j + 1;
     }
   });
-  net = d;
-  lo = l;
+  return hit;
 }
 
 // Builds the index (all threads; ends with a barrier). Lane l of a row of 256
-// takes chunk 256 row + l (consecutive chunks, free of bank conflicts); depths
-// are carried from row to row. wtot: 4 ints of LDS.
+// takes chunk 256 row + l (consecutive chunks, free of bank conflicts in the
+// LDS copy); depths are carried from row to row. wtot: 4 ints of LDS.
 __device__ void build_bracket_index(const LdsText& X, BracketIndex& bi, int32_t* wtot) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  bi.nch = (int)((X.n + X.sh + kRrChunk - 1) / kRrChunk);
+  const int64_t parts = (X.n + X.sh + 31) / 32;
+  bi.csub = (int)((parts + kRrChunks - 1) / kRrChunks);
+  bi.nch = (int)((parts + bi.csub - 1) / bi.csub);
   bi.nbl = (bi.nch + kRrBlock - 1) / kRrBlock;
   int carry = 0;  // depth before this row
   for (int row = 0; row * kRrThreads < bi.nch; ++row) {
     const int c = row * kRrThreads + tid;
     int net = 0, lo = 1 << 30;
-    if (c < bi.nch) chunk_stats(X, c, net, lo);
+    if (c < bi.nch)
+      for (int p = 0; p < bi.csub; ++p)
+        part_scan(X, (int64_t)c * bi.csub + p, 0, X.n, net, -(1 << 30), lo);
     int incl = net;  // inclusive scan within the wave
     static_for<6>([&](auto sft) {
       const int t = __shfl_up(incl, 1 << sft.value, 64);
@@ -598,26 +664,15 @@ __device__ void build_bracket_index(const LdsText& X, BracketIndex& bi, int32_t*
   __syncthreads();
 }
 
-// Over the text bytes j of chunk c with from <= j < to, from depth d: the
-// index just past the first byte after which the depth equals k, else -1
-// (d is then the depth after the last byte taken). The chunk is read into
-// registers once.
-__device__ __forceinline__ int64_t chunk_find_depth(const LdsText& X, int c, int64_t from,
-                                                    int64_t to, int& d, int k) {
-  const u32x4 w0 = *(const u32x4*)(X.base + c * kRrChunk);
-  const u32x4 w1 = *(const u32x4*)(X.base + c * kRrChunk + 16);
-  const int64_t t0 = (int64_t)c * kRrChunk - X.sh;
-  if (from < 0) from = 0;
-  if (to > X.n) to = X.n;
-  int64_t hit = -1;
-  static_for<kRrChunk>([&](auto q) {
-    const int64_t j = t0 + q.value;
-    if (hit < 0 && j >= from && j < to) {
-      d += bracket_step(chunk_byte(q.value < 16 ? w0 : w1, q.value & 15));
-      if (d == k) hit = j + 1;
-    }
-  });
-  return hit;
+// Over the text bytes j of chunk c with from <= j < to: as part_scan
+__device__ __forceinline__ int64_t chunk_find_depth(const LdsText& X, const BracketIndex& bi, int c,
+                                                    int64_t from, int64_t to, int& d, int k) {
+  int lo = 1 << 30;
+  for (int p = 0; p < bi.csub; ++p) {
+    const int64_t r = part_scan(X, (int64_t)c * bi.csub + p, from, to, d, k, lo);
+    if (r >= 0) return r;
+  }
+  return -1;
 }
 
 // X[s] == '[': index just past its matching ']', or -1 (match_close's
@@ -625,11 +680,12 @@ __device__ __forceinline__ int64_t chunk_find_depth(const LdsText& X, int c, int
 // its value before s: found in s's chunk, else in the first later chunk of
 // s's block, else of the first later block, whose lowest depth reaches it.
 __device__ int64_t bracket_match(const LdsText& X, int64_t s, const BracketIndex& bi) {
-  const int c = (int)((s + X.sh) / kRrChunk);
+  const int64_t C = 32 * (int64_t)bi.csub;
+  const int c = (int)((s + X.sh) / C);
   int d = bi.cst[c];
-  chunk_find_depth(X, c, 0, s, d, -(1 << 30));  // the depth before s
+  chunk_find_depth(X, bi, c, 0, s, d, -(1 << 30));  // the depth before s
   const int k = d++;  // the target depth; d is now the depth after s
-  const int64_t r = chunk_find_depth(X, c, s + 1, X.n, d, k);
+  const int64_t r = chunk_find_depth(X, bi, c, s + 1, X.n, d, k);
   if (r >= 0) return r;
   const int be = (c / kRrBlock + 1) * kRrBlock < bi.nch ? (c / kRrBlock + 1) * kRrBlock : bi.nch;
   int cc = c + 1;
@@ -642,85 +698,116 @@ __device__ int64_t bracket_match(const LdsText& X, int64_t s, const BracketIndex
     while (bi.cmn[cc] > k) ++cc;  // some chunk of block b reaches k
   }
   d = bi.cst[cc];
-  return chunk_find_depth(X, cc, 0, X.n, d, k);  // found: cmn[cc] <= k
+  return chunk_find_depth(X, bi, cc, 0, X.n, d, k);  // found: cmn[cc] <= k
 }
 
-struct RrTables {
-  uint32_t* names;  // kRrTable slots
-  BracketIndex bi;
-  int32_t* wtot;    // 4 ints
-};
+// is_Triton of a completion through the three bounded passes, the same in
+// every thread: 1 or 0, or -1 when the names do not fit the table. If the
+// decorated names overflow a Table64, the passes over names are repeated with
+// the names split by hash: round j of k holds the names whose hash is j mod k
+// and looks up only launch sites whose identifier hashes the same way (k is
+// the decorated-function count over 4096, doubled while a round still
+// overflows, at most kRrMaxRounds).
+constexpr int kRrMaxRounds = 64;
 
-// is_Triton of an LDS completion, the same in every thread.
-__device__ bool is_triton_lds(const LdsText& X, int require_launch, RrShared& sh, RrTables& tb) {
+template <class Table>
+__device__ int is_triton_indexed(const LdsText& X, int require_launch, RrShared& sh,
+                                 const Table& names, BracketIndex bi, int32_t* wtot) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   constexpr int kWaves = kRrThreads / 64;
-  for (int i = tid; i < kRrTable; i += kRrThreads) tb.names[i] = kRrEmpty;
-  // 1. decorators; with at most kRrList of them the waves follow each up
-  // (long scans shared by the wave), else the thread that found it does
-  const int64_t nq = (X.n + X.sh + 15) / 16;  // 16-byte chunks of the copy
-  for (int64_t q = tid; q < nq; q += kRrThreads) {
-    const int64_t t0 = 16 * q - X.sh;  // text index of the chunk's first byte
-    uint32_t m = mask16(*(const u32x4*)(X.base + 16 * q), '@') & range16(t0, 0, X.n);
-    for (; m != 0; m &= m - 1) {
-      const int64_t p = t0 + __builtin_ctz(m);
-      if (decorator_at(X, p)) {
-        const int slot = atomicAdd(&sh.nlist, 1);
-        if (slot < kRrList) sh.list[slot] = p;
+  const int64_t nq = (X.n + X.sh + 15) / 16;  // 16-byte chunks from base
+  bool indexed = false;
+  for (int rounds = 1; rounds <= kRrMaxRounds;) {
+    bool overflow = false;
+    for (int j = 0; j < rounds && !overflow; ++j) {
+      __syncthreads();  // the previous round is done with the table and the list
+      if (tid == 0) {
+        sh.count = 0;
+        sh.nlist = 0;
+        sh.overflow = 0;
+        sh.ntab = 0;
       }
-    }
-  }
-  __syncthreads();
-  const int ndeco = sh.nlist;
-  if (ndeco <= kRrList) {
-    for (int d = wave; d < ndeco; d += kWaves) {
-      int64_t ns = 0, nl = 0;
-      if (wave_decorated_name(X, sh.list[d], ns, nl) && lane == 0) {
+      names.clear();
+      __syncthreads();
+      auto add = [&](int64_t ns, int64_t nl) {  // a decorated function's name
         atomicAdd(&sh.count, 1);
-        name_insert(X, ns, nl, tb.names);
-      }
-    }
-  } else {
-    for (int64_t q = tid; q < nq; q += kRrThreads) {
-      const int64_t t0 = 16 * q - X.sh;
-      uint32_t m = mask16(*(const u32x4*)(X.base + 16 * q), '@') & range16(t0, 0, X.n);
-      for (; m != 0; m &= m - 1) {
-        const int64_t p = t0 + __builtin_ctz(m);
-        int64_t ns = 0, nl = 0;
-        if (decorator_at(X, p) && decorated_name(X, p, ns, nl)) {
-          atomicAdd(&sh.count, 1);
-          name_insert(X, ns, nl, tb.names);
+        const uint32_t h = ident_hash(X, ns, ns + nl);
+        if ((int)(h % (uint32_t)rounds) == j && !names.insert(X, ns, h, &sh.ntab)) sh.overflow = 1;
+      };
+      // 1. decorators; with at most kRrList of them the waves follow each up
+      // (long scans shared by the wave), else the thread that found it does
+      for (int64_t q = tid; q < nq; q += kRrThreads) {
+        const int64_t t0 = 16 * q - X.sh;  // text index of the chunk's first byte
+        uint32_t m = mask16(X.ld16(16 * q), '@') & range16(t0, 0, X.n);
+        for (; m != 0; m &= m - 1) {
+          const int64_t p = t0 + __builtin_ctz(m);
+          if (decorator_at(X, p)) {
+            const int slot = atomicAdd(&sh.nlist, 1);
+            if (slot < kRrList) sh.list[slot] = p;
+          }
         }
       }
-    }
-  }
-  __syncthreads();
-  if (!require_launch || sh.count == 0) return sh.count > 0;
-  // 2. the bracket index
-  build_bracket_index(X, tb.bi, tb.wtot);
-  // 3. launch sites and their names: each thread takes 16-byte chunks of the
-  // copy; every "[" whose preceding non-blank byte ends an identifier is
-  // matched through the index
-  for (int64_t q0 = 0; q0 < nq; q0 += kRrThreads) {
-    const int64_t q = q0 + tid;
-    bool hit = false;
-    if (q < nq) {
-      const int64_t t0 = 16 * q - X.sh;  // text index of the chunk's first byte
-      uint32_t m = mask16(*(const u32x4*)(X.base + 16 * q), '[') & range16(t0, 0, X.n);
-      while (m != 0 && !hit) {
-        const int64_t s = t0 + __builtin_ctz(m);
-        m &= m - 1;
-        const int64_t r = lds_back_skip_blanks(X, s - 1);
-        if (r < 0 || !is_ident(X[r])) continue;
-        int64_t e = bracket_match(X, s, tb.bi);
-        if (e < 0) continue;
-        e = lds_skip_blanks(X, e);
-        if (e < X.n && X[e] == '(') hit = name_lookup(X, lds_ident_start(X, r), r + 1, tb.names);
+      __syncthreads();
+      const int ndeco = sh.nlist;
+      if (ndeco <= kRrList) {
+        for (int d = wave; d < ndeco; d += kWaves) {
+          int64_t ns = 0, nl = 0;
+          if (wave_decorated_name(X, sh.list[d], ns, nl) && lane == 0) add(ns, nl);
+        }
+      } else {
+        for (int64_t q = tid; q < nq; q += kRrThreads) {
+          const int64_t t0 = 16 * q - X.sh;
+          uint32_t m = mask16(X.ld16(16 * q), '@') & range16(t0, 0, X.n);
+          for (; m != 0; m &= m - 1) {
+            const int64_t p = t0 + __builtin_ctz(m);
+            int64_t ns = 0, nl = 0;
+            if (decorator_at(X, p) && decorated_name(X, p, ns, nl)) add(ns, nl);
+          }
+        }
+      }
+      __syncthreads();
+      if (!require_launch || sh.count == 0) return sh.count > 0;
+      if (sh.overflow) {
+        overflow = true;
+        break;
+      }
+      // 2. the bracket index (once)
+      if (!indexed) {
+        build_bracket_index(X, bi, wtot);
+        indexed = true;
+      }
+      // 3. launch sites and their names: each thread takes 16-byte chunks;
+      // every "[" whose preceding non-blank byte ends an identifier is
+      // matched through the index
+      for (int64_t q0 = 0; q0 < nq; q0 += kRrThreads) {
+        const int64_t q = q0 + tid;
+        bool hit = false;
+        if (q < nq) {
+          const int64_t t0 = 16 * q - X.sh;  // text index of the chunk's first byte
+          uint32_t m = mask16(X.ld16(16 * q), '[') & range16(t0, 0, X.n);
+          while (m != 0 && !hit) {
+            const int64_t s = t0 + __builtin_ctz(m);
+            m &= m - 1;
+            const int64_t r = lds_back_skip_blanks(X, s - 1);
+            if (r < 0 || !is_ident(X[r])) continue;
+            int64_t e = bracket_match(X, s, bi);
+            if (e < 0) continue;
+            e = lds_skip_blanks(X, e);
+            if (e < X.n && X[e] == '(') {
+              const int64_t st = lds_ident_start(X, r);
+              const uint32_t h = ident_hash(X, st, r + 1);
+              hit = (int)(h % (uint32_t)rounds) == j && names.find(X, st, h);
+            }
+          }
+        }
+        if (__syncthreads_or(hit)) return 1;
       }
     }
-    if (__syncthreads_or(hit)) return true;
+    if (!overflow) return 0;
+    const int need = (sh.count + 4095) / 4096;
+    rounds = need > 2 * rounds ? need : 2 * rounds;
   }
-  return false;
+  return -1;
 }
 
 __global__ void __launch_bounds__(kRrThreads) k_rule_reward(RewardArgs a) {
@@ -738,6 +825,8 @@ __global__ void __launch_bounds__(kRrThreads) k_rule_reward(RewardArgs a) {
     sh.count = 0;
     sh.found = 0;
     sh.nlist = 0;
+    sh.overflow = 0;
+    sh.ntab = 0;
   }
   bool found;
   // 16-byte aligned (text is), at most 15 bytes before s0
@@ -751,11 +840,31 @@ __global__ void __launch_bounds__(kRrThreads) k_rule_reward(RewardArgs a) {
     for (int64_t g = (mid > start ? mid : start) + tid; g < s1; g += kRrThreads)
       lds[g - start] = a.text[g];
     __syncthreads();
-    RrTables tb{names, BracketIndex{cst, cmn, bmn, 0, 0}, wtot};
-    found = is_triton_lds(LdsText{lds, s0 - start, n}, a.require_launch, sh, tb);
+    found = is_triton_indexed(LdsText{lds, s0 - start, n, kRrLds}, a.require_launch, sh,
+                              Table32{names}, BracketIndex{cst, cmn, bmn, 0, 0, 1}, wtot) > 0;
   } else {
+    // longer than the copy: the same passes over the caller's text (read up
+    // to text_bytes only), the name table in the idle copy; a completion
+    // with more distinct names than that table takes falls back to the
+    // simpler scan
     __syncthreads();
-    found = is_triton_block(GlobalText{a.text + s0, n}, a.require_launch, sh);
+    int r = -1;
+    if (n < (1ll << 31))
+      r = is_triton_indexed(LdsText{a.text + start, s0 - start, n, a.text_bytes - start},
+                            a.require_launch, sh, Table64{(unsigned long long*)lds},
+                            BracketIndex{cst, cmn, bmn, 0, 0, 1}, wtot);
+    if (r >= 0) {
+      found = r > 0;
+    } else {
+      __syncthreads();
+      if (tid == 0) {
+        sh.count = 0;
+        sh.found = 0;
+        sh.nlist = 0;
+      }
+      __syncthreads();
+      found = is_triton_block(GlobalText{a.text + s0, n}, a.require_launch, sh);
+    }
   }
   if (tid == 0) {
     const bool passed = a.test_passed[b] != 0;

@@ -249,3 +249,49 @@ def test_bracket_soup():
         head = b"@triton.jit\ndef k(x):pass\n@triton.jit\ndef j(y):pass\n"
         texts.append(head + body if i % 2 else body + b"\n" + head)
     _check(texts, np.ones(len(texts), np.uint8))
+
+
+# ---- completions longer than the LDS copy (96 KiB): the same bounded passes
+# over the caller's text, with a coarser bracket index
+
+def test_long_generated_completions():
+    # generated sources of 100-400 KB, the last one ending the text (its
+    # length not a multiple of 16), against the oracle
+    texts, passed = workloads.make_completions(16, seed=5, mean_len=250_000, max_len=400_000)
+    keep = [i for i, t in enumerate(texts) if len(t) > 96 * 1024]
+    texts = [texts[i] + b"x" * (131 if i % 3 == 0 else 0) for i in keep]
+    passed = passed[keep]
+    assert len(texts) >= 8 and len(b"".join(texts)) % 16 != 0
+    _check(texts, passed)
+
+
+def test_long_adversarial_completions():
+    # 9,000 distinct decorated names (270 KB): more than the long path's name
+    # table takes, so the names are taken in rounds by hash class (8,000 too);
+    # 128,000 unclosed k[ (256 KB)
+    texts = [_distinct_names(8000), _distinct_names(8000, b"n7999[(1,)](0)\n"),
+             _distinct_names(9000, b"n8999[(1,)](0)\n"), _distinct_names(9000),
+             _distinct_names(8000, b"n8000[(1,)](0)\n")]
+    _check(texts, np.ones(len(texts), np.uint8))
+    big = [_unclosed(128000)] * 15 + [_unclosed(128000, b"](0)")]
+    f, ms = _timed_flags(big, require_launch=True)
+    print(f"16 completions x 128,000 unclosed k[ (256 KB): {ms:.2f} ms")
+    assert not f[:15].any() and f[15] == 1
+    assert ms < 100.0
+    f, ms = _timed_flags([_distinct_names(8000)] * 16, require_launch=True)
+    print(f"16 completions x 8,000 distinct names (240 KB), no launch: {ms:.2f} ms")
+    assert not f.any()
+    assert ms < 100.0
+
+
+def test_long_bracket_soup():
+    # a 200 KB soup of launch-like tokens around decorated k and j: parity at
+    # the coarser index granularity (one index chunk spans several 32-byte parts)
+    rng = np.random.default_rng(12)
+    alphabet = [b"k", b"j", b"q", b"[", b"]", b"(", b")", b" ", b"\n", b"[", b"]", b"x"]
+    head = b"@triton.jit\ndef k(x):pass\n@triton.jit\ndef j(y):pass\n"
+    texts = []
+    for i in range(4):
+        body = b"".join(alphabet[c] for c in rng.integers(0, len(alphabet), 200_000 + 977 * i))
+        texts.append(head + body if i % 2 else body + b"\n" + head)
+    _check(texts, np.ones(len(texts), np.uint8))
