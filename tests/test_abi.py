@@ -263,3 +263,10 @@ def test_static_pack_limits_without_a_device(lib):
     assert f(NULL, P, 101, 100, P, P, P, NULL, NULL) == 2
     # more rollouts than the static scratch holds
     assert f(NULL, P, (1 << 20) + 1, 1 << 21, P, P, P, NULL, NULL) == 6
+
+
+def test_binding_fails_loudly_without_the_library(monkeypatch):
+    # no fallback: a missing libgrpo.so is an error, not a silent CPU path
+    monkeypatch.setattr(grpo, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        grpo.load("/nonexistent/libgrpo.so")
