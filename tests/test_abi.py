@@ -267,6 +267,8 @@ def test_static_pack_limits_without_a_device(lib):
 
 def test_binding_fails_loudly_without_the_library(monkeypatch):
     # no fallback: a missing libgrpo.so is an error, not a silent CPU path
+    from paper_2507_05687_amd import grpo
+
     monkeypatch.setattr(grpo, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         grpo.load("/nonexistent/libgrpo.so")
