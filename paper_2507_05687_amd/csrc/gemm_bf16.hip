@@ -62,7 +62,10 @@ __device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, char* lds, 
 // loads' LDS destinations and would wait for every load in flight before each
 // of them. Here the compiler sees no load at all, so the kernel itself waits
 // (vmcnt) before LDS that a load writes is read or reused. M0 is set in the
-// same statement; no other code of these kernels uses it.
+// same statement; no other code of these kernels uses it. The resource and
+// the scalar offset must be values the compiler holds in scalar registers
+// (wave-uniform); where it does not, the assembler rejects the instruction,
+// so such a change fails the build rather than the run.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void load_lds16_asm(__amdgpu_buffer_rsrc_t r, uint32_t lds,
