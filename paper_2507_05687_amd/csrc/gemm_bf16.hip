@@ -173,9 +173,10 @@ struct EpiLse {
   static constexpr bool kKPositive = true;  // K = H >= 32
   const int32_t* y_p;  // sampled id of each packed token
   float* zy;           // z at the sampled id, per packed token
-  float2* ms;          // [tiles_m][ldms] partial (max, sum-exp) per tile and token
+  float2* ms;          // [tiles of V][ldms] partial (max, sum-exp) per tile and token
   int64_t ldms;
   int64_t V;
+  int64_t v0;          // first vocabulary row of this launch (a multiple of 256)
 
   // the sampled id of each column of this lane, loaded before the main loop so
   // that the loop hides its latency (the per-token arrays hold a value for
@@ -234,13 +235,14 @@ struct EpiLse {
 
   __device__ __forceinline__ void operator()(Acc& acc, const Frag& f, int, int n_valid,
                                              char* smem, const Pre& pre) const {
-    const int vbase = f.tm * kTile + f.row(0, 0);
+    const int64_t tile_v = v0 / kTile + f.tm;  // this tile's index over the vocabulary
+    const int64_t vbase = tile_v * kTile + f.row(0, 0);
     const int vlim = (int)(V - vbase);  // row offset o of this lane is valid iff o < vlim
-    const bool full = (int64_t)f.tm * kTile + f.wm * 128 + 128 <= V;  // wave-uniform
+    const bool full = tile_v * kTile + f.wm * 128 + 128 <= V;  // wave-uniform
     float pm[8], ps[8];
     static_for<8>([&](auto j) {
       const int64_t t = (int64_t)f.tn * kTile + f.col(j);
-      const int y = t < n_valid ? pre.y[j] - vbase : -1;  // y as a row offset of this lane
+      const int y = t < n_valid ? (int)(pre.y[j] - vbase) : -1;  // y as a row offset of this lane
       if (full)
         column<true>(acc, j, pm[j], ps[j], vlim, y, zy + t);
       else
@@ -260,7 +262,7 @@ struct EpiLse {
         const int64_t t = (int64_t)f.tn * kTile + f.col(j);
         const float2 u = xchg[j * 16 + f.lane];
         merge2(pm[j], ps[j], u.x, u.y);
-        if (t < n_valid) ms[(int64_t)f.tm * ldms + t] = make_float2(pm[j], ps[j]);
+        if (t < n_valid) ms[tile_v * ldms + t] = make_float2(pm[j], ps[j]);
       });
     }
   }
@@ -701,9 +703,9 @@ __global__ void __launch_bounds__(256, 1) k_gemm(GemmArgs g, Epi epi) {
 }
 
 void launch_gemm_lse(const GemmArgs& g, const int32_t* y_p, float* zy, float2* ms, int64_t ldms,
-                     int64_t V, hipStream_t s) {
+                     int64_t V, int64_t v0, hipStream_t s) {
   hipLaunchKernelGGL((k_gemm<EpiLse, false, false>), dim3(gemm_grid(g.tiles_m, g.tiles_n)),
-                     dim3(256), 0, s, g, EpiLse{y_p, zy, ms, ldms, V});
+                     dim3(256), 0, s, g, EpiLse{y_p, zy, ms, ldms, V, v0});
 }
 
 void launch_gemm_dz(const GemmArgs& g, const float* lse_p, const float* g_p, uint16_t* dz,

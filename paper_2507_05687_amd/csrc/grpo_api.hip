@@ -143,6 +143,7 @@ constexpr int64_t kPackSeg = 4096;  // rows per packing workgroup without cu_seq
 constexpr int64_t kMaxAdvPrompts = 4 * ((1ll << 24) - 1);  // group_advantages' grid limit
 constexpr size_t kDefaultDzBudget = (size_t)16 << 30;  // bytes for the bf16 dz chunks
 constexpr int64_t kVcMax = 8192;                        // columns per vocabulary chunk
+constexpr int64_t kScoreRows = 8192;  // vocabulary rows per scoring launch (a multiple of 256)
 
 struct Layout {
   int64_t Npad = 0, Vpad = 0, tiles_v = 0, Vc = 0, nchunks = 0, dh_group = 0;
@@ -424,9 +425,13 @@ grpo_status run_scoring(const Layout& L, void* ws, grpo_dtype dt, const void* hi
     });
   }
   float2* ms = at<float2>(ws, L.ms);
-  GemmArgs g = gemm_args(at<uint16_t>(ws, L.WK), L.sK, V, at<uint16_t>(ws, L.hK), L.sK, L.R,
-                         nullptr, &hdr->num_valid, L.Hk, nullptr);
-  TRY(timed(K_GEMM_LSE, s, [&] { launch_gemm_lse(g, y_p, zy, ms, L.R, V, s); }));
+  const uint16_t* WK = at<uint16_t>(ws, L.WK);
+  for (int64_t v0 = 0; v0 < V; v0 += kScoreRows) {
+    const int64_t Mc = V - v0 < kScoreRows ? V - v0 : kScoreRows;
+    GemmArgs g = gemm_args(WK + (v0 / kTile) * L.sK * kTileElems, L.sK, Mc, at<uint16_t>(ws, L.hK),
+                           L.sK, L.R, nullptr, &hdr->num_valid, L.Hk, nullptr);
+    TRY(timed(K_GEMM_LSE, s, [&] { launch_gemm_lse(g, y_p, zy, ms, L.R, V, v0, s); }));
+  }
   return timed(K_LSE_FIN, s, [&] {
     launch_lse_finalize(ms, L.R, (int)L.tiles_v, zy, hdr, lse_p, logp_p, L.R, s);
   });

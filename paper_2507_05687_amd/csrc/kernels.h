@@ -48,8 +48,10 @@ struct StoreArgs {
 };
 
 int gemm_grid(int tiles_m, int tiles_n);
+// scoring of the vocabulary rows [v0, v0 + g.M) (A = those rows of W); the
+// partials of vocabulary tile i go to row i of ms
 void launch_gemm_lse(const GemmArgs& g, const int32_t* y_p, float* zy, float2* ms, int64_t ldms,
-                     int64_t V, hipStream_t s);
+                     int64_t V, int64_t v0, hipStream_t s);
 // dz = -g * exp(z - lse) for a vocabulary chunk starting at row v0 (the
 // sampled id's +g is left to the gradient products' callers)
 void launch_gemm_dz(const GemmArgs& g, const float* lse_p, const float* g_p, uint16_t* dz,
