@@ -82,15 +82,38 @@ __device__ __forceinline__ void load_lds16_asm(__amdgpu_buffer_rsrc_t r, uint32_
 // padding workgroups of the last band. With fewer than 8 kGM tile-rows there
 // are not enough rows for a band per XCD (column_tile_of).
 __device__ inline bool tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
-  int xcd = bid & 7, loc = bid >> 3;
-  int per_band = kGM * tiles_n;
-  int band = loc / per_band;
-  int r = loc - band * per_band;
-  int nb = r / (kGM * kGN);
-  int r2 = r - nb * (kGM * kGN);
-  tm = band * (8 * kGM) + xcd * kGM + r2 % kGM;
-  tn = nb * kGN + r2 / kGM;
-  return tm < tiles_m;
+  const int xcd = bid & 7, loc = bid >> 3;
+  const int per_band = kGM * tiles_n;
+  const int full = tiles_m / (8 * kGM);  // whole groups of 8 bands
+  const int band = loc / per_band;
+  if (band < full) {
+    const int r = loc - band * per_band;
+    const int nb = r / (kGM * kGN);
+    const int r2 = r - nb * (kGM * kGN);
+    tm = band * (8 * kGM) + xcd * kGM + r2 % kGM;
+    tn = nb * kGN + r2 / kGM;
+    return true;
+  }
+  // The rem tile-rows after them are shared out so that the XCDs get equal
+  // work: from 8 rows on, each XCD takes rem/8 or rem/8 + 1 consecutive rows
+  // and walks them kGN columns at a time; below 8, each XCD takes an eighth
+  // of the columns over all rem rows.
+  const int rem = tiles_m - full * (8 * kGM);
+  const int l = loc - full * per_band;
+  if (rem == 0) return false;
+  if (rem >= 8) {
+    const int q = rem >> 3, e = rem & 7;
+    const int cnt = q + (xcd < e ? 1 : 0);
+    const int nb = l / (cnt * kGN), r2 = l - nb * (cnt * kGN);
+    tm = full * (8 * kGM) + xcd * q + min(xcd, e) + r2 % cnt;
+    tn = nb * kGN + r2 / cnt;
+    return tn < tiles_n;
+  }
+  const int cols = (tiles_n + 7) >> 3;
+  if (l >= rem * cols) return false;
+  tm = full * (8 * kGM) + l % rem;
+  tn = xcd * cols + l / rem;
+  return tn < tiles_n;
 }
 
 // Few tile-rows: each XCD takes an eighth of the tile-columns that hold valid
@@ -144,7 +167,15 @@ __device__ inline bool gemm_tile(const GemmArgs& g, int m_valid, int n_valid, in
 int gemm_grid(int tiles_m, int tiles_n) {
   if (split_bands(tiles_m)) return 8 * kGM * (int)round_up(split_band_cols(tiles_m, tiles_n), kGN);
   if (tiles_m < 8 * kGM) return 8 * tiles_m * (int)ceil_div(tiles_n, 8);
-  return (int)ceil_div(tiles_m, 8 * kGM) * 8 * kGM * tiles_n;
+  // workgroups per XCD: the whole groups of bands, then the rows tile_of
+  // shares out after them
+  const int full = tiles_m / (8 * kGM), rem = tiles_m % (8 * kGM);
+  int tail = 0;
+  if (rem >= 8)
+    tail = ((rem + 7) / 8) * kGN * (int)ceil_div(tiles_n, kGN);
+  else if (rem > 0)
+    tail = rem * (int)ceil_div(tiles_n, 8);
+  return 8 * (full * kGM * tiles_n + tail);
 }
 
 // ------------------------------------------------------------ layout

@@ -192,6 +192,11 @@ SMALL = {
     "split_rounds": dict(prompts=2, group=4, seq_len=40, hidden=4096, vocab=5376),
     # a wide hidden state: 2048 K steps per scoring tile, 256 gradient tile-columns
     "wide_hidden": dict(prompts=2, group=4, seq_len=32, hidden=65536, vocab=300),
+    # dL/dh over 45 token tile-rows: 32 in whole XCD bands, the other 13 shared
+    # out as 2 rows to each of 5 XCDs and 1 to each of 3
+    "uneven_row_bands": dict(prompts=3, group=4, seq_len=960, hidden=512, vocab=700),
+    # 37 token tile-rows: the 5 after the whole bands split by columns over the XCDs
+    "few_rows_after_bands": dict(prompts=1, group=8, seq_len=1184, hidden=512, vocab=700),
 }
 
 
