@@ -371,12 +371,17 @@ def main():
     # whole GiB (at most the library default of 48) that keeps it within --scratch-gb
     max_valid = n_valid if use_mask is not None else N
     op_main = grpo.OP_SFT_FWD_BWD if sft else grpo.OP_LOSS_FWD_BWD
+    # Double scoring: the reference model is frozen, so its W is tiled once
+    # (here, before the timed steps); the policy's W is tiled once per step and
+    # read tiled by both calls that use it (its scoring and the loss).
+    flag = grpo.WS_TILED_WEIGHT if w.double_scoring else 0
 
     def ws_need(budget):
-        fwd = grpo.workspace_bytes(grpo.OP_LOGPROB_FWD, grpo.BF16, N, H, V, 1, max_valid)
+        fwd = grpo.workspace_bytes(grpo.OP_LOGPROB_FWD | flag, grpo.BF16, N, H, V, 1, max_valid)
         if args.workload == "fwd_bf16":  # scoring only
             return fwd
-        return max(grpo.workspace_bytes(op_main, grpo.BF16, N, H, V, B, max_valid, budget), fwd)
+        return max(grpo.workspace_bytes(op_main | flag, grpo.BF16, N, H, V, B, max_valid, budget),
+                   fwd)
     dz_budget = 48 << 30
     while dz_budget > (1 << 30) and ws_need(dz_budget) > args.scratch_gb * 1e9:
         dz_budget -= 1 << 30
@@ -388,10 +393,15 @@ def main():
     P = grpo._ptr
     stream = grpo._stream()
     mptr = P(use_mask)
+    if w.double_scoring:
+        Wref_t = grpo.tile_weight(Wref).buf
+        W_t = grpo.tile_weight(W).buf  # rewritten in every step
+    else:
+        Wref_t = W_t = None
 
     def step():
         if sft:  # the supervised stage: cross-entropy over the response tokens
-            st = lib.sft_ce_fwd_bwd(grpo.BF16, P(h), P(W), P(tokens), mptr, N, H, V, P(loss),
+            st = lib.sft_ce_fwd_bwd(grpo.BF16, P(h), P(W), None, P(tokens), mptr, N, H, V, P(loss),
                                     None, P(gh), grpo.BF16, P(gw), 0, P(ws), ws.numel(),
                                     max_valid, dz_budget, stream)
             assert st == 0, st
@@ -399,23 +409,26 @@ def main():
         st = lib.group_advantages(P(rewards), w.prompts, w.group, 1e-6, 1, P(adv), stream)
         assert st == 0, st
         if args.workload == "fwd_bf16":
-            st = lib.grpo_logprob_fwd(grpo.BF16, P(h), P(W), P(tokens), mptr, N, H, V,
+            st = lib.grpo_logprob_fwd(grpo.BF16, P(h), P(W), None, P(tokens), mptr, N, H, V,
                                       P(old_buf), P(lse_buf), P(ws), ws.numel(), max_valid,
                                       stream)
             assert st == 0, st
             return
         lse_in, o, r = None, old, ref
         if w.double_scoring:  # S8: score under the policy (old) and the reference
-            st = lib.grpo_logprob_fwd(grpo.BF16, P(h), P(W), P(tokens), mptr, N, H, V,
+            st = lib.grpo_tile_weight(P(W), V, H, P(W_t), W_t.numel(), stream)
+            assert st == 0, st
+            st = lib.grpo_logprob_fwd(grpo.BF16, P(h), P(W), P(W_t), P(tokens), mptr, N, H, V,
                                       P(old_buf), P(lse_buf), P(ws), ws.numel(), max_valid,
                                       stream)
             assert st == 0, st
-            st = lib.grpo_logprob_fwd(grpo.BF16, P(h), P(Wref), P(tokens), mptr, N, H, V,
-                                      P(ref_buf), None, P(ws), ws.numel(), max_valid, stream)
+            st = lib.grpo_logprob_fwd(grpo.BF16, P(h), P(Wref), P(Wref_t), P(tokens), mptr, N, H,
+                                      V, P(ref_buf), None, P(ws), ws.numel(), max_valid, stream)
             assert st == 0, st
             lse_in, o, r = lse_buf, old_buf, ref_buf
-        st = lib.grpo_loss_fwd_bwd(grpo.BF16, P(h), P(W), P(tokens), mptr, P(cu), B, N, H, V,
-                                   P(o), P(r), P(adv), w.clip_eps, w.beta, 0, P(lse_in), P(loss),
+        st = lib.grpo_loss_fwd_bwd(grpo.BF16, P(h), P(W), P(W_t), P(tokens), mptr, P(cu), B, N,
+                                   H, V, P(o), P(r), P(adv), w.clip_eps, w.beta, 0, P(lse_in),
+                                   P(loss),
                                    None, None, None, None, None, P(gh), grpo.BF16, P(gw), 0,
                                    P(ws), ws.numel(), max_valid, dz_budget, stream)
         assert st == 0, st

@@ -100,6 +100,10 @@ typedef enum grpo_op {
   GRPO_OP_SFT_FWD_BWD = 2
 } grpo_op;
 
+/* OR-ed into the op of grpo_workspace_bytes for a bf16 call that will be
+ * given weight_tiled: the workspace then holds no tiled copy of the weight. */
+#define GRPO_WS_TILED_WEIGHT 0x100
+
 /*
  * group_advantages -- Eq. 2 of AutoTriton Sec. 3.3: the advantage of
  * rollout i of a prompt is (r_i - mean) / (std + std_eps), where mean and
@@ -169,19 +173,24 @@ grpo_status grpo_pack_valid_static(const uint8_t* mask, const int64_t* cu_seqlen
  *   dt        GRPO_BF16 (hidden, weight bf16; MFMA, fp32 accumulation) or
  *             GRPO_F32 (fp32 throughout).
  *   hidden    [N, H] dt. Device.       weight [V, H] dt. Device.
+ *   weight_tiled  NULL, or grpo_tile_weight's output for this weight (bf16
+ *             only): the call reads it instead of tiling weight into the
+ *             workspace (see grpo_tile_weight). Device, 256-byte aligned.
  *   tokens    [N] int64 sampled ids.   mask   [N] uint8 or NULL.
  *   logp, lse [N] fp32 outputs (0 on masked rows). Either may be NULL.
  *   workspace >= grpo_workspace_bytes(GRPO_OP_LOGPROB_FWD, dt, N, H, V, 1,
- *             max_valid, 0), 256-byte aligned.
+ *             max_valid, 0) (with GRPO_WS_TILED_WEIGHT in the op when
+ *             weight_tiled is given), 256-byte aligned.
  *   max_valid 0 (= N) or the most valid rows the mask will have, <= N.
  * Requires N, H, V >= 1, N < 2^31, V < 2^31, H < 2^20; bf16 also needs
  * H % 8 == 0, (ceil(V/256) + 32) * ceil(N/256) < 2^31 and 16-byte aligned
  * hidden/weight; fp32 needs H <= 8192. fp32 arrays are 4-byte aligned.
  */
 grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weight,
-                             const int64_t* tokens, const uint8_t* mask, int64_t N, int64_t H,
-                             int64_t V, float* logp, float* lse, void* workspace,
-                             size_t workspace_bytes, int64_t max_valid, hipStream_t stream);
+                             const void* weight_tiled, const int64_t* tokens,
+                             const uint8_t* mask, int64_t N, int64_t H, int64_t V, float* logp,
+                             float* lse, void* workspace, size_t workspace_bytes,
+                             int64_t max_valid, hipStream_t stream);
 
 /*
  * grpo_loss_fwd_bwd -- loss = -J of Eq. 1 (AutoTriton Sec. 3.3) and its
@@ -200,7 +209,9 @@ grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weig
  * dL/dweight_{y_t} as a fixed-order sum of g_t * hidden_t), so the gradients'
  * error is that of the bf16 rounding of the small -g p terms.
  *
- *   dt, hidden, weight, tokens, mask, N, H, V   as grpo_logprob_fwd.
+ *   dt, hidden, weight, weight_tiled, tokens, mask, N, H, V
+ *              as grpo_logprob_fwd (weight is read as well: the sampled
+ *              ids' rows).
  *   cu_seqlens [num_seqs + 1] int64. Device.
  *   old_logp   [N] fp32: log pi_theta_old of each row. Device.
  *   ref_logp   [N] fp32: log pi_ref of each row; may be NULL iff beta == 0.
@@ -218,14 +229,16 @@ grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weig
  *   grad_weight [V, H] fp32: overwritten, or added to when
  *               accumulate_grad_weight != 0.
  * workspace >= grpo_workspace_bytes(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, num_seqs,
- * max_valid, dz_budget) (see the workspace-size convention above).
+ * max_valid, dz_budget) (see the workspace-size convention above; with
+ * GRPO_WS_TILED_WEIGHT in the op when weight_tiled is given).
  * Sizes as grpo_logprob_fwd, and for bf16 N <= 2^22 (4,194,304 rows per call;
  * larger batches are split by the caller, accumulating grad_weight).
  */
 grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight,
-                              const int64_t* tokens, const uint8_t* mask,
-                              const int64_t* cu_seqlens, int64_t num_seqs, int64_t N, int64_t H,
-                              int64_t V, const float* old_logp, const float* ref_logp,
+                              const void* weight_tiled, const int64_t* tokens,
+                              const uint8_t* mask, const int64_t* cu_seqlens,
+                              int64_t num_seqs, int64_t N, int64_t H, int64_t V,
+                              const float* old_logp, const float* ref_logp,
                               const float* adv, float clip_eps, float beta, grpo_agg agg,
                               const float* lse_in, float* loss, float* logp_out, float* lse_out,
                               float* token_loss, float* dlogp, uint8_t* clip_flag,
@@ -244,21 +257,22 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
  * the caller shifts labels). dL/dlogp_t = -1 / n_valid, and dL/dhidden,
  * dL/dweight follow through the log-softmax exactly as in grpo_loss_fwd_bwd.
  *
- *   dt, hidden, weight, tokens, mask, N, H, V   as grpo_logprob_fwd (mask
- *               marks the supervised rows, e.g. the response tokens).
+ *   dt, hidden, weight, weight_tiled, tokens, mask, N, H, V
+ *               as grpo_loss_fwd_bwd (mask marks the supervised rows, e.g.
+ *               the response tokens).
  *   loss        [1] fp32 output, fixed-order reduction. Device.
  *   logp_out    [N] fp32 or NULL (0 on masked rows). Device.
  *   grad_hidden, grad_hidden_dt, grad_weight, accumulate_grad_weight
  *               as grpo_loss_fwd_bwd (either gradient may be NULL).
  * workspace >= grpo_workspace_bytes(GRPO_OP_SFT_FWD_BWD, dt, N, H, V, 1, max_valid,
- * dz_budget).
+ * dz_budget) (GRPO_WS_TILED_WEIGHT in the op when weight_tiled is given).
  * Sizes and errors as grpo_loss_fwd_bwd (a token id outside [0, V) sets the flag that
  * grpo_check_error reports).
  */
 grpo_status sft_ce_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight,
-                           const int64_t* tokens, const uint8_t* mask, int64_t N, int64_t H,
-                           int64_t V, float* loss, float* logp_out, void* grad_hidden,
-                           grpo_dtype grad_hidden_dt, float* grad_weight,
+                           const void* weight_tiled, const int64_t* tokens, const uint8_t* mask,
+                           int64_t N, int64_t H, int64_t V, float* loss, float* logp_out,
+                           void* grad_hidden, grpo_dtype grad_hidden_dt, float* grad_weight,
                            int32_t accumulate_grad_weight, void* workspace,
                            size_t workspace_bytes, int64_t max_valid, size_t dz_budget,
                            hipStream_t stream);
@@ -324,9 +338,32 @@ grpo_status triton_rule_reward(const uint8_t* text, int64_t text_bytes, const in
 /* Bytes of workspace an operation needs for these sizes (0 if the sizes are
  * invalid). For GRPO_OP_LOGPROB_FWD and GRPO_OP_SFT_FWD_BWD pass
  * num_seqs = 1; max_valid and dz_budget as described under "Workspace size"
- * (dz_budget is ignored for GRPO_OP_LOGPROB_FWD). Host only. */
+ * (dz_budget is ignored for GRPO_OP_LOGPROB_FWD). op may carry
+ * GRPO_WS_TILED_WEIGHT (bf16 only). Host only. */
 size_t grpo_workspace_bytes(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V,
                             int64_t num_seqs, int64_t max_valid, size_t dz_budget);
+
+/*
+ * grpo_tile_weight -- the LM head W [V, H] (bf16, row-major) in the tiled
+ * layout that the bf16 scoring and gradient products of Eq. 1 read: 256-row
+ * by 32-column blocks (16 KiB each), tile-row r's blocks at
+ * (r * (ceil(H/32) + 1) + k) * 8192 elements, rows >= V and columns >= H zero.
+ * grpo_logprob_fwd, grpo_loss_fwd_bwd and sft_ce_fwd_bwd tile W themselves
+ * unless given this copy as weight_tiled, so a caller whose W stays fixed over
+ * several calls (a frozen reference model, the policy over the micro-batches
+ * of one optimiser step) tiles it once: 2 * V * H bytes read and written
+ * (0.55 ms at V = 155136, H = 4096). The copy is only valid while W is
+ * unchanged; the library cannot tell when it is stale.
+ *   weight   [V, H] bf16, 16-byte aligned. Device.
+ *   out      grpo_weight_tiled_bytes(V, H) bytes, 256-byte aligned. Device,
+ *            caller-owned.
+ * Requires 1 <= V < 2^31 - 256, 1 <= H < 2^20, H % 8 == 0. Errors:
+ * GRPO_ERR_NULL, GRPO_ERR_SHAPE (also out_bytes too small), GRPO_ERR_ALIGN.
+ * Enqueued on `stream`.
+ */
+size_t grpo_weight_tiled_bytes(int64_t V, int64_t H);
+grpo_status grpo_tile_weight(const void* weight, int64_t V, int64_t H, void* out,
+                             size_t out_bytes, hipStream_t stream);
 
 /* Synchronises `stream`, then reads and clears the device error flags kept in
  * the workspace by the most recent call that used it. Returns GRPO_OK,

@@ -155,6 +155,7 @@ struct Layout {
   int64_t Hk = 0;  // H rounded up to the tiled block width
   // tiled buffers and their tile-row strides in blocks
   size_t WK = 0, hK = 0, dz = 0, dhacc = 0, dwpart = 0, dhpart = 0;
+  const uint16_t* WKx = nullptr;  // the caller's tiled weight (no WK in the workspace)
   size_t okeys[2] = {0, 0}, ovals[2] = {0, 0}, ocounts = 0;  // sort of the sampled ids
   int64_t sK = 0, sChunk = 0;
   size_t total = 0;
@@ -247,7 +248,7 @@ void chunking(int64_t R, int64_t Vpad, int64_t Hpad, size_t budget, int64_t& Vc,
 // max_valid: the most valid rows a call will have (0: all N); dz_budget: bytes
 // for the logits-gradient chunks (0: the default).
 Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_t B,
-              int64_t max_valid, size_t dz_budget) {
+              int64_t max_valid, size_t dz_budget, bool tiled_weight = false) {
   Layout L;
   L.Npad = round_up(N, kTile);
   L.Vpad = round_up(V, kTile);
@@ -273,7 +274,7 @@ Layout layout(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V, int64_
     // tiled copies of W and of the valid hidden rows (K = H contiguous blocks)
     L.Hk = round_up(H, kBK);
     L.sK = tile_stride(H);
-    L.WK = take(c, 2 * L.Vpad * L.sK * kBK);
+    if (!tiled_weight) L.WK = take(c, 2 * L.Vpad * L.sK * kBK);
     L.hK = take(c, 2 * L.R * L.sK * kBK);
     if (op == GRPO_OP_LOSS_FWD_BWD) {
       const int64_t Hpad = round_up(H, kTile);
@@ -313,6 +314,11 @@ T* at(void* ws, size_t off) {
   return (T*)((char*)ws + off);
 }
 
+// The tiled weight the products read: the caller's, else the workspace copy.
+const uint16_t* weight_k(const Layout& L, void* ws) {
+  return L.WKx ? L.WKx : at<uint16_t>(ws, L.WK);
+}
+
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 grpo_status check_sizes(grpo_dtype dt, int64_t N, int64_t H, int64_t V) {
@@ -333,6 +339,13 @@ constexpr int64_t kMaxBwdTokens = 1ll << 22;
 grpo_status check_bwd_sizes(grpo_dtype dt, int64_t N, int64_t H, int64_t V) {
   TRY(check_sizes(dt, N, H, V));
   return dt == GRPO_BF16 && N > kMaxBwdTokens ? GRPO_ERR_SHAPE : GRPO_OK;
+}
+
+// weight_tiled: bf16 only, 256-byte aligned (the layout of grpo_tile_weight)
+grpo_status check_weight_tiled(grpo_dtype dt, const void* weight_tiled) {
+  if (!weight_tiled) return GRPO_OK;
+  if (dt != GRPO_BF16) return GRPO_ERR_DTYPE;
+  return aligned(weight_tiled, kAlign) ? GRPO_OK : GRPO_ERR_ALIGN;
 }
 
 grpo_status check_ws(void* ws, size_t bytes, const Layout& L) {
@@ -393,16 +406,19 @@ grpo_status run_pack(const Layout& L, void* ws, const uint8_t* mask, const int64
   return timed(K_PACK, s, [&] { launch_pack(a, s); });
 }
 
-// Tiled copies of W (all V rows) and of the valid hidden rows in packed
-// order, the operands of the scoring and dz products.
+// Tiled copies of W (all V rows; not when the caller gave a tiled W) and of
+// the valid hidden rows in packed order, the operands of the scoring and dz
+// products.
 grpo_status run_tiles(const Layout& L, void* ws, const void* hidden, const void* weight,
                       int64_t H, int64_t V, hipStream_t s) {
   const int32_t* rows_p = at<int32_t>(ws, L.rows);
   const WsHeader* hdr = at<WsHeader>(ws, L.hdr);
-  TRY(timed(K_TILE, s, [&] {
-    launch_tile_rows((const uint16_t*)weight, H, nullptr, V, nullptr, L.Vpad, H, L.sK,
-                     at<uint16_t>(ws, L.WK), s);
-  }));
+  if (!L.WKx) {
+    TRY(timed(K_TILE, s, [&] {
+      launch_tile_rows((const uint16_t*)weight, H, nullptr, V, nullptr, L.Vpad, H, L.sK,
+                       at<uint16_t>(ws, L.WK), s);
+    }));
+  }
   return timed(K_TILE, s, [&] {
     launch_tile_rows((const uint16_t*)hidden, H, rows_p, 0, hdr, L.R, H, L.sK,
                      at<uint16_t>(ws, L.hK), s);
@@ -425,7 +441,10 @@ grpo_status run_scoring(const Layout& L, void* ws, grpo_dtype dt, const void* hi
     });
   }
   float2* ms = at<float2>(ws, L.ms);
-  const uint16_t* WK = at<uint16_t>(ws, L.WK);
+  // One launch per kScoreRows vocabulary rows: the tiles of a launch start in
+  // step, while over one launch of the whole vocabulary the tiles that share
+  // operand slices drift apart in K and miss in L2 (7% slower at N = 131072).
+  const uint16_t* WK = weight_k(L, ws);
   for (int64_t v0 = 0; v0 < V; v0 += kScoreRows) {
     const int64_t Mc = V - v0 < kScoreRows ? V - v0 : kScoreRows;
     GemmArgs g = gemm_args(WK + (v0 / kTile) * L.sK * kTileElems, L.sK, Mc, at<uint16_t>(ws, L.hK),
@@ -469,7 +488,7 @@ grpo_status run_backward(const Layout& L, void* ws, grpo_dtype dt, const void* h
   }
 
   uint16_t* dz = at<uint16_t>(ws, L.dz);
-  uint16_t* WK = at<uint16_t>(ws, L.WK);
+  const uint16_t* WK = weight_k(L, ws);
   uint16_t* hK = at<uint16_t>(ws, L.hK);
   float* dhacc = L.nchunks > L.dh_group ? at<float>(ws, L.dhacc) : nullptr;
   // The tiled operands: W [V x H] and the valid hidden rows [R x H] (the
@@ -621,16 +640,37 @@ const char* grpo_status_string(grpo_status st) {
   return "unknown status";
 }
 
-size_t grpo_workspace_bytes(grpo_op op, grpo_dtype dt, int64_t N, int64_t H, int64_t V,
+size_t grpo_workspace_bytes(grpo_op op_flags, grpo_dtype dt, int64_t N, int64_t H, int64_t V,
                             int64_t num_seqs, int64_t max_valid, size_t dz_budget) {
+  const bool tiled_weight = ((int)op_flags & GRPO_WS_TILED_WEIGHT) != 0;
+  const grpo_op op = (grpo_op)((int)op_flags & ~GRPO_WS_TILED_WEIGHT);
   if (op != GRPO_OP_LOGPROB_FWD && op != GRPO_OP_LOSS_FWD_BWD && op != GRPO_OP_SFT_FWD_BWD)
     return 0;
+  if (tiled_weight && dt != GRPO_BF16) return 0;
   if (check_sizes(dt, N, H, V) != GRPO_OK || num_seqs < 1) return 0;
   if (max_valid < 0 || max_valid > N) return 0;
   if (op != GRPO_OP_LOGPROB_FWD && check_bwd_sizes(dt, N, H, V) != GRPO_OK) return 0;
   if (op == GRPO_OP_SFT_FWD_BWD)
-    return layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, 1, max_valid, dz_budget).total;
-  return layout(op, dt, N, H, V, num_seqs, max_valid, dz_budget).total;
+    return layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, 1, max_valid, dz_budget, tiled_weight).total;
+  return layout(op, dt, N, H, V, num_seqs, max_valid, dz_budget, tiled_weight).total;
+}
+
+size_t grpo_weight_tiled_bytes(int64_t V, int64_t H) {
+  if (check_sizes(GRPO_BF16, 1, H, V) != GRPO_OK) return 0;
+  return (size_t)2 * round_up(V, kTile) * tile_stride(H) * kBK;
+}
+
+grpo_status grpo_tile_weight(const void* weight, int64_t V, int64_t H, void* out,
+                             size_t out_bytes, hipStream_t stream) {
+  TRY(check_sizes(GRPO_BF16, 1, H, V));
+  if (!weight || !out) return GRPO_ERR_NULL;
+  if (!aligned(weight, 16) || !aligned(out, kAlign)) return GRPO_ERR_ALIGN;
+  if (out_bytes < grpo_weight_tiled_bytes(V, H)) return GRPO_ERR_SHAPE;
+  TRY(check_device());
+  return timed(K_TILE, stream, [&] {
+    launch_tile_rows((const uint16_t*)weight, H, nullptr, V, nullptr, round_up(V, kTile), H,
+                     tile_stride(H), (uint16_t*)out, stream);
+  });
 }
 
 grpo_status group_advantages(const float* rewards, int64_t num_prompts, int32_t group_size,
@@ -694,16 +734,19 @@ grpo_status grpo_pack_valid_static(const uint8_t* mask, const int64_t* cu_seqlen
 }
 
 grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weight,
-                             const int64_t* tokens, const uint8_t* mask, int64_t N, int64_t H,
-                             int64_t V, float* logp, float* lse, void* workspace,
-                             size_t workspace_bytes, int64_t max_valid, hipStream_t stream) {
+                             const void* weight_tiled, const int64_t* tokens,
+                             const uint8_t* mask, int64_t N, int64_t H, int64_t V, float* logp,
+                             float* lse, void* workspace, size_t workspace_bytes,
+                             int64_t max_valid, hipStream_t stream) {
   TRY(check_sizes(dt, N, H, V));
   if (max_valid < 0 || max_valid > N) return GRPO_ERR_SHAPE;
   if (!hidden || !weight || !tokens) return GRPO_ERR_NULL;
   size_t al = dt == GRPO_BF16 ? 16 : 4;
   if (!aligned(hidden, al) || !aligned(weight, al) || !aligned(tokens, 8)) return GRPO_ERR_ALIGN;
   if ((logp && !aligned(logp, 4)) || (lse && !aligned(lse, 4))) return GRPO_ERR_ALIGN;
-  Layout L = layout(GRPO_OP_LOGPROB_FWD, dt, N, H, V, 1, max_valid, 0);
+  TRY(check_weight_tiled(dt, weight_tiled));
+  Layout L = layout(GRPO_OP_LOGPROB_FWD, dt, N, H, V, 1, max_valid, 0, weight_tiled != nullptr);
+  L.WKx = (const uint16_t*)weight_tiled;
   TRY(check_ws(workspace, workspace_bytes, L));
   TRY(check_device());
   // one "rollout" covering every row (cu_seqlens = NULL means {0, N})
@@ -720,9 +763,10 @@ grpo_status grpo_logprob_fwd(grpo_dtype dt, const void* hidden, const void* weig
 }
 
 grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight,
-                              const int64_t* tokens, const uint8_t* mask,
-                              const int64_t* cu_seqlens, int64_t num_seqs, int64_t N, int64_t H,
-                              int64_t V, const float* old_logp, const float* ref_logp,
+                              const void* weight_tiled, const int64_t* tokens,
+                              const uint8_t* mask, const int64_t* cu_seqlens,
+                              int64_t num_seqs, int64_t N, int64_t H, int64_t V,
+                              const float* old_logp, const float* ref_logp,
                               const float* adv, float clip_eps, float beta, grpo_agg agg,
                               const float* lse_in, float* loss, float* logp_out, float* lse_out,
                               float* token_loss, float* dlogp, uint8_t* clip_flag,
@@ -751,7 +795,10 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
   for (const void* p : {(const void*)ref_logp, (const void*)lse_in, (const void*)logp_out,
                         (const void*)lse_out, (const void*)token_loss, (const void*)dlogp})
     if (p && !aligned(p, 4)) return GRPO_ERR_ALIGN;
-  Layout L = layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, num_seqs, max_valid, dz_budget);
+  TRY(check_weight_tiled(dt, weight_tiled));
+  Layout L = layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, num_seqs, max_valid, dz_budget,
+                    weight_tiled != nullptr);
+  L.WKx = (const uint16_t*)weight_tiled;
   TRY(check_ws(workspace, workspace_bytes, L));
   TRY(check_device());
 
@@ -820,9 +867,9 @@ grpo_status grpo_loss_fwd_bwd(grpo_dtype dt, const void* hidden, const void* wei
 }
 
 grpo_status sft_ce_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight,
-                           const int64_t* tokens, const uint8_t* mask, int64_t N, int64_t H,
-                           int64_t V, float* loss, float* logp_out, void* grad_hidden,
-                           grpo_dtype grad_hidden_dt, float* grad_weight,
+                           const void* weight_tiled, const int64_t* tokens, const uint8_t* mask,
+                           int64_t N, int64_t H, int64_t V, float* loss, float* logp_out,
+                           void* grad_hidden, grpo_dtype grad_hidden_dt, float* grad_weight,
                            int32_t accumulate_grad_weight, void* workspace,
                            size_t workspace_bytes, int64_t max_valid, size_t dz_budget,
                            hipStream_t stream) {
@@ -838,7 +885,10 @@ grpo_status sft_ce_fwd_bwd(grpo_dtype dt, const void* hidden, const void* weight
   if ((logp_out && !aligned(logp_out, 4)) || (grad_hidden && !aligned(grad_hidden, 4)) ||
       (grad_weight && !aligned(grad_weight, 4)))
     return GRPO_ERR_ALIGN;
-  Layout L = layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, 1, max_valid, dz_budget);
+  TRY(check_weight_tiled(dt, weight_tiled));
+  Layout L = layout(GRPO_OP_LOSS_FWD_BWD, dt, N, H, V, 1, max_valid, dz_budget,
+                    weight_tiled != nullptr);
+  L.WKx = (const uint16_t*)weight_tiled;
   TRY(check_ws(workspace, workspace_bytes, L));
   TRY(check_device());
   void* ws = workspace;

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libgrpo.so")
 F32, BF16 = 0, 1
 AGG_SEQ_MEAN, AGG_TOKEN_MEAN = 0, 1
 OP_LOGPROB_FWD, OP_LOSS_FWD_BWD, OP_SFT_FWD_BWD = 0, 1, 2
+WS_TILED_WEIGHT = 0x100  # OR-ed into an op: the call is given a tiled weight
 
 STATUS = {0: "GRPO_OK", 1: "GRPO_ERR_NULL", 2: "GRPO_ERR_SHAPE", 3: "GRPO_ERR_DTYPE",
           4: "GRPO_ERR_PARAM", 5: "GRPO_ERR_ALIGN", 6: "GRPO_ERR_WORKSPACE",
@@ -32,18 +33,20 @@ SIGNATURES = {
     "group_advantages": (_i32, [_vp, _i64, _i32, _f32, _i32, _vp, _vp]),
     "grpo_pack_valid": (_i32, [_vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _sz, _vp]),
     "grpo_pack_valid_static": (_i32, [_vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp]),
-    "grpo_logprob_fwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp, _sz,
-                                _i64, _vp]),
-    "grpo_loss_fwd_bwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _vp, _vp,
-                                 _vp, _f32, _f32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
-                                 _i32, _vp, _i32, _vp, _sz, _i64, _sz, _vp]),
-    "sft_ce_fwd_bwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp, _i32,
-                              _vp, _i32, _vp, _sz, _i64, _sz, _vp]),
+    "grpo_logprob_fwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp,
+                                _sz, _i64, _vp]),
+    "grpo_loss_fwd_bwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _vp,
+                                 _vp, _vp, _f32, _f32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                 _vp, _i32, _vp, _i32, _vp, _sz, _i64, _sz, _vp]),
+    "sft_ce_fwd_bwd": (_i32, [_i32, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp,
+                              _i32, _vp, _i32, _vp, _sz, _i64, _sz, _vp]),
     "adamw_step": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _f32, _f32, _f32, _f32, _f32, _i64,
                           _vp]),
     "triton_rule_reward": (_i32, [_vp, _i64, _vp, _i64, _vp, _i32, _i32, _f32, _f32, _vp, _vp,
                                _vp]),
     "grpo_workspace_bytes": (_sz, [_i32, _i32, _i64, _i64, _i64, _i64, _i64, _sz]),
+    "grpo_weight_tiled_bytes": (_sz, [_i64, _i64]),
+    "grpo_tile_weight": (_i32, [_vp, _i64, _i64, _vp, _sz, _vp]),
     "grpo_check_error": (_i32, [_vp, _vp]),
     "grpo_status_string": (ctypes.c_char_p, [_i32]),
     "grpo_profile_enable": (None, [_i32]),
@@ -181,6 +184,47 @@ def free_workspace():
     _ws_cache.clear()
 
 
+class TiledWeight:
+    """A bf16 head weight [V, H] in the library's tiled operand layout
+    (grpo_tile_weight), for calls that share one W: pass it as weight_tiled
+    together with the same weight. It is only valid while W is unchanged."""
+
+    def __init__(self, buf: torch.Tensor, V: int, H: int):
+        self.buf, self.V, self.H = buf, V, H  # buf: 256-byte-aligned uint8 view
+
+
+@_on_tensor_device
+def tile_weight(weight: torch.Tensor) -> TiledWeight:
+    """grpo_tile_weight: W [V, H] bf16 -> a TiledWeight on W's device and stream."""
+    _need(weight, "weight", torch.bfloat16)
+    if weight.dim() != 2:
+        raise ValueError("weight must be 2-D [V, H]")
+    V, H = weight.shape
+    nbytes = int(load().grpo_weight_tiled_bytes(V, H))
+    if nbytes == 0:
+        raise ValueError(f"weight shape {(V, H)} is outside the library's limits")
+    raw = torch.empty(nbytes + 256, dtype=torch.uint8, device=weight.device)
+    off = (-raw.data_ptr()) % 256
+    buf = raw[off:off + nbytes]
+    st = load().grpo_tile_weight(_ptr(weight), V, H, _ptr(buf), nbytes, _stream())
+    _check(st, "grpo_tile_weight")
+    return TiledWeight(buf, V, H)
+
+
+def _tiled(weight_tiled, weight) -> tuple:
+    """(pointer, op flag) for an optional TiledWeight matching weight."""
+    if weight_tiled is None:
+        return None, 0
+    if not isinstance(weight_tiled, TiledWeight):
+        raise TypeError("weight_tiled must come from tile_weight()")
+    if (weight_tiled.V, weight_tiled.H) != tuple(weight.shape) or weight.dtype != torch.bfloat16:
+        raise ValueError(f"weight_tiled is for a bf16 [{weight_tiled.V}, {weight_tiled.H}] "
+                         f"weight, the call's weight is {weight.dtype} {tuple(weight.shape)}")
+    if weight_tiled.buf.device != weight.device:
+        raise ValueError("weight_tiled is on another device than weight")
+    return _ptr(weight_tiled.buf), WS_TILED_WEIGHT
+
+
 # ------------------------------------------------------------ entry points
 @_on_tensor_device
 def group_advantages(rewards: torch.Tensor, group_size: int, std_eps: float = 1e-6,
@@ -222,9 +266,11 @@ def pack_valid(mask: torch.Tensor | None, cu_seqlens: torch.Tensor):
 
 @_on_tensor_device
 def logprob_fwd(hidden: torch.Tensor, weight: torch.Tensor, tokens: torch.Tensor,
-                mask: torch.Tensor | None = None, check: bool = False, max_valid: int = 0):
+                mask: torch.Tensor | None = None, check: bool = False, max_valid: int = 0,
+                weight_tiled: TiledWeight | None = None):
     """Per-token log-prob and log-sum-exp over the vocabulary: (logp, lse), fp32 [N].
-    max_valid: the most valid rows the mask has (0: N), which sizes the workspace."""
+    max_valid: the most valid rows the mask has (0: N), which sizes the workspace;
+    weight_tiled: tile_weight(weight), to skip tiling W in this call."""
     _need(hidden, "hidden")
     _need(weight, "weight", hidden.dtype)
     _need(tokens, "tokens", torch.int64)
@@ -235,10 +281,12 @@ def logprob_fwd(hidden: torch.Tensor, weight: torch.Tensor, tokens: torch.Tensor
     dt = _dt(hidden)
     logp = torch.empty(N, dtype=torch.float32, device=hidden.device)
     lse = torch.empty(N, dtype=torch.float32, device=hidden.device)
-    ws = workspace(workspace_bytes(OP_LOGPROB_FWD, dt, N, H, V, 1, max_valid), hidden.device)
+    wt, flag = _tiled(weight_tiled, weight)
+    ws = workspace(workspace_bytes(OP_LOGPROB_FWD | flag, dt, N, H, V, 1, max_valid),
+                   hidden.device)
     m = None if mask is None else _need(mask, "mask").view(torch.uint8)
-    st = load().grpo_logprob_fwd(dt, _ptr(hidden), _ptr(weight), _ptr(tokens), _ptr(m), N, H, V,
-                                 _ptr(logp), _ptr(lse), _ptr(ws), ws.numel(), max_valid,
+    st = load().grpo_logprob_fwd(dt, _ptr(hidden), _ptr(weight), wt, _ptr(tokens), _ptr(m), N,
+                                 H, V, _ptr(logp), _ptr(lse), _ptr(ws), ws.numel(), max_valid,
                                  _stream())
     _check(st, "grpo_logprob_fwd")
     if check:
@@ -252,11 +300,13 @@ def loss_fwd_bwd(hidden, weight, tokens, mask, cu_seqlens, old_logp, ref_logp, a
                  lse_in=None, grad_hidden: bool = True, grad_weight: bool = True,
                  grad_hidden_dtype=None, grad_weight_out: torch.Tensor | None = None,
                  accumulate_grad_weight: bool = False, token_outputs: bool = True,
-                 check: bool = False, max_valid: int = 0, dz_budget: int = 0) -> dict:
+                 check: bool = False, max_valid: int = 0, dz_budget: int = 0,
+                 weight_tiled: TiledWeight | None = None) -> dict:
     """GRPO loss (Eq. 1, k3 KL) and its gradients. Returns a dict of tensors:
     loss [1], logp/lse/token_loss/dlogp [N], clip_flag uint8 [N],
     grad_hidden [N,H], grad_weight [V,H] fp32 (as requested). max_valid (0: N)
-    and dz_budget (bytes, 0: default) size the workspace (see grpo.h)."""
+    and dz_budget (bytes, 0: default) size the workspace (see grpo.h);
+    weight_tiled: tile_weight(weight), to skip tiling W in this call."""
     _need(hidden, "hidden")
     _need(weight, "weight", hidden.dtype)
     _need(tokens, "tokens", torch.int64)
@@ -294,11 +344,13 @@ def loss_fwd_bwd(hidden, weight, tokens, mask, cu_seqlens, old_logp, ref_logp, a
                                                torch.float32), "grad_weight_out", V, H)
         else:
             out["grad_weight"] = torch.empty(V, H, **f32)
-    ws = workspace(workspace_bytes(OP_LOSS_FWD_BWD, dt, N, H, V, B, max_valid, dz_budget), dev)
+    wt, flag = _tiled(weight_tiled, weight)
+    ws = workspace(workspace_bytes(OP_LOSS_FWD_BWD | flag, dt, N, H, V, B, max_valid, dz_budget),
+                   dev)
     m = None if mask is None else _need(mask, "mask").view(torch.uint8)
     g = out.get
     st = load().grpo_loss_fwd_bwd(
-        dt, _ptr(hidden), _ptr(weight), _ptr(tokens), _ptr(m), _ptr(cu_seqlens), B, N, H, V,
+        dt, _ptr(hidden), _ptr(weight), wt, _ptr(tokens), _ptr(m), _ptr(cu_seqlens), B, N, H, V,
         _ptr(old_logp), _ptr(ref_logp), _ptr(adv), clip_eps, beta, agg, _ptr(lse_in),
         _ptr(out["loss"]), _ptr(g("logp")), _ptr(g("lse")), _ptr(g("token_loss")),
         _ptr(g("dlogp")), _ptr(g("clip_flag")), _ptr(g("grad_hidden")),
@@ -315,9 +367,11 @@ def sft_ce_fwd_bwd(hidden, weight, tokens, mask=None, grad_hidden: bool = True,
                    grad_weight: bool = True, grad_hidden_dtype=None,
                    grad_weight_out: torch.Tensor | None = None,
                    accumulate_grad_weight: bool = False, logp_out: bool = True,
-                   check: bool = False, max_valid: int = 0, dz_budget: int = 0) -> dict:
+                   check: bool = False, max_valid: int = 0, dz_budget: int = 0,
+                   weight_tiled: TiledWeight | None = None) -> dict:
     """SFT next-token cross-entropy (mean over supervised tokens) and its gradients.
-    Returns loss [1], logp [N] (if logp_out), grad_hidden [N,H], grad_weight [V,H] fp32."""
+    Returns loss [1], logp [N] (if logp_out), grad_hidden [N,H], grad_weight [V,H] fp32;
+    weight_tiled: tile_weight(weight), to skip tiling W in this call."""
     _need(hidden, "hidden")
     _need(weight, "weight", hidden.dtype)
     _need(tokens, "tokens", torch.int64)
@@ -340,11 +394,13 @@ def sft_ce_fwd_bwd(hidden, weight, tokens, mask=None, grad_hidden: bool = True,
                                                torch.float32), "grad_weight_out", V, H)
         else:
             out["grad_weight"] = torch.empty(V, H, **f32)
-    ws = workspace(workspace_bytes(OP_SFT_FWD_BWD, dt, N, H, V, 1, max_valid, dz_budget), dev)
+    wt, flag = _tiled(weight_tiled, weight)
+    ws = workspace(workspace_bytes(OP_SFT_FWD_BWD | flag, dt, N, H, V, 1, max_valid, dz_budget),
+                   dev)
     m = None if mask is None else _need(mask, "mask").view(torch.uint8)
     g = out.get
     st = load().sft_ce_fwd_bwd(
-        dt, _ptr(hidden), _ptr(weight), _ptr(tokens), _ptr(m), N, H, V, _ptr(out["loss"]),
+        dt, _ptr(hidden), _ptr(weight), wt, _ptr(tokens), _ptr(m), N, H, V, _ptr(out["loss"]),
         _ptr(g("logp")), _ptr(g("grad_hidden")),
         _dt(out["grad_hidden"]) if grad_hidden else F32, _ptr(g("grad_weight")),
         int(accumulate_grad_weight), _ptr(ws), ws.numel(), max_valid, dz_budget, _stream())

@@ -32,7 +32,7 @@ def test_header_declares_the_boundary():
     names = _declared_functions()
     for required in ("group_advantages", "grpo_logprob_fwd", "grpo_loss_fwd_bwd",
                      "sft_ce_fwd_bwd", "adamw_step", "triton_rule_reward", "grpo_pack_valid",
-                     "grpo_workspace_bytes",
+                     "grpo_workspace_bytes", "grpo_tile_weight", "grpo_weight_tiled_bytes",
                      "grpo_check_error", "grpo_status_string"):
         assert required in names
 
@@ -94,7 +94,7 @@ P = ctypes.c_void_p(0x1000)  # a non-NULL, 256-byte-aligned dummy (never derefer
 
 
 def _loss(lib, **kw):
-    a = dict(dt=1, hidden=P, weight=P, tokens=P, mask=NULL, cu=P, B=2, N=8, H=64, V=100,
+    a = dict(dt=1, hidden=P, weight=P, wt=NULL, tokens=P, mask=NULL, cu=P, B=2, N=8, H=64, V=100,
              old=P, ref=P, adv=P, eps=0.2, beta=0.01, agg=0, lse_in=NULL, loss=P, logp=NULL,
              lse=NULL, tl=NULL, dlogp=NULL, clip=NULL, gh=NULL, gh_dt=1, gw=NULL, acc=0,
              ws=NULL, ws_bytes=0, max_valid=0, dz_budget=0, stream=NULL)
@@ -138,15 +138,15 @@ def test_other_entry_point_errors(lib):
     # one wave per prompt: the grid's thread count must stay below 2^32
     assert adv(P, 4 * ((1 << 24) - 1) + 1, 2, 1e-6, 1, P, NULL) == 2
     fwd = lib.grpo_logprob_fwd
-    assert fwd(1, NULL, P, P, NULL, 8, 64, 100, P, P, P, 1 << 30, 0, NULL) == 1
-    assert fwd(1, P, P, P, NULL, 8, 12, 100, P, P, P, 1 << 30, 0, NULL) == 2
-    assert fwd(1, P, P, P, NULL, 8, 64, 0, P, P, P, 1 << 30, 0, NULL) == 2
-    assert fwd(2, P, P, P, NULL, 8, 64, 100, P, P, P, 1 << 30, 0, NULL) == 3
-    assert fwd(1, P, P, P, NULL, 8, 64, 100, P, P, P, 8, 0, NULL) == 6
+    assert fwd(1, NULL, P, NULL, P, NULL, 8, 64, 100, P, P, P, 1 << 30, 0, NULL) == 1
+    assert fwd(1, P, P, NULL, P, NULL, 8, 12, 100, P, P, P, 1 << 30, 0, NULL) == 2
+    assert fwd(1, P, P, NULL, P, NULL, 8, 64, 0, P, P, P, 1 << 30, 0, NULL) == 2
+    assert fwd(2, P, P, NULL, P, NULL, 8, 64, 100, P, P, P, 1 << 30, 0, NULL) == 3
+    assert fwd(1, P, P, NULL, P, NULL, 8, 64, 100, P, P, P, 8, 0, NULL) == 6
     # bf16 scoring grid beyond 32 bits; fp32 H beyond its LDS rows
-    assert fwd(1, P, P, P, NULL, 1 << 22, 8, (1 << 31) - 512, P, P, P, 1 << 30, 0, NULL) == 2
-    assert fwd(0, P, P, P, NULL, 8, 8200, 100, P, P, P, 1 << 30, 0, NULL) == 2
-    assert fwd(1, P, P, P, NULL, 8, 64, 100, P, P, P, 1 << 30, 9, NULL) == 2
+    assert fwd(1, P, P, NULL, P, NULL, 1 << 22, 8, (1 << 31) - 512, P, P, P, 1 << 30, 0, NULL) == 2
+    assert fwd(0, P, P, NULL, P, NULL, 8, 8200, 100, P, P, P, 1 << 30, 0, NULL) == 2
+    assert fwd(1, P, P, NULL, P, NULL, 8, 64, 100, P, P, P, 1 << 30, 9, NULL) == 2
     pk = lib.grpo_pack_valid
     assert pk(NULL, NULL, 2, 8, P, P, P, P, 1 << 30, NULL) == 1
     assert pk(NULL, P, 0, 8, P, P, P, P, 1 << 30, NULL) == 2
@@ -154,8 +154,47 @@ def test_other_entry_point_errors(lib):
     assert lib.grpo_check_error(NULL, NULL) == 1
 
 
+def test_tiled_weight_host_checks(lib):
+    tb = lib.grpo_weight_tiled_bytes
+    # 256-row x 32-column bf16 blocks, ceil(H/32) + 1 blocks per tile-row
+    assert tb(100, 64) == 2 * 256 * (2 + 1) * 32
+    assert tb(155136, 4096) == 2 * 155136 * (128 + 1) * 32
+    assert tb(257, 8) == 2 * 512 * 2 * 32
+    assert tb(0, 64) == 0 and tb(100, 60) == 0 and tb(100, 1 << 20) == 0
+    # a workspace for a call given the tiled weight holds no copy of it
+    flag = 0x100
+    for op, B in ((0, 1), (1, 4), (2, 1)):
+        full = lib.grpo_workspace_bytes(op, 1, 1000, 4096, 155136, B, 0, 0)
+        lean = lib.grpo_workspace_bytes(op | flag, 1, 1000, 4096, 155136, B, 0, 0)
+        assert full - lean == tb(155136, 4096), op
+    assert lib.grpo_workspace_bytes(0 | flag, 0, 1000, 64, 1000, 1, 0, 0) == 0  # bf16 only
+    tile = lib.grpo_tile_weight
+    big = 1 << 40
+    assert tile(NULL, 100, 64, P, big, NULL) == 1
+    assert tile(P, 100, 64, NULL, big, NULL) == 1
+    assert tile(P, 100, 60, P, big, NULL) == 2
+    assert tile(P, 0, 64, P, big, NULL) == 2
+    assert tile(P, 100, 64, P, tb(100, 64) - 1, NULL) == 2    # out too small
+    assert tile(ctypes.c_void_p(0x1008), 100, 64, P, big, NULL) == 5
+    assert tile(P, 100, 64, ctypes.c_void_p(0x1010), big, NULL) == 5
+    # the compute calls: bf16 only, 256-byte aligned; the lean workspace needs it
+    fwd = lib.grpo_logprob_fwd
+    assert fwd(0, P, P, P, P, NULL, 8, 64, 100, P, P, P, 1 << 30, 0, NULL) == 3
+    assert fwd(1, P, P, ctypes.c_void_p(0x1010), P, NULL, 8, 64, 100, P, P, P, 1 << 30, 0,
+               NULL) == 5
+    lean = lib.grpo_workspace_bytes(0 | flag, 1, 8, 64, 100, 1, 0, 0)
+    assert fwd(1, P, P, NULL, P, NULL, 8, 64, 100, P, P, P, lean, 0, NULL) == 6
+    assert _loss(lib, dt=0, wt=P) == 3
+    assert _loss(lib, wt=ctypes.c_void_p(0x1040)) == 5
+    lean = lib.grpo_workspace_bytes(1 | flag, 1, 8, 64, 100, 2, 0, 0)
+    assert _loss(lib, ws=P, ws_bytes=lean) == 6
+    assert _sft(lib, dt=0, wt=P) == 3
+    lean = lib.grpo_workspace_bytes(2 | flag, 1, 8, 64, 100, 1, 0, 0)
+    assert _sft(lib, ws=P, ws_bytes=lean) == 6
+
+
 def _sft(lib, **kw):
-    a = dict(dt=1, hidden=P, weight=P, tokens=P, mask=NULL, N=8, H=64, V=100, loss=P,
+    a = dict(dt=1, hidden=P, weight=P, wt=NULL, tokens=P, mask=NULL, N=8, H=64, V=100, loss=P,
              logp=NULL, gh=NULL, gh_dt=1, gw=NULL, acc=0, ws=NULL, ws_bytes=0, max_valid=0,
              dz_budget=0, stream=NULL)
     a.update(kw)

@@ -314,6 +314,39 @@ def test_deterministic_bits():
         assert torch.equal(a[k], c[k]), k
 
 
+@pytest.mark.parametrize("case", ["ragged_tiles", "multi_chunk"])
+def test_tiled_weight_gives_the_same_bits(case):
+    # grpo_tile_weight once, then every bf16 entry point given the tiled copy:
+    # the same bits as the calls that tile W themselves, with the workspace
+    # sized without the copy
+    kw = dict(SMALL[case], dtype="bf16", rms_norm_hidden=True, beta=0.01, noise_sigma=0.1,
+              seed=17)
+    w, W, h, b, adv, old, ref = _problem("fwdbwd_bf16", **kw)
+    Wd, hd = to_dev(W, "bf16"), to_dev(h, "bf16")
+    wt = grpo.tile_weight(Wd)
+    grpo.free_workspace()
+    a = grpo.logprob_fwd(hd, Wd, dev(b["tokens"]), dev(b["mask"]))
+    c = grpo.logprob_fwd(hd, Wd, dev(b["tokens"]), dev(b["mask"]), weight_tiled=wt)
+    assert torch.equal(a[0], c[0]) and torch.equal(a[1], c[1])
+    a = _run_loss(w, W, h, b, adv, old, ref)
+    c = _run_loss(w, W, h, b, adv, old, ref, weight_tiled=wt)
+    for k in ("loss", "logp", "lse", "dlogp", "clip_flag", "grad_hidden", "grad_weight"):
+        assert torch.equal(a[k], c[k]), k
+    # the double-scoring path (lse_in): the gradients read the tiled copy
+    lse = a["lse"]
+    a = _run_loss(w, W, h, b, adv, old, ref, lse_in=lse)
+    c = _run_loss(w, W, h, b, adv, old, ref, lse_in=lse, weight_tiled=wt)
+    for k in ("loss", "logp", "grad_hidden", "grad_weight"):
+        assert torch.equal(a[k], c[k]), k
+    a = grpo.sft_ce_fwd_bwd(hd, Wd, dev(b["tokens"]), dev(b["mask"]))
+    c = grpo.sft_ce_fwd_bwd(hd, Wd, dev(b["tokens"]), dev(b["mask"]), weight_tiled=wt)
+    for k in ("loss", "logp", "grad_hidden", "grad_weight"):
+        assert torch.equal(a[k], c[k]), k
+    # a copy of another weight's shape is refused by the binding
+    with pytest.raises(ValueError):
+        grpo.logprob_fwd(hd, Wd[:-1].contiguous(), dev(b["tokens"]), weight_tiled=wt)
+
+
 def test_side_stream_and_workspace_per_stream():
     # the binding launches on the caller's current stream, with a workspace of
     # that stream's own; a side stream gives the same bits as the default one
