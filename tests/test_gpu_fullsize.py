@@ -351,7 +351,9 @@ def test_ragged_full_size_sampled_rows_and_identities():
 def test_double_scoring_full_size_sampled_rows():
     """The two-model sequence at full size (16 x 8 x 2048 tokens, N = 262144):
     policy and reference scoring, then the loss on the policy reusing its
-    log-sum-exp; sampled rows against the oracle and the on-policy ratio."""
+    log-sum-exp; sampled rows against the oracle and the on-policy ratio. As
+    bench.py runs it, each W is tiled once (grpo_tile_weight) and every call
+    reads the tiled copy."""
     w = workloads.WORKLOADS["double_bf16"]
     Wp, Wr = workloads.make_weight(w, "policy"), workloads.make_weight(w, "reference")
     h_bits, b = workloads.make_hidden(w), workloads.make_batch(w)
@@ -361,8 +363,10 @@ def test_double_scoring_full_size_sampled_rows():
     del h_bits
     Wpd, Wrd = to_dev(Wp, "bf16"), to_dev(Wr, "bf16")
     y = dev(b["tokens"])
-    lp_pol, lse_pol = grpo.logprob_fwd(hd, Wpd, y)
-    lp_ref, _ = grpo.logprob_fwd(hd, Wrd, y)
+    wt_pol, wt_ref = grpo.tile_weight(Wpd), grpo.tile_weight(Wrd)
+    lp_pol, lse_pol = grpo.logprob_fwd(hd, Wpd, y, weight_tiled=wt_pol)
+    lp_ref, _ = grpo.logprob_fwd(hd, Wrd, y, weight_tiled=wt_ref)
+    del wt_ref
     Wpo = oracle.decode(Wp, "bf16")
     o_lse_p, o_lp_p, _ = oracle.score_rows(hs, Wpo, b["tokens"][rows])
     _, o_lp_r, _ = oracle.score_rows(hs, oracle.decode(Wr, "bf16"), b["tokens"][rows])
@@ -370,8 +374,9 @@ def test_double_scoring_full_size_sampled_rows():
     assert rel_err(host64(lp_ref)[rows], o_lp_r) <= TOL
     adv = oracle.advantages(b["rewards"], w.group).astype(np.float32)
     out = grpo.loss_fwd_bwd(hd, Wpd, y, None, dev(b["cu_seqlens"]), lp_pol, lp_ref, dev(adv),
-                            w.clip_eps, w.beta, lse_in=lse_pol, check=True)
+                            w.clip_eps, w.beta, lse_in=lse_pol, check=True, weight_tiled=wt_pol)
     torch.cuda.synchronize()
+    del wt_pol
     # on policy: old = the policy's own log-prob, so rho = 1 up to the
     # difference between the gathered z_y of the two calls (the reused-lse
     # path takes z_y from a dot product, the scoring call from its GEMM)
