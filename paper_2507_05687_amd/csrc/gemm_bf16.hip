@@ -22,9 +22,11 @@
 // kGM tile-rows and walks the tile-columns in blocks of kGN, and all 8 XCDs
 // walk the same columns at the same time: the B operand is then shared
 // through the last-level cache and each XCD's L2 sees only kGM + kGN
-// distinct operand slices per K step. Products with fewer than 8 kGM
-// tile-rows split the valid tile-columns among the XCDs instead. A product
-// may also split K over the grid's y dimension (partial sums to a buffer).
+// distinct operand slices per K step. Tile-rows after the last whole group
+// of 8 bands are shared out evenly over the XCDs; products with fewer than
+// 8 kGM tile-rows split the valid tile-columns among the XCDs instead. A
+// product may also split K over the grid's y dimension (partial sums to a
+// buffer).
 #include "kernels.h"
 
 namespace grpo {
