@@ -161,7 +161,8 @@ def main():
     prop = torch.cuda.get_device_properties(0)
     cmd = ("rocprofv3 --kernel-trace -d <raw> -o vsb -- python -m paper_2507_05687_amd.vs_hipblaslt "
            + " ".join(sys.argv[1:]) + "; python -m paper_2507_05687_amd.vs_hipblaslt --kernels-from <raw>")
-    lines = [f"# scoring product vs hipBLASLt (torch.matmul W @ h^T), V={V}, H={H}, bf16",
+    lines = [f"# GEMM products vs hipBLASLt's plain GEMMs of their shapes (torch.matmul), "
+             f"V={V}, H={H}, bf16",
              f"# command: {cmd}",
              f"# device: {prop.gcnArchName}, {prop.multi_processor_count} CUs, "
              f"{prop.total_memory / 2**30:.0f} GiB; torch {torch.__version__}",
