@@ -197,6 +197,8 @@ SMALL = {
     "uneven_row_bands": dict(prompts=3, group=4, seq_len=960, hidden=512, vocab=700),
     # 37 token tile-rows: the 5 after the whole bands split by columns over the XCDs
     "few_rows_after_bands": dict(prompts=1, group=8, seq_len=1184, hidden=512, vocab=700),
+    # the scoring product launched per 8192 vocabulary rows: a last launch of one row
+    "one_row_last_scoring_chunk": dict(prompts=2, group=4, seq_len=40, hidden=64, vocab=8193),
 }
 
 
