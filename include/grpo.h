@@ -44,7 +44,8 @@
  *    dL/dhidden accumulator: the gradients are then summed in another
  *    grouping (equal up to fp32 rounding; the same arguments always give the
  *    same bits). Pass the same values to grpo_workspace_bytes and to the
- *    call.
+ *    call, with GRPO_WS_TILED_WEIGHT in the op when the call is given a
+ *    tiled weight (grpo_tile_weight): the workspace then holds no copy of W.
  */
 #ifndef GRPO_H_
 #define GRPO_H_
