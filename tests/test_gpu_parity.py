@@ -316,7 +316,7 @@ def test_deterministic_bits():
         assert torch.equal(a[k], c[k]), k
 
 
-@pytest.mark.parametrize("case", ["ragged_tiles", "multi_chunk"])
+@pytest.mark.parametrize("case", ["ragged_tiles", "multi_chunk", "k_tail"])
 def test_tiled_weight_gives_the_same_bits(case):
     # grpo_tile_weight once, then every bf16 entry point given the tiled copy:
     # the same bits as the calls that tile W themselves, with the workspace
